@@ -1,0 +1,455 @@
+/*
+ * kvx_oracle.c -- plain CPU oracle of the KV-cache conversion performed by the
+ * heterogeneous compatible transmission module (paper Sec. III-B).
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg, never by the GPU library.
+ *
+ * What is computed, and where it comes from:
+ *   - parallel-strategy alignment (Sec. III-B-3 and Fig. 4): a decode rank's
+ *     heads are one contiguous range of the global KV heads, and the prefill
+ *     ranks that overlap that range are merged (src TP > dst TP) or split
+ *     (src TP < dst TP), as in the TP=4 -> TP=2 example of that subsection;
+ *   - VRAM-management alignment (Sec. III-B-2 and Fig. 5): the prefill side's
+ *     layout is flattened into a one-dimensional transfer tensor and then
+ *     restored into the decode side's paged cache with its own page (block)
+ *     size and layout;
+ *   - precision alignment (named among the module's components in Sec. I):
+ *     the decode side's element type.  The paper gives no rounding rule; the
+ *     reading taken is IEEE round-to-nearest-even, and for the 8-bit e4m3fn
+ *     format a per-(token, head) scale max|x|/448 in fp32 with a saturating
+ *     cast.
+ *
+ * Casts are written from the format definitions: decode the bits to an exact
+ * real value (double), round that value to the nearest point of the target
+ * grid with ties to even, encode.  No bit tricks.
+ *
+ * Build: plain C99, no fast-math, no contraction (-ffp-contract=off), so the
+ * one fp32 divide of the e4m3 path is the IEEE correctly rounded divide.
+ */
+#include "kvx_oracle.h"
+
+#include <fenv.h>
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ */
+/* formats                                                              */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    int total_bits;  /* storage width */
+    int exp_bits;
+    int man_bits;    /* stored fraction bits */
+    int bias;
+} orc_fmt_desc;
+
+static orc_fmt_desc fmt_desc(int fmt)
+{
+    orc_fmt_desc f;
+    switch (fmt) {
+    case ORC_FP16:   f.total_bits = 16; f.exp_bits = 5; f.man_bits = 10; f.bias = 15;  break;
+    case ORC_BF16:   f.total_bits = 16; f.exp_bits = 8; f.man_bits = 7;  f.bias = 127; break;
+    default:         f.total_bits = 8;  f.exp_bits = 4; f.man_bits = 3;  f.bias = 7;   break;
+    }
+    return f;
+}
+
+int orc_fmt_size(int fmt) { return fmt == ORC_E4M3FN ? 1 : 2; }
+
+/* Exact value of an encoded number.  IEEE formats (fp16, bf16): all-ones
+ * exponent is Inf (zero fraction) or NaN.  OCP e4m3fn: no Inf; only
+ * S.1111.111 is NaN, and exponent field 15 with other fractions is finite. */
+double orc_decode(int fmt, uint32_t bits)
+{
+    orc_fmt_desc f = fmt_desc(fmt);
+    uint32_t sign = (bits >> (f.total_bits - 1)) & 1u;
+    uint32_t e = (bits >> f.man_bits) & ((1u << f.exp_bits) - 1u);
+    uint32_t m = bits & ((1u << f.man_bits) - 1u);
+    uint32_t emax_field = (1u << f.exp_bits) - 1u;
+    double v;
+    if (fmt == ORC_E4M3FN) {
+        if (e == emax_field && m == ((1u << f.man_bits) - 1u))
+            return sign ? -NAN : NAN;
+    } else if (e == emax_field) {
+        if (m != 0) return sign ? -NAN : NAN;
+        return sign ? -INFINITY : INFINITY;
+    }
+    if (e == 0) /* subnormal: m * 2^(1 - bias - man_bits) */
+        v = ldexp((double)m, 1 - f.bias - f.man_bits);
+    else        /* normal: (2^man_bits + m) * 2^(e - bias - man_bits) */
+        v = ldexp((double)((1u << f.man_bits) + m), (int)e - f.bias - f.man_bits);
+    return sign ? -v : v;
+}
+
+/* Round a >= 0 (finite, exact in double) to the nearest point of the grid of
+ * a binary format with `p` significand bits and minimum normal exponent
+ * `emin`; ties go to the point with an even last significand bit.  The grid
+ * spacing in the binade [2^E, 2^(E+1)) is 2^(E-p+1); below 2^emin it is the
+ * subnormal spacing 2^(emin-p+1). */
+static double rne_to_grid(double a, int p, int emin)
+{
+    int e;
+    if (a == 0.0) return 0.0;
+    (void)frexp(a, &e);          /* a in [2^(e-1), 2^e) */
+    int E = e - 1;
+    if (E < emin) E = emin;
+    double spacing = ldexp(1.0, E - (p - 1));
+    double n = a / spacing;      /* exact: power-of-two scaling */
+    double r = nearbyint(n);     /* default mode: round half to even */
+    return r * spacing;          /* exact */
+}
+
+/* Encode a magnitude that lies on the grid (and within the finite range)
+ * with the given sign. */
+static uint32_t encode(int fmt, uint32_t sign, double mag)
+{
+    orc_fmt_desc f = fmt_desc(fmt);
+    int emin = 1 - f.bias;
+    uint32_t s = sign << (f.total_bits - 1);
+    if (mag == 0.0) return s;
+    int e;
+    (void)frexp(mag, &e);
+    int E = e - 1;
+    if (E < emin) { /* subnormal: exponent field 0, fraction = mag / 2^(emin - man_bits) */
+        double frac = ldexp(mag, -(emin - f.man_bits));
+        return s | (uint32_t)frac;
+    }
+    double frac = ldexp(mag, -(E - f.man_bits)) - ldexp(1.0, f.man_bits);
+    return s | ((uint32_t)(E + f.bias) << f.man_bits) | (uint32_t)frac;
+}
+
+/* fp16 -> bf16.  Finite values and infinities: round the exact value to the
+ * bf16 grid (8 significand bits, emin = -126), ties to even; no fp16 value
+ * can overflow bf16.  NaN (paper silent; reading taken): keep the sign, set
+ * the quiet bit, keep the top 7 fraction bits of the fp16 payload. */
+uint16_t orc_fp16_to_bf16(uint16_t h)
+{
+    uint32_t sign = (h >> 15) & 1u;
+    double x = orc_decode(ORC_FP16, h);
+    if (isnan(x))
+        return (uint16_t)((sign << 15) | 0x7F80u | 0x0040u | ((h & 0x03FFu) >> 3));
+    if (isinf(x))
+        return (uint16_t)((sign << 15) | 0x7F80u);
+    double m = rne_to_grid(fabs(x), 8, -126);
+    return (uint16_t)encode(ORC_BF16, sign, m);
+}
+
+/* fp32 -> OCP e4m3fn, round to nearest even, saturating: any magnitude whose
+ * rounding would exceed 448 (the largest finite value) gives +-448.  NaN gives
+ * the NaN code S.1111.111 with the sign kept. */
+uint8_t orc_f32_to_e4m3fn(float v)
+{
+    uint32_t sign = signbit(v) ? 1u : 0u;
+    if (isnan(v)) return (uint8_t)((sign << 7) | 0x7Fu);
+    double a = fabs((double)v);
+    if (a >= 448.0) return (uint8_t)encode(ORC_E4M3FN, sign, 448.0);
+    double m = rne_to_grid(a, 4, -6);
+    if (m > 448.0) m = 448.0; /* unreachable: a < 448 and 448 is a grid point */
+    return (uint8_t)encode(ORC_E4M3FN, sign, m);
+}
+
+/* Per-row scale: the largest magnitude over the row (NaN elements ignored),
+ * divided by 448 with one IEEE fp32 divide. */
+float orc_row_scale(const float *x, int n)
+{
+    float amax = 0.0f;
+    for (int d = 0; d < n; ++d) {
+        if (isnan(x[d])) continue;
+        float a = fabsf(x[d]);
+        if (a > amax) amax = a;
+    }
+    return amax / 448.0f;
+}
+
+void orc_fp16_to_bf16_n(const uint16_t *in, uint16_t *out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) out[k] = orc_fp16_to_bf16(in[k]);
+}
+
+void orc_f32_to_e4m3fn_n(const float *in, uint8_t *out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) out[k] = orc_f32_to_e4m3fn(in[k]);
+}
+
+void orc_decode_n(int fmt, const void *in, double *out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) {
+        uint32_t b = (fmt == ORC_E4M3FN) ? ((const uint8_t *)in)[k] : ((const uint16_t *)in)[k];
+        out[k] = orc_decode(fmt, b);
+    }
+}
+
+void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void *dst_row,
+                     float *scale)
+{
+    const uint16_t *s = (const uint16_t *)src_row;
+    if (src_fmt == dst_fmt) {               /* same type: bits unchanged */
+        memcpy(dst_row, src_row, (size_t)D * (size_t)orc_fmt_size(src_fmt));
+        return;
+    }
+    if (src_fmt == ORC_FP16 && dst_fmt == ORC_BF16) {
+        uint16_t *o = (uint16_t *)dst_row;
+        for (int d = 0; d < D; ++d) o[d] = orc_fp16_to_bf16(s[d]);
+        return;
+    }
+    /* 16-bit float -> e4m3fn with a per-row fp32 scale */
+    float *x = (float *)calloc((size_t)D, sizeof(float));
+    uint8_t *o = (uint8_t *)dst_row;
+    if (!x) abort();
+    for (int d = 0; d < D; ++d) x[d] = (float)orc_decode(src_fmt, s[d]); /* exact widening */
+    float sc = orc_row_scale(x, D);
+    *scale = sc;
+    for (int d = 0; d < D; ++d) {
+        uint32_t sign = (s[d] >> 15) & 1u;
+        if (isnan(x[d]))
+            o[d] = (uint8_t)((sign << 7) | 0x7Fu);
+        else if (sc == 0.0f)                /* all finite elements are zero */
+            o[d] = (uint8_t)(sign << 7);
+        else
+            o[d] = orc_f32_to_e4m3fn(x[d] / sc);
+    }
+    free(x);
+}
+
+/* ------------------------------------------------------------------ */
+/* index maps                                                          */
+/* ------------------------------------------------------------------ */
+
+int orc_validate(const orc_problem *p)
+{
+    if (!p) return -1;
+    if (p->layers <= 0 || p->heads <= 0 || p->head_dim <= 0) return -1;
+    if (p->src_tp <= 0 || p->dst_tp <= 0) return -1;
+    if (p->heads % p->src_tp != 0 || p->heads % p->dst_tp != 0) return -1;
+    if (p->dst_rank < 0 || p->dst_rank >= p->dst_tp) return -1;
+    if (p->block_size <= 0 || p->num_blocks <= 0) return -1;
+    if (p->num_requests < 0 || (p->num_requests > 0 && !p->seq_lens)) return -1;
+    for (int r = 0; r < p->num_requests; ++r)
+        if (p->seq_lens[r] < 0) return -1;
+    if (p->src_order != ORC_TOKEN_MAJOR && p->src_order != ORC_HEAD_MAJOR) return -1;
+    int sf = p->src_fmt, df = p->dst_fmt;
+    if (sf != ORC_FP16 && sf != ORC_BF16) return -2;
+    if (sf == df) return 0;
+    if (sf == ORC_FP16 && df == ORC_BF16) return 0;
+    if (df == ORC_E4M3FN) return 0;
+    return -2;
+}
+
+/* Decode-side head i of rank dst_rank is global head g = dst_rank*Hd + i; the
+ * prefill shard holding it is g / Hs, at local position g % Hs. */
+void orc_head_source(const orc_problem *p, int i, int *shard, int *head)
+{
+    int Hs = p->heads / p->src_tp;
+    int Hd = p->heads / p->dst_tp;
+    int g = p->dst_rank * Hd + i;
+    *shard = g / Hs;
+    *head = g % Hs;
+}
+
+/* Requests are stored back to back in every shard buffer, each one as
+ * [layer][k/v][...Hs heads x T tokens...][dim]. */
+int64_t orc_src_request_base(const orc_problem *p, int r)
+{
+    int64_t Hs = p->heads / p->src_tp;
+    int64_t base = 0;
+    for (int q = 0; q < r; ++q)
+        base += (int64_t)p->layers * 2 * p->seq_lens[q] * Hs * p->head_dim;
+    return base;
+}
+
+/* element index of (r, l, kv, t, i, d) in its shard buffer, given the start
+ * `base` of request r in that buffer */
+static int64_t src_index_from(const orc_problem *p, int64_t base, int r, int l, int kv, int t,
+                              int i, int d, int *shard)
+{
+    int j, h;
+    orc_head_source(p, i, &j, &h);
+    *shard = j;
+    int64_t Hs = p->heads / p->src_tp;
+    int64_t T = p->seq_lens[r];
+    int64_t D = p->head_dim;
+    int64_t plane = (int64_t)l * 2 + kv;
+    if (p->src_order == ORC_TOKEN_MAJOR)
+        return base + ((plane * T + t) * Hs + h) * D + d;
+    return base + ((plane * Hs + h) * T + t) * D + d;
+}
+
+int64_t orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, int d, int *shard)
+{
+    return src_index_from(p, orc_src_request_base(p, r), r, l, kv, t, i, d, shard);
+}
+
+/* decode-side paged cache: [layer][k/v][block][slot][Hd][dim] */
+int64_t orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d)
+{
+    int64_t Hd = p->heads / p->dst_tp;
+    int64_t plane = (int64_t)l * 2 + kv;
+    return (((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i) * p->head_dim + d;
+}
+
+/* decode-side scales: [layer][k/v][block][slot][Hd] */
+int64_t orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i)
+{
+    int64_t Hd = p->heads / p->dst_tp;
+    int64_t plane = (int64_t)l * 2 + kv;
+    return ((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i;
+}
+
+static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+/* Transfer tensor: request-major segments, each starting on a 256-byte
+ * boundary; a segment is [layer][k/v][token][Hd][dim] in the destination type,
+ * then (e4m3fn only) [layer][k/v][token][Hd] fp32 scales on the next 256-byte
+ * boundary.  Returns the total size in bytes. */
+int64_t orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off)
+{
+    int64_t Hd = p->heads / p->dst_tp;
+    int64_t esz = orc_fmt_size(p->dst_fmt);
+    int64_t off = 0;
+    for (int r = 0; r < p->num_requests; ++r) {
+        int64_t rows = (int64_t)p->layers * 2 * p->seq_lens[r] * Hd;
+        off = align256(off);
+        if (data_off) data_off[r] = off;
+        off += rows * p->head_dim * esz;
+        if (p->dst_fmt == ORC_E4M3FN) {
+            off = align256(off);
+            if (scale_off) scale_off[r] = off;
+            off += rows * 4;
+        } else if (scale_off) {
+            scale_off[r] = -1;
+        }
+    }
+    return align256(off);
+}
+
+/* Gather source row (r, l, kv, t, i) element by element and convert it. */
+static void source_row_converted(const orc_problem *p, const void *const *shards, int64_t base,
+                                 int r, int l, int kv, int t, int i, uint16_t *tmp, void *out_row,
+                                 float *scale)
+{
+    for (int d = 0; d < p->head_dim; ++d) {
+        int j;
+        int64_t idx = src_index_from(p, base, r, l, kv, t, i, d, &j);
+        tmp[d] = ((const uint16_t *)shards[j])[idx];
+    }
+    orc_convert_row(p->src_fmt, p->dst_fmt, p->head_dim, tmp, out_row, scale);
+}
+
+int orc_pack(const orc_problem *p, const void *const *shards, void *wire)
+{
+    int rc = orc_validate(p);
+    if (rc) return rc;
+    int Hd = p->heads / p->dst_tp, D = p->head_dim;
+    int64_t esz = orc_fmt_size(p->dst_fmt);
+    int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
+    int64_t *soff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
+    uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
+    orc_wire_layout(p, doff, soff);
+    uint8_t *w = (uint8_t *)wire;
+    for (int r = 0; r < p->num_requests; ++r) {
+        int T = p->seq_lens[r];
+        int64_t base = orc_src_request_base(p, r);
+        for (int l = 0; l < p->layers; ++l)
+            for (int kv = 0; kv < 2; ++kv)
+                for (int t = 0; t < T; ++t)
+                    for (int i = 0; i < Hd; ++i) {
+                        int64_t row = (((int64_t)l * 2 + kv) * T + t) * Hd + i;
+                        float sc = 0.0f;
+                        source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
+                                             w + doff[r] + row * D * esz, &sc);
+                        if (p->dst_fmt == ORC_E4M3FN)
+                            memcpy(w + soff[r] + row * 4, &sc, 4);
+                    }
+    }
+    free(doff); free(soff); free(tmp);
+    return 0;
+}
+
+int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scales,
+               const int32_t *block_table, int32_t bt_stride)
+{
+    int rc = orc_validate(p);
+    if (rc) return rc;
+    int Hd = p->heads / p->dst_tp, D = p->head_dim, bs = p->block_size;
+    int64_t esz = orc_fmt_size(p->dst_fmt);
+    int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
+    int64_t *soff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
+    orc_wire_layout(p, doff, soff);
+    const uint8_t *w = (const uint8_t *)wire;
+    uint8_t *c = (uint8_t *)cache;
+    for (int r = 0; r < p->num_requests; ++r) {
+        int T = p->seq_lens[r];
+        for (int l = 0; l < p->layers; ++l)
+            for (int kv = 0; kv < 2; ++kv)
+                for (int t = 0; t < T; ++t) {
+                    int64_t b = block_table[(int64_t)r * bt_stride + t / bs];
+                    int slot = t % bs;
+                    for (int i = 0; i < Hd; ++i) {
+                        int64_t row = (((int64_t)l * 2 + kv) * T + t) * Hd + i;
+                        memcpy(c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
+                               w + doff[r] + row * D * esz, (size_t)(D * esz));
+                        if (p->dst_fmt == ORC_E4M3FN)
+                            memcpy(&scales[orc_cache_scale_index(p, b, l, kv, slot, i)],
+                                   w + soff[r] + row * 4, 4);
+                    }
+                }
+    }
+    free(doff); free(soff);
+    return 0;
+}
+
+int orc_repack(const orc_problem *p, const void *const *shards, void *cache, float *scales,
+               const int32_t *block_table, int32_t bt_stride)
+{
+    int rc = orc_validate(p);
+    if (rc) return rc;
+    int Hd = p->heads / p->dst_tp, D = p->head_dim, bs = p->block_size;
+    int64_t esz = orc_fmt_size(p->dst_fmt);
+    uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
+    uint8_t *c = (uint8_t *)cache;
+    for (int r = 0; r < p->num_requests; ++r) {
+        int T = p->seq_lens[r];
+        int64_t base = orc_src_request_base(p, r);
+        for (int l = 0; l < p->layers; ++l)
+            for (int kv = 0; kv < 2; ++kv)
+                for (int t = 0; t < T; ++t) {
+                    int64_t b = block_table[(int64_t)r * bt_stride + t / bs];
+                    int slot = t % bs;
+                    for (int i = 0; i < Hd; ++i) {
+                        float sc = 0.0f;
+                        source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
+                                             c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
+                                             &sc);
+                        if (p->dst_fmt == ORC_E4M3FN)
+                            scales[orc_cache_scale_index(p, b, l, kv, slot, i)] = sc;
+                    }
+                }
+    }
+    free(tmp);
+    return 0;
+}
+
+int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, int l, int kv,
+                      int t0, int nt, void *out_rows, float *out_scales)
+{
+    int rc = orc_validate(p);
+    if (rc) return rc;
+    if (r < 0 || r >= p->num_requests || l < 0 || l >= p->layers || kv < 0 || kv > 1) return -1;
+    if (t0 < 0 || nt < 0 || t0 + nt > p->seq_lens[r]) return -1;
+    int Hd = p->heads / p->dst_tp, D = p->head_dim;
+    int64_t esz = orc_fmt_size(p->dst_fmt);
+    uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
+    uint8_t *o = (uint8_t *)out_rows;
+    int64_t base = orc_src_request_base(p, r);
+    for (int t = t0; t < t0 + nt; ++t)
+        for (int i = 0; i < Hd; ++i) {
+            int64_t row = (int64_t)(t - t0) * Hd + i;
+            float sc = 0.0f;
+            source_row_converted(p, shards, base, r, l, kv, t, i, tmp, o + row * D * esz, &sc);
+            if (p->dst_fmt == ORC_E4M3FN && out_scales) out_scales[row] = sc;
+        }
+    free(tmp);
+    return 0;
+}

@@ -1,0 +1,87 @@
+/*
+ * kvx_oracle.h -- plain, slow CPU oracle for the KV-cache conversion of the
+ * heterogeneous compatible transmission module (Sec. III-B of the paper:
+ * precision alignment, VRAM-management alignment and parallel-strategy
+ * alignment).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark may load this library.  It shares no code,
+ * header, table or constant with the GPU library, and the GPU library never
+ * calls it.
+ *
+ * Everything here is written from the plain definition of the result: nested
+ * loops over (request, layer, k/v, token, head, dim), index maps written out
+ * one formula per coordinate, and casts computed on exact real values in
+ * double precision (decode -> round to the target grid -> encode).
+ */
+#ifndef KVX_ORACLE_H
+#define KVX_ORACLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element formats */
+enum { ORC_FP16 = 1, ORC_BF16 = 2, ORC_E4M3FN = 3 };
+/* source storage orders of one (layer, k/v) plane of a request */
+enum { ORC_TOKEN_MAJOR = 0 /* [token][head][dim] */, ORC_HEAD_MAJOR = 1 /* [head][token][dim] */ };
+
+typedef struct {
+    int32_t layers;      /* L */
+    int32_t heads;       /* H, global KV heads */
+    int32_t head_dim;    /* D */
+    int32_t src_tp;      /* tensor-parallel degree of the prefill side */
+    int32_t dst_tp;      /* tensor-parallel degree of the decode side */
+    int32_t dst_rank;    /* which decode rank's head shard is produced */
+    int32_t src_fmt;     /* ORC_FP16 or ORC_BF16 */
+    int32_t dst_fmt;     /* ORC_FP16, ORC_BF16 or ORC_E4M3FN */
+    int32_t src_order;   /* ORC_TOKEN_MAJOR or ORC_HEAD_MAJOR */
+    int32_t block_size;  /* tokens per destination page */
+    int64_t num_blocks;  /* pages in the destination pool (per plane) */
+    int32_t num_requests;
+    const int32_t *seq_lens; /* [num_requests], tokens per request */
+} orc_problem;
+
+/* ---- casts (precision alignment) ---- */
+double   orc_decode(int fmt, uint32_t bits);             /* exact value; NaN/Inf as such */
+uint16_t orc_fp16_to_bf16(uint16_t h);                   /* IEEE round-to-nearest-even */
+uint8_t  orc_f32_to_e4m3fn(float v);                     /* RNE, saturating to +-448 */
+float    orc_row_scale(const float *x, int n);           /* max|x| / 448, fp32 divide */
+void     orc_fp16_to_bf16_n(const uint16_t *in, uint16_t *out, int64_t n);
+void     orc_f32_to_e4m3fn_n(const float *in, uint8_t *out, int64_t n);
+void     orc_decode_n(int fmt, const void *in, double *out, int64_t n);
+/* convert one row of D source elements to the destination format; *scale is
+ * written only for an e4m3fn destination */
+void     orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row,
+                         void *dst_row, float *scale);
+
+/* ---- index maps (parallel-strategy and VRAM-management alignment) ---- */
+int      orc_validate(const orc_problem *p);             /* 0 ok, -1 invalid, -2 unsupported */
+void     orc_head_source(const orc_problem *p, int i, int *shard, int *head);
+int64_t  orc_src_request_base(const orc_problem *p, int r);  /* elements */
+int64_t  orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, int d, int *shard);
+int64_t  orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d);
+int64_t  orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i);
+/* wire ("one-dimensional tensor") segments: byte offsets per request */
+int64_t  orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off);
+int      orc_fmt_size(int fmt);
+
+/* ---- the three operations ---- */
+int orc_pack(const orc_problem *p, const void *const *shards, void *wire);
+int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scales,
+               const int32_t *block_table, int32_t bt_stride);
+int orc_repack(const orc_problem *p, const void *const *shards, void *cache, float *scales,
+               const int32_t *block_table, int32_t bt_stride);
+
+/* expected destination rows of request r, plane (l, kv), tokens [t0, t0+nt):
+ * nt*Hd rows in (token, head) order, plus nt*Hd scales for e4m3fn */
+int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, int l, int kv,
+                      int t0, int nt, void *out_rows, float *out_scales);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,133 @@
+"""Workload cases and helpers shared by the test modules.
+
+Small cases keep the structure of the five full workloads (same heads,
+head_dim, TP mapping, dtypes, orders and page sizes) with fewer layers,
+requests and tokens, so the oracle finishes in well under a second while
+still spanning several pages per request and a ragged last page."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import workload as W
+
+FULL = W.WORKLOADS
+TINY = FULL["tiny_tp1to2_fp16_bf16"]
+L8B = FULL["llama3_8b_bf16_bs16"]
+L70B = FULL["llama3_70b_tp4to2_bf16_bs32"]
+QWEN = FULL["qwen7b_htd_fp16_bf16_bs64"]
+FP8 = FULL["fp8_decode_61l_bf16_e4m3_bs16"]
+
+SMALL = {
+    "tiny": TINY,
+    "llama3_8b_small": L8B.replace(name="llama3_8b_small", layers=2, total_layers=2,
+                                   num_requests=3, len_lo=17, len_hi=100, num_blocks=64),
+    "llama3_70b_small_r0": L70B.replace(name="llama3_70b_small_r0", layers=2, total_layers=2,
+                                        num_requests=2, len_lo=33, len_hi=90, num_blocks=16),
+    "llama3_70b_small_r1": L70B.replace(name="llama3_70b_small_r1", layers=2, total_layers=2,
+                                        num_requests=2, len_lo=33, len_hi=90, num_blocks=16,
+                                        dst_rank=1),
+    "qwen_htd_small": QWEN.replace(name="qwen_htd_small", layers=2, total_layers=2,
+                                   num_requests=3, len_lo=10, len_hi=150, num_blocks=16),
+    "fp8_small": FP8.replace(name="fp8_small", layers=2, total_layers=3, num_requests=3,
+                             len_lo=5, len_hi=70, num_blocks=64),
+    # split: prefill TP2 -> decode TP4, rank 3 (second half of shard 1)
+    "split_tp2to4_r3": L8B.replace(name="split_tp2to4_r3", layers=2, total_layers=2, src_tp=2,
+                                   dst_tp=4, dst_rank=3, num_requests=2, len_lo=20, len_hi=50,
+                                   num_blocks=16),
+    # merge everything: prefill TP8 -> decode TP1, head-major fp16 -> bf16
+    "merge_tp8to1_htd": QWEN.replace(name="merge_tp8to1_htd", heads=8, layers=1, total_layers=1,
+                                     src_tp=8, dst_tp=1, num_requests=2, len_lo=3, len_hi=40,
+                                     block_size=16, num_blocks=16),
+    # ratio that is not a power of two: 6 heads, prefill TP2 -> decode TP3 rank 1
+    "tp2to3_r1_fp8": FP8.replace(name="tp2to3_r1_fp8", heads=6, layers=2, total_layers=2,
+                                 src_tp=2, dst_tp=3, dst_rank=1, num_requests=2, len_lo=1,
+                                 len_hi=33, num_blocks=16),
+    # fp16 -> e4m3fn, head-major, with an empty request in the batch
+    "fp16_e4m3_htd_empty": QWEN.replace(name="fp16_e4m3_htd_empty", dst_dtype="e4m3fn",
+                                        layers=1, total_layers=1, num_requests=4,
+                                        lens_override=(37, 0, 16, 1), block_size=16,
+                                        num_blocks=16, seed=99),
+}
+
+
+def fmt_codes(mod):
+    """dtype name -> the integer code used by `mod` (oracle or GPU binding)."""
+    return {"fp16": mod.FP16, "bf16": mod.BF16, "e4m3fn": mod.E4M3FN}
+
+
+def dst_size(w):
+    return 1 if w.dst_dtype == "e4m3fn" else 2
+
+
+def oracle_problem(O, w, lens, layers=None):
+    f = fmt_codes(O)
+    order = O.TOKEN_MAJOR if w.src_order == "thd" else O.HEAD_MAJOR
+    return O.OracleProblem(layers or w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp,
+                           w.dst_rank, f[w.src_dtype], f[w.dst_dtype], order, w.block_size,
+                           w.num_blocks, lens)
+
+
+def inputs(w, layer0=0, nlayers=None):
+    lens = W.seq_lens(w)
+    bt, stride = W.block_table(w, lens)
+    shards = W.source_shards(w, lens, layer0, nlayers)
+    return lens, bt, stride, shards
+
+
+# ---- library-only construction of what the decode side must see ------------
+
+_TDT = {"fp16": torch.float16, "bf16": torch.bfloat16}
+
+
+def consumer_rows(w, lens, r, layer0, nlayers):
+    """Expected decode-side rows of request r, built only from the generator's
+    logical values and torch library conversions:
+    returns (rows uint8 [L][2][T][Hd][D*esize], scales float32 [L][2][T][Hd] or None).
+
+    Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd).
+    Casts: same type = bits; fp16->bf16 = torch .to(bfloat16);
+    e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn)."""
+    x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers)).to(_TDT[w.src_dtype])
+    x = x[:, :, w.dst_rank * w.hd:(w.dst_rank + 1) * w.hd]        # [L][2][Hd][T][D]
+    x = x.permute(0, 1, 3, 2, 4).contiguous()                      # [L][2][T][Hd][D]
+    if w.dst_dtype == w.src_dtype:
+        return x.view(torch.uint8).numpy().reshape(*x.shape[:4], -1), None
+    if w.dst_dtype == "bf16":
+        y = x.to(torch.bfloat16)
+        return y.view(torch.uint8).numpy().reshape(*y.shape[:4], -1), None
+    xf = x.float()
+    s = xf.abs().amax(dim=-1) / torch.tensor(448.0)
+    v = xf / s[..., None]
+    q = v.clamp(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8)
+    zero_rows = (s == 0)[..., None].expand_as(q)
+    signed_zero = torch.where(torch.signbit(xf), 0x80, 0).to(torch.uint8)
+    q = torch.where(zero_rows, signed_zero, q)
+    return q.numpy(), s.numpy()
+
+
+def gather_pages(cache_u8, w, lens, bt, r, nlayers, scales=None):
+    """What a paged-attention reader sees for request r: the pages listed in
+    its block-table row, in order, cut at T tokens.  cache_u8 is the whole
+    destination pool as bytes; returns rows shaped like consumer_rows."""
+    T = int(lens[r])
+    nblk = (T + w.block_size - 1) // w.block_size
+    row = w.head_dim * dst_size(w)
+    c = cache_u8.reshape(nlayers, 2, w.num_blocks, w.block_size, w.hd, row)
+    pages = c[:, :, bt[r, :nblk]]                                   # [L][2][nblk][bs][Hd][row]
+    rows = pages.reshape(nlayers, 2, nblk * w.block_size, w.hd, row)[:, :, :T]
+    sc = None
+    if scales is not None:
+        s = scales.reshape(nlayers, 2, w.num_blocks, w.block_size, w.hd)
+        sc = s[:, :, bt[r, :nblk]].reshape(nlayers, 2, nblk * w.block_size, w.hd)[:, :, :T]
+    return rows, sc
+
+
+def written_mask(w, lens, bt, nlayers):
+    """Bytes of the pool that the conversion must write (per page slot)."""
+    m = np.zeros((nlayers, 2, w.num_blocks, w.block_size), dtype=bool)
+    for r, T in enumerate(lens):
+        for k in range((int(T) + w.block_size - 1) // w.block_size):
+            n = min(w.block_size, int(T) - k * w.block_size)
+            m[:, :, bt[r, k], :n] = True
+    return m

@@ -1,0 +1,259 @@
+"""Seeded synthetic KV-cache workloads, shared by the tests and the benchmark.
+
+This module draws random numbers and arranges them in the prefill side's
+storage order; it holds none of the conversion's arithmetic (no head map to
+the decode side, no paging, no casts of the method).  Values are keyed by
+logical coordinates (request, layer, k/v, global head, token, dim), so a
+different shard split or storage order of the same workload holds the same
+values.
+
+The C core (``gen.c``) is a counter-based splitmix64 stream; see its header.
+Streams: 1 sequence lengths, 2 block-table permutation, 3 values,
+4 outlier mask, 5 outlier sign, 6 per-(layer, k/v, head) scale.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gen.c")
+_LIB_PATH = os.path.join(_HERE, "libkvxgen.so")
+GCC_CMD = ["gcc", "-std=c99", "-O2", "-Wall", "-fPIC", "-shared", "-pthread", "-o", _LIB_PATH,
+           _SRC, "-lm"]
+
+SENTINEL = 0xA5
+
+S_LENS, S_TABLE, S_VALUES, S_OUTLIER, S_OUTSIGN, S_HEADSCALE = 1, 2, 3, 4, 5, 6
+
+
+def build() -> str:
+    subprocess.run(GCC_CMD, check=True)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        u64, u32, i64, vp = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64, ctypes.c_void_p
+        L.wl_word.restype = u64
+        L.wl_word.argtypes = [u64, u32, u64]
+        L.wl_uniform.restype = ctypes.c_double
+        L.wl_uniform.argtypes = [u64, u32, u64]
+        L.wl_normal.restype = ctypes.c_double
+        L.wl_normal.argtypes = [u64, u32, u64]
+        L.wl_fill_normal.argtypes = [u64, u32, u64, i64, ctypes.c_double, vp, ctypes.c_int]
+        L.wl_fill_uniform.argtypes = [u64, u32, u64, i64, vp]
+        L.wl_select.restype = i64
+        L.wl_select.argtypes = [u64, u32, u64, i64, ctypes.c_double, vp]
+        L.wl_permutation.argtypes = [u64, u32, i64, vp]
+        _lib = L
+    return _lib
+
+
+def _threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    layers: int            # layers handled by one plan (a layer group for grouped runs)
+    total_layers: int      # layers of the model; values are keyed by the global layer
+    heads: int             # global KV heads
+    head_dim: int
+    src_tp: int
+    dst_tp: int
+    dst_rank: int
+    src_dtype: str         # "fp16" | "bf16"
+    dst_dtype: str         # "fp16" | "bf16" | "e4m3fn"
+    src_order: str         # "thd" = [token][head][dim], "htd" = [head][token][dim]
+    block_size: int
+    num_blocks: int
+    num_requests: int
+    len_lo: int
+    len_hi: int
+    seed: int
+    sigma: float = 1.0
+    outlier_frac: float = 0.0
+    outlier_value: float = 0.0
+    head_scale_log10: tuple | None = None
+    lens_override: tuple | None = None   # explicit tokens per request (edge cases)
+
+    @property
+    def hs(self):
+        return self.heads // self.src_tp
+
+    @property
+    def hd(self):
+        return self.heads // self.dst_tp
+
+    @property
+    def layer_groups(self):
+        return math.ceil(self.total_layers / self.layers)
+
+    def group_layers(self, g: int) -> tuple[int, int]:
+        """(first global layer, layer count) of layer group g."""
+        l0 = g * self.layers
+        return l0, min(self.layers, self.total_layers - l0)
+
+    def read_shards(self) -> list[int]:
+        """Prefill shards whose head range overlaps the produced decode rank."""
+        lo, hi = self.dst_rank * self.hd, (self.dst_rank + 1) * self.hd
+        return [j for j in range(self.src_tp) if j * self.hs < hi and (j + 1) * self.hs > lo]
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+# The five workloads: the decode-side shapes of four model families plus a
+# tiny one.  Sizes: layers x KV heads x head_dim, tokens per request.
+WORKLOADS = {
+    w.name: w
+    for w in [
+        # 2 layers, 4 heads, dim 64, one 256-token request, TP1 -> TP2 rank 0,
+        # fp16 -> bf16, 64-block pool of 16-token pages
+        Workload("tiny_tp1to2_fp16_bf16", 2, 2, 4, 64, 1, 2, 0, "fp16", "bf16", "thd",
+                 16, 64, 1, 256, 256, seed=17542),
+        # Llama-3-8B KV shape: 32 layers, 8 heads, dim 128; 16 requests of
+        # 512..4096 tokens; bf16 re-layout into 16-token pages of a 65536-page pool
+        Workload("llama3_8b_bf16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "bf16", "thd",
+                 16, 65536, 16, 512, 4096, seed=17543),
+        # Llama-3-70B shard: 80 layers, 8 heads, dim 128; 8 requests of
+        # 1024..8192 tokens; prefill TP4 -> decode TP2 rank 0 (merges shards 0, 1);
+        # 32-token pages, 16384-page pool
+        Workload("llama3_70b_tp4to2_bf16_bs32", 80, 80, 8, 128, 4, 2, 0, "bf16", "bf16", "thd",
+                 32, 16384, 8, 1024, 8192, seed=17544),
+        # Qwen-7B-style GQA: 28 layers, 4 heads, dim 128; 32 requests of
+        # 128..2048 tokens; fp16 head-major source, sigma 2 with 0.1% outliers at
+        # +-60000 -> bf16 token-major 64-token pages, 8192-page pool
+        Workload("qwen7b_htd_fp16_bf16_bs64", 28, 28, 4, 128, 1, 1, 0, "fp16", "bf16", "htd",
+                 64, 8192, 32, 128, 2048, seed=17545, sigma=2.0, outlier_frac=0.001,
+                 outlier_value=60000.0),
+        # fp8 decode cache: 61 layers (run as groups of 4), 8 heads, dim 128;
+        # 64 requests of 256..16384 tokens; bf16 with a per-(layer, k/v, head)
+        # scale 10^U(-2, 2) -> e4m3fn + fp32 per-(token, head) scale, 16-token
+        # pages of a 2^20-page pool
+        Workload("fp8_decode_61l_bf16_e4m3_bs16", 4, 61, 8, 128, 1, 1, 0, "bf16", "e4m3fn", "thd",
+                 16, 1 << 20, 64, 256, 16384, seed=17546, head_scale_log10=(-2.0, 2.0)),
+    ]
+}
+
+
+def seq_lens(w: Workload) -> np.ndarray:
+    """T_r = lo + floor(u_r * (hi - lo + 1)), or the explicit lengths."""
+    if w.lens_override is not None:
+        return np.asarray(w.lens_override, dtype=np.int32)
+    u = np.empty(w.num_requests, dtype=np.float64)
+    lib().wl_fill_uniform(w.seed, S_LENS, 0, w.num_requests, u.ctypes.data)
+    lens = w.len_lo + np.floor(u * (w.len_hi - w.len_lo + 1)).astype(np.int64)
+    return np.minimum(lens, w.len_hi).astype(np.int32)
+
+
+def permutation(seed: int, n: int, stream: int = S_TABLE) -> np.ndarray:
+    out = np.empty(n, dtype=np.int32)
+    lib().wl_permutation(seed, stream, n, out.ctypes.data)
+    return out
+
+
+def block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
+    """Pages for each request, drawn in order from a seeded permutation of the
+    pool.  Returns ([R, stride] int32 with -1 in unused entries, stride)."""
+    nblk = [(int(t) + w.block_size - 1) // w.block_size for t in lens]
+    stride = max(nblk + [1])
+    need = sum(nblk)
+    if need > w.num_blocks:
+        raise ValueError(f"{w.name}: {need} pages needed, pool has {w.num_blocks}")
+    perm = permutation(w.seed, w.num_blocks)
+    bt = np.full((len(lens), stride), -1, dtype=np.int32)
+    pos = 0
+    for r, n in enumerate(nblk):
+        bt[r, :n] = perm[pos:pos + n]
+        pos += n
+    return bt, stride
+
+
+def _request_value_base(w: Workload, lens: np.ndarray, r: int) -> int:
+    return int(sum(w.total_layers * 2 * w.heads * int(t) * w.head_dim for t in lens[:r]))
+
+
+def logical_values(w: Workload, lens: np.ndarray, r: int, layer0: int, nlayers: int) -> np.ndarray:
+    """float32 values of request r, layers [layer0, layer0+nlayers), shaped
+    [layer][k/v][global head][token][dim]."""
+    T = int(lens[r])
+    H, D = w.heads, w.head_dim
+    n = nlayers * 2 * H * T * D
+    start = _request_value_base(w, lens, r) + layer0 * 2 * H * T * D
+    x = np.empty(n, dtype=np.float32)
+    if n:
+        lib().wl_fill_normal(w.seed, S_VALUES, start, n, w.sigma, x.ctypes.data, _threads())
+    x = x.reshape(nlayers, 2, H, T, D)
+    if w.head_scale_log10 is not None and n:
+        lo, hi = w.head_scale_log10
+        u = np.empty(w.total_layers * 2 * H, dtype=np.float64)
+        lib().wl_fill_uniform(w.seed, S_HEADSCALE, 0, u.size, u.ctypes.data)
+        s = (10.0 ** (lo + (hi - lo) * u)).astype(np.float32).reshape(w.total_layers, 2, H)
+        x *= s[layer0:layer0 + nlayers, :, :, None, None]
+    if w.outlier_frac > 0 and n:
+        idx = np.empty(n, dtype=np.int64)
+        c = lib().wl_select(w.seed, S_OUTLIER, start, n, w.outlier_frac, idx.ctypes.data)
+        idx = idx[:c]
+        flat = x.reshape(-1)
+        for k in idx:
+            neg = lib().wl_uniform(w.seed, S_OUTSIGN, start + int(k)) < 0.5
+            flat[k] = -w.outlier_value if neg else w.outlier_value
+    return x
+
+
+def _to_bits(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float32 to the 16-bit storage type (torch's round-to-nearest-even)
+    and return the bit patterns as uint16."""
+    import torch
+    tdt = {"fp16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    t = torch.from_numpy(x).to(tdt)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int | None = None,
+                  shards: list[int] | None = None) -> list[np.ndarray | None]:
+    """Prefill-side shard buffers (uint16 bit patterns), one per source TP rank.
+
+    Shard j holds global heads [j*Hs, (j+1)*Hs); requests are stored back to
+    back, each as [layer][k/v][token][head][dim] ("thd") or
+    [layer][k/v][head][token][dim] ("htd").  Shards not listed are None."""
+    import torch
+    if nlayers is None:
+        nlayers = w.layers
+    if shards is None:
+        shards = w.read_shards()
+    Hs, D = w.hs, w.head_dim
+    per_shard = sum(nlayers * 2 * int(t) * Hs * D for t in lens)
+    out: list[np.ndarray | None] = [None] * w.src_tp
+    for j in shards:
+        out[j] = np.empty(per_shard, dtype=np.uint16)
+    off = 0
+    for r in range(len(lens)):
+        T = int(lens[r])
+        n = nlayers * 2 * T * Hs * D
+        if n == 0:
+            continue
+        bits = _to_bits(logical_values(w, lens, r, layer0, nlayers), w.src_dtype)
+        tb = torch.from_numpy(bits.view(np.int16))
+        for j in shards:
+            part = tb[:, :, j * Hs:(j + 1) * Hs]
+            if w.src_order == "thd":
+                part = part.permute(0, 1, 3, 2, 4)
+            out[j][off:off + n] = part.contiguous().numpy().reshape(-1).view(np.uint16)
+        off += n
+    return out
