@@ -1,0 +1,189 @@
+/*
+ * kvx.h -- C ABI of the KV-cache conversion library for MI355X (gfx950).
+ *
+ * The library implements the data path of the heterogeneous compatible
+ * transmission module of "Disaggregated Prefill and Decoding Inference System
+ * for Large Language Model Serving on Multi-Vendor GPUs" (Sec. III-B): the KV
+ * cache that a prefill (P) instance produced is converted into the layout,
+ * page size, element type and tensor-parallel head shard that a decode (D)
+ * instance with another parallel strategy expects.  The three data components
+ * of the module map to the calls below:
+ *
+ *   - parallel-strategy alignment (Sec. III-B-3, Fig. 4): a decode rank holds
+ *     one contiguous range of the global KV heads; the prefill shards that
+ *     overlap it are merged (src_tp > dst_tp) or split (src_tp < dst_tp);
+ *   - VRAM-management alignment (Sec. III-B-2, Fig. 5): the prefill layout is
+ *     flattened into a one-dimensional transfer tensor (kvx_pack) and restored
+ *     into the decode side's paged cache with its own page size and layout
+ *     (kvx_unpack); kvx_repack does both in one pass when both sides are on
+ *     the same device;
+ *   - precision alignment (Sec. I, contribution 1, named only): the decode
+ *     element type.  Casts round to nearest even; the e4m3fn cast uses a
+ *     per-(token, head) fp32 scale max|x| / 448 and saturates at +-448.
+ *
+ * Layouts (element indices; all dimensions row-major):
+ *   source shard j (j = 0..src_tp-1) holds global heads [j*Hs, (j+1)*Hs),
+ *     Hs = num_kv_heads / src_tp; requests are stored back to back, request r
+ *     as [layer][k/v][token][Hs][dim] (KVX_THD) or [layer][k/v][Hs][token][dim]
+ *     (KVX_HTD), T_r tokens;
+ *   decode rank dst_rank holds global heads [dst_rank*Hd, (dst_rank+1)*Hd),
+ *     Hd = num_kv_heads / dst_tp;
+ *   cache:  [layer][k/v][num_blocks][block_size][Hd][dim] in dst_dtype; token
+ *     t of request r goes to page block_table[r*bt_stride + t/block_size],
+ *     slot t % block_size;
+ *   scales (e4m3fn only): [layer][k/v][num_blocks][block_size][Hd] fp32;
+ *   transfer tensor: per request, starting on a 256-byte boundary,
+ *     [layer][k/v][token][Hd][dim] in dst_dtype, then (e4m3fn only) on the
+ *     next 256-byte boundary [layer][k/v][token][Hd] fp32 scales.
+ * Bytes outside these positions (slots past the end of a request's last page,
+ * pages not in a block-table row, transfer-tensor padding) are never written.
+ *
+ * Ownership: every buffer is caller-owned device memory; the library never
+ * allocates or frees it.  A plan is library-owned: kvx_plan copies seq_lens
+ * and allocates a small device table on the device current at that time.
+ *
+ * Streams: kvx_pack / kvx_unpack / kvx_repack only enqueue work on the given
+ * hipStream_t (passed as void*, NULL = default stream) and return; buffers must
+ * stay alive until the stream reaches that point.  A plan is immutable and may
+ * be used concurrently on several streams of its device.
+ *
+ * Errors: every call returns a kvx_status; nothing is thrown and nothing
+ * aborts.  kvx_last_error() gives a message for the calling thread's last
+ * non-OK status.
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVX_ABI_VERSION 1
+
+typedef enum {
+    KVX_OK = 0,
+    KVX_EINVAL = -1,       /* invalid argument, shape or pointer */
+    KVX_EUNSUPPORTED = -2, /* valid request this library does not implement */
+    KVX_ENOMEM = -3,       /* host or device allocation failed (kvx_plan only) */
+    KVX_EDEVICE = -4       /* no usable device for the plan, or a HIP error */
+} kvx_status;
+
+typedef enum { KVX_FP16 = 1, KVX_BF16 = 2, KVX_FP8_E4M3FN = 3 } kvx_dtype;
+
+typedef enum {
+    KVX_THD = 0, /* [token][head][dim] within one (layer, k/v) plane of a request */
+    KVX_HTD = 1  /* [head][token][dim] */
+} kvx_order;
+
+typedef struct kvx_plan_s kvx_plan_t; /* opaque, library-owned */
+
+/* The conversion problem, in the terms of Sec. III-B: the two parallel
+ * strategies (src_tp, dst_tp, dst_rank), the page size and layout of the
+ * decode side (block_size, num_blocks, src_order), the precision of each side
+ * (src_dtype, dst_dtype), and the requests whose KV moves. */
+typedef struct {
+    int32_t num_layers;     /* L >= 1 */
+    int32_t num_kv_heads;   /* H >= 1, global KV heads */
+    int32_t head_dim;       /* D >= 1 */
+    int32_t src_tp;         /* prefill TP degree, divides H */
+    int32_t dst_tp;         /* decode TP degree, divides H */
+    int32_t dst_rank;       /* 0 <= dst_rank < dst_tp */
+    int32_t src_dtype;      /* kvx_dtype: KVX_FP16 or KVX_BF16 */
+    int32_t dst_dtype;      /* kvx_dtype */
+    int32_t src_order;      /* kvx_order */
+    int32_t block_size;     /* tokens per decode page, >= 1 */
+    int64_t num_blocks;     /* pages per (layer, k/v) plane of the pool, >= 1 */
+    int32_t num_requests;   /* >= 0 */
+    const int32_t *seq_lens;/* host array [num_requests], T_r >= 0; copied */
+} kvx_desc;
+
+typedef struct {
+    uint64_t wire_bytes;            /* transfer tensor size (multiple of 256) */
+    int64_t total_tokens;           /* sum of T_r */
+    int64_t read_bytes_pack, write_bytes_pack;     /* algorithmic bytes per call */
+    int64_t read_bytes_unpack, write_bytes_unpack;
+    int64_t read_bytes_repack, write_bytes_repack;
+    int32_t max_blocks_per_request; /* minimum valid bt_stride */
+    int32_t num_items;              /* logical pages over all requests (per plane) */
+    int32_t device;                 /* HIP device of the plan's tables, -1 = none */
+    int32_t reserved;
+} kvx_plan_info;
+
+/* Validate the problem and build a plan (host tables, plus a device table on
+ * the current HIP device when one is usable; otherwise the plan is host-only
+ * and the launch calls return KVX_EDEVICE).
+ * Returns KVX_EINVAL for: NULL desc/out; a dimension <= 0; H % src_tp != 0 or
+ * H % dst_tp != 0; dst_rank outside [0, dst_tp); block_size <= 0;
+ * num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
+ * an unknown order; head_dim * element size not a multiple of 16 bytes on
+ * either side.  KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16,
+ * bf16->bf16, fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row
+ * (head_dim * dst size) above 1024 bytes; more than 128 heads per decode
+ * rank; more than 65535 source heads per shard; 2*L > 65535; more than 2^24-1
+ * logical pages (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if the table cannot be allocated. */
+kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);
+
+kvx_status kvx_plan_info_get(const kvx_plan_t *plan, kvx_plan_info *info);
+
+/* Byte offsets of request r's data and scale regions in the transfer tensor
+ * (scale_off = -1 unless dst is e4m3fn).  KVX_EINVAL for r out of range. */
+kvx_status kvx_plan_segment(const kvx_plan_t *plan, int32_t r, int64_t *data_off,
+                            int64_t *scale_off);
+
+/* Frees the plan and its device table (synchronous; the caller ensures no
+ * launch using it is still pending).  NULL is accepted. */
+kvx_status kvx_plan_destroy(kvx_plan_t *plan);
+
+/* Pack (VRAM-management alignment, prefill side, Sec. III-B-2): gather the
+ * decode rank's heads from the source shards, cast to dst_dtype and write the
+ * transfer tensor.
+ *   src_shards: host array of src_tp device pointers, one per prefill shard in
+ *               the layout above; shards the decode rank does not read may be
+ *               NULL.  Each read pointer must be 16-byte aligned.
+ *   wire:       device, >= wire_bytes, 16-byte aligned.
+ * KVX_EINVAL for a NULL plan/array, a NULL or misaligned needed pointer;
+ * KVX_EDEVICE for a host-only plan, a current device other than the plan's,
+ * or a launch error. */
+kvx_status kvx_pack(const kvx_plan_t *plan, const void *const *src_shards, void *wire,
+                    void *hip_stream);
+
+/* Unpack (VRAM-management alignment, decode side): scatter the transfer
+ * tensor into the paged cache (and the scales) without further casting.
+ *   cache:       device [L][2][num_blocks][block_size][Hd][D] dst_dtype, 16-byte aligned.
+ *   scales:      device [L][2][num_blocks][block_size][Hd] fp32, 16-byte aligned;
+ *                non-NULL if and only if dst_dtype is e4m3fn.
+ *   block_table: device int32 [num_requests][bt_stride]; the first
+ *                ceil(T_r/block_size) entries of row r are used.  Contents are a
+ *                caller contract (kvx_check_block_table checks them on the
+ *                host); a page id outside [0, num_blocks) is skipped, never
+ *                written.  Ids shared by two requests are two writers (a race).
+ *   bt_stride:   >= max_blocks_per_request.
+ * Errors as kvx_pack, plus KVX_EINVAL for a scales pointer whose presence does
+ * not match dst_dtype, a NULL block table with pages to write, or a short
+ * bt_stride. */
+kvx_status kvx_unpack(const kvx_plan_t *plan, const void *wire, void *cache, float *scales,
+                      const int32_t *block_table, int32_t bt_stride, void *hip_stream);
+
+/* Repack: kvx_pack followed by kvx_unpack in one pass with no transfer tensor;
+ * the cache and scales it writes are bit-identical to that pair's. */
+kvx_status kvx_repack(const kvx_plan_t *plan, const void *const *src_shards, void *cache,
+                      float *scales, const int32_t *block_table, int32_t bt_stride,
+                      void *hip_stream);
+
+/* Host-side check of a block table: every used entry in [0, num_blocks) and no
+ * page used twice.  KVX_EINVAL (with a message) otherwise. */
+kvx_status kvx_check_block_table(const kvx_plan_t *plan, const int32_t *host_block_table,
+                                 int32_t bt_stride);
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char *kvx_last_error(void);
+
+int32_t kvx_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KVX_H */

@@ -1,0 +1,206 @@
+"""Python binding of the kvx C ABI (include/kvx.h): argument marshalling only.
+
+Every step of the conversion runs in the gfx950 kernels of libkvx.so; this
+module converts Python arguments (ints, torch tensors) to the C types and
+turns non-OK statuses into KvxError.  torch is imported first so that the
+library binds to the HIP runtime torch already loaded; torch serves only for
+device memory and streams.
+
+Importing fails loudly (ImportError) when libkvx.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (loads the process's HIP runtime before libkvx.so)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkvx.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"kvx HIP library not built: {LIB_PATH} is missing "
+                      "(run `python -m paper_2509_17542_amd.build`)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, EINVAL, EUNSUPPORTED, ENOMEM, EDEVICE = 0, -1, -2, -3, -4
+FP16, BF16, E4M3FN = 1, 2, 3
+THD, HTD = 0, 1
+_STATUS = {0: "KVX_OK", -1: "KVX_EINVAL", -2: "KVX_EUNSUPPORTED", -3: "KVX_ENOMEM",
+           -4: "KVX_EDEVICE"}
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class kvx_desc(ctypes.Structure):
+    _fields_ = [
+        ("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("src_tp", ctypes.c_int32), ("dst_tp", ctypes.c_int32),
+        ("dst_rank", ctypes.c_int32), ("src_dtype", ctypes.c_int32),
+        ("dst_dtype", ctypes.c_int32), ("src_order", ctypes.c_int32),
+        ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int64),
+        ("num_requests", ctypes.c_int32), ("seq_lens", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+class kvx_plan_info(ctypes.Structure):
+    _fields_ = [
+        ("wire_bytes", ctypes.c_uint64), ("total_tokens", ctypes.c_int64),
+        ("read_bytes_pack", ctypes.c_int64), ("write_bytes_pack", ctypes.c_int64),
+        ("read_bytes_unpack", ctypes.c_int64), ("write_bytes_unpack", ctypes.c_int64),
+        ("read_bytes_repack", ctypes.c_int64), ("write_bytes_repack", ctypes.c_int64),
+        ("max_blocks_per_request", ctypes.c_int32), ("num_items", ctypes.c_int32),
+        ("device", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_lib.kvx_plan.restype = ctypes.c_int
+_lib.kvx_plan.argtypes = [ctypes.POINTER(kvx_desc), ctypes.POINTER(_vp)]
+_lib.kvx_plan_info_get.restype = ctypes.c_int
+_lib.kvx_plan_info_get.argtypes = [_vp, ctypes.POINTER(kvx_plan_info)]
+_lib.kvx_plan_segment.restype = ctypes.c_int
+_lib.kvx_plan_segment.argtypes = [_vp, _i32, ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64)]
+_lib.kvx_plan_destroy.restype = ctypes.c_int
+_lib.kvx_plan_destroy.argtypes = [_vp]
+_lib.kvx_pack.restype = ctypes.c_int
+_lib.kvx_pack.argtypes = [_vp, _vp, _vp, _vp]
+_lib.kvx_unpack.restype = ctypes.c_int
+_lib.kvx_unpack.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp]
+_lib.kvx_repack.restype = ctypes.c_int
+_lib.kvx_repack.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp]
+_lib.kvx_check_block_table.restype = ctypes.c_int
+_lib.kvx_check_block_table.argtypes = [_vp, _vp, _i32]
+_lib.kvx_last_error.restype = ctypes.c_char_p
+_lib.kvx_last_error.argtypes = []
+_lib.kvx_abi_version.restype = ctypes.c_int32
+_lib.kvx_abi_version.argtypes = []
+
+EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_destroy", "kvx_pack",
+           "kvx_unpack", "kvx_repack", "kvx_check_block_table", "kvx_last_error",
+           "kvx_abi_version")
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise KvxError(status, kvx_last_error())
+
+
+def _addr(x) -> int | None:
+    """Device (or host) address of a tensor, an int, or None."""
+    if x is None:
+        return None
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+class Plan:
+    """Owns a kvx_plan_t*; destroyed with kvx_plan_destroy."""
+
+    _destroy = _lib.kvx_plan_destroy  # kept reachable during interpreter shutdown
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h:
+            self._destroy(h)
+
+    @property
+    def _as_parameter_(self):
+        return ctypes.c_void_p(self.handle)
+
+
+def make_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype, dst_dtype,
+              src_order, block_size, num_blocks, seq_lens):
+    """kvx_desc plus the int32 array its seq_lens points into."""
+    lens = (ctypes.c_int32 * max(len(seq_lens), 1))(*[int(t) for t in seq_lens])
+    d = kvx_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype,
+                 dst_dtype, src_order, block_size, num_blocks, len(seq_lens),
+                 ctypes.cast(lens, ctypes.POINTER(ctypes.c_int32)))
+    d._lens = lens
+    return d
+
+
+def kvx_plan(desc: kvx_desc) -> Plan:
+    h = _vp()
+    _check(_lib.kvx_plan(ctypes.byref(desc), ctypes.byref(h)))
+    return Plan(h.value)
+
+
+def kvx_plan_info_get(plan: Plan) -> kvx_plan_info:
+    info = kvx_plan_info()
+    _check(_lib.kvx_plan_info_get(plan, ctypes.byref(info)))
+    return info
+
+
+def kvx_plan_segment(plan: Plan, r: int) -> tuple[int, int]:
+    d, s = ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.kvx_plan_segment(plan, r, ctypes.byref(d), ctypes.byref(s)))
+    return d.value, s.value
+
+
+def kvx_plan_destroy(plan: Plan) -> None:
+    h, plan.handle = plan.handle, None
+    _check(_lib.kvx_plan_destroy(h))
+
+
+def _shard_array(shards):
+    arr = (_vp * max(len(shards), 1))()
+    for j, s in enumerate(shards):
+        arr[j] = _addr(s)
+    return arr
+
+
+def kvx_pack(plan: Plan, src_shards, wire, stream=None) -> None:
+    _check(_lib.kvx_pack(plan, _shard_array(src_shards), _addr(wire), _stream(stream)))
+
+
+def kvx_unpack(plan: Plan, wire, cache, scales, block_table, bt_stride: int, stream=None) -> None:
+    _check(_lib.kvx_unpack(plan, _addr(wire), _addr(cache), _addr(scales), _addr(block_table),
+                           bt_stride, _stream(stream)))
+
+
+def kvx_repack(plan: Plan, src_shards, cache, scales, block_table, bt_stride: int,
+               stream=None) -> None:
+    _check(_lib.kvx_repack(plan, _shard_array(src_shards), _addr(cache), _addr(scales),
+                           _addr(block_table), bt_stride, _stream(stream)))
+
+
+def kvx_check_block_table(plan: Plan, host_block_table, bt_stride: int) -> None:
+    """host_block_table: a contiguous int32 numpy array or CPU tensor."""
+    if isinstance(host_block_table, torch.Tensor):
+        assert host_block_table.device.type == "cpu" and host_block_table.dtype == torch.int32
+        keep = host_block_table.contiguous()
+        ptr = keep.data_ptr()
+    else:
+        import numpy as np
+        keep = np.ascontiguousarray(host_block_table, dtype=np.int32)
+        ptr = keep.ctypes.data
+    _check(_lib.kvx_check_block_table(plan, ptr, bt_stride))
+    del keep
+
+
+def kvx_last_error() -> str:
+    return _lib.kvx_last_error().decode()
+
+
+def kvx_abi_version() -> int:
+    return int(_lib.kvx_abi_version())

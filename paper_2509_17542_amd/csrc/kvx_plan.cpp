@@ -1,0 +1,401 @@
+// Host side of the C ABI: problem validation, the plan (head-shard map,
+// request offsets, work items, transfer-tensor segments, byte accounting),
+// argument checks and launch dispatch.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kvx.h"
+#include "kvx_internal.h"
+
+using kvx::Item;
+using kvx::ReqInfo;
+
+struct kvx_plan_s {
+    kvx_desc d;                   // seq_lens points into lens
+    std::vector<int32_t> lens;
+    std::vector<ReqInfo> reqs;
+    std::vector<Item> items;
+    int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
+    int first_shard = 0, num_read_shards = 0;
+    int cpr = 0, lg_lpr = 0;
+    uint32_t head_src[kvx::kMaxHeadsPerRank] = {};
+    int32_t max_blocks = 0;
+    uint64_t wire_bytes = 0;
+    int64_t total_tokens = 0;
+    int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
+    int device = -1;
+    void* dev_table = nullptr;    // [items][reqs]
+    const Item* dev_items = nullptr;
+    const ReqInfo* dev_reqs = nullptr;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kvx_status fail(kvx_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+kvx_status fail(kvx_status s, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+int dtype_size(int dt) { return dt == KVX_FP8_E4M3FN ? 1 : 2; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+// conversion kernel variant for a dtype pair, or -1 if unsupported
+int pick_conv(int s, int d)
+{
+    if (s != KVX_FP16 && s != KVX_BF16) return -1;
+    if (s == d) return kvx::kCopy16;
+    if (s == KVX_FP16 && d == KVX_BF16) return kvx::kF16Bf16;
+    if (s == KVX_BF16 && d == KVX_FP8_E4M3FN) return kvx::kBf16E4m3;
+    if (s == KVX_FP16 && d == KVX_FP8_E4M3FN) return kvx::kF16E4m3;
+    return -1;
+}
+
+kvx_status validate(const kvx_desc* d)
+{
+    if (d->num_layers <= 0 || d->num_kv_heads <= 0 || d->head_dim <= 0)
+        return fail(KVX_EINVAL, "num_layers, num_kv_heads and head_dim must be >= 1");
+    if (d->src_tp <= 0 || d->dst_tp <= 0)
+        return fail(KVX_EINVAL, "src_tp and dst_tp must be >= 1");
+    if (d->num_kv_heads % d->src_tp || d->num_kv_heads % d->dst_tp)
+        return fail(KVX_EINVAL, "num_kv_heads (%d) must be divisible by src_tp (%d) and dst_tp (%d)",
+                    d->num_kv_heads, d->src_tp, d->dst_tp);
+    if (d->dst_rank < 0 || d->dst_rank >= d->dst_tp)
+        return fail(KVX_EINVAL, "dst_rank %d outside [0, %d)", d->dst_rank, d->dst_tp);
+    if (d->block_size <= 0) return fail(KVX_EINVAL, "block_size must be >= 1");
+    if (d->num_blocks <= 0) return fail(KVX_EINVAL, "num_blocks must be >= 1");
+    if (d->num_requests < 0) return fail(KVX_EINVAL, "num_requests must be >= 0");
+    if (d->num_requests > 0 && !d->seq_lens) return fail(KVX_EINVAL, "seq_lens is NULL");
+    for (int r = 0; r < d->num_requests; ++r)
+        if (d->seq_lens[r] < 0) return fail(KVX_EINVAL, "seq_lens[%d] < 0", r);
+    if (d->src_order != KVX_THD && d->src_order != KVX_HTD)
+        return fail(KVX_EINVAL, "unknown src_order %d", d->src_order);
+    if (d->src_dtype != KVX_FP16 && d->src_dtype != KVX_BF16 && d->src_dtype != KVX_FP8_E4M3FN)
+        return fail(KVX_EINVAL, "unknown src_dtype %d", d->src_dtype);
+    if (d->dst_dtype != KVX_FP16 && d->dst_dtype != KVX_BF16 && d->dst_dtype != KVX_FP8_E4M3FN)
+        return fail(KVX_EINVAL, "unknown dst_dtype %d", d->dst_dtype);
+    if (pick_conv(d->src_dtype, d->dst_dtype) < 0)
+        return fail(KVX_EUNSUPPORTED, "dtype pair %d -> %d is not supported", d->src_dtype,
+                    d->dst_dtype);
+    if ((int64_t(d->head_dim) * dtype_size(d->src_dtype)) % 16 ||
+        (int64_t(d->head_dim) * dtype_size(d->dst_dtype)) % 16)
+        return fail(KVX_EINVAL, "head_dim %d: rows must be whole 16-byte vectors on both sides",
+                    d->head_dim);
+    if (int64_t(d->head_dim) * dtype_size(d->dst_dtype) > 16 * kvx::kMaxRowChunks)
+        return fail(KVX_EUNSUPPORTED, "destination rows above %d bytes", 16 * kvx::kMaxRowChunks);
+    if (d->num_kv_heads / d->dst_tp > kvx::kMaxHeadsPerRank)
+        return fail(KVX_EUNSUPPORTED, "more than %d heads per decode rank", kvx::kMaxHeadsPerRank);
+    if (d->num_kv_heads / d->src_tp > 65535)
+        return fail(KVX_EUNSUPPORTED, "more than 65535 heads per source shard");
+    if (int64_t(d->num_layers) * 2 > 65535)
+        return fail(KVX_EUNSUPPORTED, "2 * num_layers above 65535");
+    return KVX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t kvx_abi_version(void) { return KVX_ABI_VERSION; }
+
+const char* kvx_last_error(void) { return g_last_error.c_str(); }
+
+kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
+{
+    if (!desc || !out) return fail(KVX_EINVAL, "NULL desc or out");
+    *out = nullptr;
+    kvx_status st = validate(desc);
+    if (st != KVX_OK) return st;
+
+    kvx_plan_s* p = new (std::nothrow) kvx_plan_s();
+    if (!p) return fail(KVX_ENOMEM, "host allocation failed");
+    const kvx_desc& d = *desc;
+    p->d = d;
+    p->lens.assign(d.seq_lens, d.seq_lens + d.num_requests);
+    p->d.seq_lens = p->lens.data();
+    p->hs = d.num_kv_heads / d.src_tp;
+    p->hd = d.num_kv_heads / d.dst_tp;
+    p->esz_src = dtype_size(d.src_dtype);
+    p->esz_dst = dtype_size(d.dst_dtype);
+    p->conv = pick_conv(d.src_dtype, d.dst_dtype);
+
+    // parallel-strategy alignment: decode head i -> global g -> (shard, head)
+    const int g0 = d.dst_rank * p->hd;
+    p->first_shard = g0 / p->hs;
+    const int last_shard = (g0 + p->hd - 1) / p->hs;
+    p->num_read_shards = last_shard - p->first_shard + 1;
+    if (p->num_read_shards > kvx::kMaxReadShards) {
+        delete p;
+        return fail(KVX_EUNSUPPORTED, "decode rank reads more than %d shards", kvx::kMaxReadShards);
+    }
+    for (int i = 0; i < p->hd; ++i) {
+        const int g = g0 + i;
+        p->head_src[i] = (uint32_t(g / p->hs - p->first_shard) << 16) | uint32_t(g % p->hs);
+    }
+
+    // lanes per row: the smallest power of two covering the row's 16-byte chunks
+    p->cpr = d.head_dim * p->esz_dst / 16;
+    while ((1 << p->lg_lpr) < p->cpr) ++p->lg_lpr;
+
+    // requests: source offsets, transfer-tensor segments, work items
+    const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
+    const int64_t L2 = int64_t(d.num_layers) * 2;
+    int64_t src_off = 0, wire = 0, nitems = 0;
+    p->reqs.resize(std::max(d.num_requests, 1));
+    for (int r = 0; r < d.num_requests; ++r) {
+        const int64_t T = p->lens[r];
+        const int64_t rows = L2 * T * p->hd;
+        ReqInfo& q = p->reqs[r];
+        q.src_base = src_off;
+        q.tokens = int32_t(T);
+        q.pad = 0;
+        src_off += L2 * T * p->hs * d.head_dim;
+        wire = align256(wire);
+        q.wire_data = wire;
+        wire += rows * d.head_dim * p->esz_dst;
+        if (fp8) {
+            wire = align256(wire);
+            q.wire_scale = wire;
+            wire += rows * 4;
+        } else {
+            q.wire_scale = -1;
+        }
+        const int64_t nb = (T + d.block_size - 1) / d.block_size;
+        p->max_blocks = std::max<int64_t>(p->max_blocks, nb);
+        nitems += nb;
+        p->total_tokens += T;
+        p->elems_rows += rows;
+    }
+    p->wire_bytes = uint64_t(align256(wire));
+    if (nitems > kvx::kMaxItems) {
+        delete p;
+        return fail(KVX_EUNSUPPORTED, "more than %d logical pages", kvx::kMaxItems);
+    }
+    p->items.reserve(size_t(std::max<int64_t>(nitems, 1)));
+    for (int r = 0; r < d.num_requests; ++r) {
+        const int nb = (p->lens[r] + d.block_size - 1) / d.block_size;
+        for (int k = 0; k < nb; ++k) p->items.push_back(Item{r, k});
+    }
+    if (p->items.empty()) p->items.push_back(Item{0, 0});  // keeps the table non-empty
+
+    // device table on the current device, when one is usable
+    int dev = -1;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0) {
+        const size_t ib = p->items.size() * sizeof(Item);
+        const size_t rb = p->reqs.size() * sizeof(ReqInfo);
+        const size_t ioff = 0, roff = (ib + 255) & ~size_t(255);
+        void* t = nullptr;
+        if (hipMalloc(&t, roff + rb) != hipSuccess) {
+            delete p;
+            return fail(KVX_ENOMEM, "device table allocation failed");
+        }
+        if (hipMemcpy(static_cast<char*>(t) + ioff, p->items.data(), ib, hipMemcpyHostToDevice) !=
+                hipSuccess ||
+            hipMemcpy(static_cast<char*>(t) + roff, p->reqs.data(), rb, hipMemcpyHostToDevice) !=
+                hipSuccess) {
+            (void)hipFree(t);
+            delete p;
+            return fail(KVX_EDEVICE, "device table upload failed");
+        }
+        p->device = dev;
+        p->dev_table = t;
+        p->dev_items = reinterpret_cast<const Item*>(static_cast<char*>(t) + ioff);
+        p->dev_reqs = reinterpret_cast<const ReqInfo*>(static_cast<char*>(t) + roff);
+    } else {
+        (void)hipGetLastError();  // no device: host-only plan
+    }
+    // the real item count (the placeholder item is never launched)
+    if (nitems == 0) p->items.clear();
+    *out = p;
+    return KVX_OK;
+}
+
+kvx_status kvx_plan_info_get(const kvx_plan_t* p, kvx_plan_info* info)
+{
+    if (!p || !info) return fail(KVX_EINVAL, "NULL plan or info");
+    std::memset(info, 0, sizeof *info);
+    const int64_t D = p->d.head_dim;
+    const int64_t rd = p->elems_rows * D * p->esz_src;
+    const int64_t wr = p->elems_rows * D * p->esz_dst +
+                       (p->d.dst_dtype == KVX_FP8_E4M3FN ? p->elems_rows * 4 : 0);
+    info->wire_bytes = p->wire_bytes;
+    info->total_tokens = p->total_tokens;
+    info->read_bytes_pack = rd;
+    info->write_bytes_pack = wr;
+    info->read_bytes_unpack = wr;
+    info->write_bytes_unpack = wr;
+    info->read_bytes_repack = rd;
+    info->write_bytes_repack = wr;
+    info->max_blocks_per_request = p->max_blocks;
+    info->num_items = int32_t(p->items.size());
+    info->device = p->device;
+    return KVX_OK;
+}
+
+kvx_status kvx_plan_segment(const kvx_plan_t* p, int32_t r, int64_t* data_off, int64_t* scale_off)
+{
+    if (!p) return fail(KVX_EINVAL, "NULL plan");
+    if (r < 0 || r >= p->d.num_requests)
+        return fail(KVX_EINVAL, "request %d outside [0, %d)", r, p->d.num_requests);
+    if (data_off) *data_off = p->reqs[r].wire_data;
+    if (scale_off) *scale_off = p->reqs[r].wire_scale;
+    return KVX_OK;
+}
+
+kvx_status kvx_plan_destroy(kvx_plan_t* p)
+{
+    if (!p) return KVX_OK;
+    if (p->dev_table) (void)hipFree(p->dev_table);
+    delete p;
+    return KVX_OK;
+}
+
+kvx_status kvx_check_block_table(const kvx_plan_t* p, const int32_t* bt, int32_t bt_stride)
+{
+    if (!p) return fail(KVX_EINVAL, "NULL plan");
+    if (p->items.empty()) return KVX_OK;
+    if (!bt) return fail(KVX_EINVAL, "NULL block table");
+    if (bt_stride < p->max_blocks)
+        return fail(KVX_EINVAL, "bt_stride %d < max_blocks_per_request %d", bt_stride, p->max_blocks);
+    std::vector<int32_t> used;
+    used.reserve(p->items.size());
+    for (int r = 0; r < p->d.num_requests; ++r) {
+        const int nb = (p->lens[r] + p->d.block_size - 1) / p->d.block_size;
+        for (int k = 0; k < nb; ++k) {
+            const int32_t b = bt[int64_t(r) * bt_stride + k];
+            if (b < 0 || b >= p->d.num_blocks)
+                return fail(KVX_EINVAL, "block_table[%d][%d] = %d outside [0, %lld)", r, k, b,
+                            (long long)p->d.num_blocks);
+            used.push_back(b);
+        }
+    }
+    std::sort(used.begin(), used.end());
+    for (size_t k = 1; k < used.size(); ++k)
+        if (used[k] == used[k - 1]) return fail(KVX_EINVAL, "page %d is used twice", used[k]);
+    return KVX_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Shared argument checks of the launch calls; fills the kernel arguments.
+kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, const void* wire,
+                   void* dst, float* scales, const int32_t* bt, int32_t bt_stride, kvx::KArgs& a)
+{
+    if (!p) return fail(KVX_EINVAL, "NULL plan");
+    const bool fp8 = p->d.dst_dtype == KVX_FP8_E4M3FN;
+    std::memset(&a, 0, sizeof a);
+    if (mode != kvx::kUnpack) {
+        if (!shards) return fail(KVX_EINVAL, "NULL src_shards array");
+        for (int k = 0; k < p->num_read_shards; ++k) {
+            const void* s = shards[p->first_shard + k];
+            if (!s) return fail(KVX_EINVAL, "src_shards[%d] is NULL", p->first_shard + k);
+            if (!aligned16(s))
+                return fail(KVX_EINVAL, "src_shards[%d] is not 16-byte aligned", p->first_shard + k);
+            a.src[k] = s;
+        }
+    } else {
+        if (!wire) return fail(KVX_EINVAL, "NULL transfer tensor");
+        if (!aligned16(wire)) return fail(KVX_EINVAL, "transfer tensor not 16-byte aligned");
+        a.wire_in = wire;
+    }
+    if (!dst) return fail(KVX_EINVAL, mode == kvx::kPack ? "NULL transfer tensor" : "NULL cache");
+    if (!aligned16(dst)) return fail(KVX_EINVAL, "destination not 16-byte aligned");
+    if (mode != kvx::kPack) {
+        if (fp8 != (scales != nullptr))
+            return fail(KVX_EINVAL, fp8 ? "e4m3fn destination needs a scales buffer"
+                                        : "scales given for a 16-bit destination");
+        if (scales && !aligned16(scales)) return fail(KVX_EINVAL, "scales not 16-byte aligned");
+        if (!p->items.empty() && !bt) return fail(KVX_EINVAL, "NULL block table");
+        if (bt_stride < p->max_blocks)
+            return fail(KVX_EINVAL, "bt_stride %d < max_blocks_per_request %d", bt_stride,
+                        p->max_blocks);
+    }
+    if (p->device < 0) return fail(KVX_EDEVICE, "plan has no device tables (no HIP device)");
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != p->device)
+        return fail(KVX_EDEVICE, "current device %d is not the plan's device %d", cur, p->device);
+
+    const kvx_desc& d = p->d;
+    a.dst = dst;
+    a.dscale = scales;
+    a.items = p->dev_items;
+    a.reqs = p->dev_reqs;
+    a.bt = bt;
+    a.num_blocks = d.num_blocks;
+    a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_dst;
+    a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
+    a.bt_stride = bt_stride;
+    a.block_size = d.block_size;
+    a.hs = p->hs;
+    a.hd = p->hd;
+    a.head_dim = d.head_dim;
+    a.row_dst_bytes = d.head_dim * p->esz_dst;
+    a.cpr = p->cpr;
+    a.lg_lpr = p->lg_lpr;
+    const int rpp = kvx::kThreads >> p->lg_lpr;
+    a.dq = rpp / p->hd;
+    a.dr = rpp % p->hd;
+    std::memcpy(a.head_src, p->head_src, sizeof a.head_src);
+    return KVX_OK;
+}
+
+kvx_status run(const kvx_plan_t* p, int mode, const kvx::KArgs& a, void* stream)
+{
+    if (p->items.empty()) return KVX_OK;
+    int conv = p->conv;
+    if (mode == kvx::kUnpack) conv = p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
+    const int err = kvx::launch(mode, conv, p->d.src_order, a, int64_t(p->items.size()),
+                                2 * p->d.num_layers, stream);
+    if (err != 0)
+        return fail(KVX_EDEVICE, "kernel launch failed: %s", hipGetErrorString(hipError_t(err)));
+    return KVX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+kvx_status kvx_pack(const kvx_plan_t* p, const void* const* shards, void* wire, void* stream)
+{
+    kvx::KArgs a;
+    kvx_status st = prepare(p, kvx::kPack, shards, nullptr, wire, nullptr, nullptr, 0, a);
+    return st != KVX_OK ? st : run(p, kvx::kPack, a, stream);
+}
+
+kvx_status kvx_unpack(const kvx_plan_t* p, const void* wire, void* cache, float* scales,
+                      const int32_t* bt, int32_t bt_stride, void* stream)
+{
+    kvx::KArgs a;
+    kvx_status st = prepare(p, kvx::kUnpack, nullptr, wire, cache, scales, bt, bt_stride, a);
+    return st != KVX_OK ? st : run(p, kvx::kUnpack, a, stream);
+}
+
+kvx_status kvx_repack(const kvx_plan_t* p, const void* const* shards, void* cache, float* scales,
+                      const int32_t* bt, int32_t bt_stride, void* stream)
+{
+    kvx::KArgs a;
+    kvx_status st = prepare(p, kvx::kRepack, shards, nullptr, cache, scales, bt, bt_stride, a);
+    return st != KVX_OK ? st : run(p, kvx::kRepack, a, stream);
+}
+
+}  // extern "C"

@@ -88,8 +88,9 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd).
     Casts: same type = bits; fp16->bf16 = torch .to(bfloat16);
     e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn)."""
-    x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers)).to(_TDT[w.src_dtype])
-    x = x[:, :, w.dst_rank * w.hd:(w.dst_rank + 1) * w.hd]        # [L][2][Hd][T][D]
+    heads = (w.dst_rank * w.hd, (w.dst_rank + 1) * w.hd)
+    x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers, heads))
+    x = x.to(_TDT[w.src_dtype])                                     # [L][2][Hd][T][D]
     x = x.permute(0, 1, 3, 2, 4).contiguous()                      # [L][2][T][Hd][D]
     if w.dst_dtype == w.src_dtype:
         return x.view(torch.uint8).numpy().reshape(*x.shape[:4], -1), None

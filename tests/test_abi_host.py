@@ -1,0 +1,163 @@
+"""Host side of the C ABI (runs without a GPU): the library loads and exports
+every entry point declared in include/kvx.h; plans validate their problem,
+report the algorithmic byte counts and transfer-tensor segments; argument
+errors come back as status codes."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from cases import SMALL, FULL, oracle_problem
+from conftest import ROOT
+
+import oracle as O
+import workload as W
+
+K = pytest.importorskip("paper_2509_17542_amd")
+
+
+def declared_entry_points():
+    with open(os.path.join(ROOT, "include", "kvx.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:kvx_status|const char \*|int32_t)\s*\*?\s*(kvx_\w+)\s*\(",
+                                 text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_entry_points()
+    assert len(names) == 10, names
+    for n in names:
+        assert hasattr(K._lib, n), n
+    assert sorted(K.EXPORTS) == names
+    assert K.kvx_abi_version() == 1
+
+
+def desc_for(w, lens, **over):
+    f = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
+    kw = dict(num_layers=w.layers, num_kv_heads=w.heads, head_dim=w.head_dim, src_tp=w.src_tp,
+              dst_tp=w.dst_tp, dst_rank=w.dst_rank, src_dtype=f[w.src_dtype],
+              dst_dtype=f[w.dst_dtype], src_order=K.THD if w.src_order == "thd" else K.HTD,
+              block_size=w.block_size, num_blocks=w.num_blocks, seq_lens=list(lens))
+    kw.update(over)
+    return K.make_desc(**kw)
+
+
+@pytest.mark.parametrize("name", list(SMALL) + list(FULL))
+def test_plan_bytes_and_segments(name):
+    w = (SMALL | FULL)[name]
+    lens = W.seq_lens(w)
+    plan = K.kvx_plan(desc_for(w, lens))
+    info = K.kvx_plan_info_get(plan)
+    esz_s, esz_d = 2, (1 if w.dst_dtype == "e4m3fn" else 2)
+    rows = w.layers * 2 * int(lens.sum()) * w.hd
+    rd = rows * w.head_dim * esz_s
+    wr = rows * w.head_dim * esz_d + (rows * 4 if w.dst_dtype == "e4m3fn" else 0)
+    assert (info.read_bytes_repack, info.write_bytes_repack) == (rd, wr)
+    assert (info.read_bytes_pack, info.write_bytes_pack) == (rd, wr)
+    assert (info.read_bytes_unpack, info.write_bytes_unpack) == (wr, wr)
+    nb = [(int(t) + w.block_size - 1) // w.block_size for t in lens]
+    assert info.max_blocks_per_request == max(nb + [0])
+    assert info.num_items == sum(nb)
+    assert info.total_tokens == int(lens.sum())
+    # transfer-tensor segments agree with the oracle's layout
+    doff, soff, total = O.wire_layout(oracle_problem(O, w, lens))
+    assert info.wire_bytes == total
+    for r in range(len(lens)):
+        assert K.kvx_plan_segment(plan, r) == (int(doff[r]), int(soff[r]))
+
+
+BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_rank=0,
+            src_dtype=1, dst_dtype=2, src_order=0, block_size=16, num_blocks=64, seq_lens=[40, 7])
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(num_layers=0), K.EINVAL), (dict(num_kv_heads=0), K.EINVAL), (dict(head_dim=-64), K.EINVAL),
+    (dict(src_tp=3), K.EINVAL), (dict(dst_tp=3), K.EINVAL), (dict(dst_rank=2), K.EINVAL),
+    (dict(dst_rank=-1), K.EINVAL), (dict(block_size=0), K.EINVAL), (dict(num_blocks=0), K.EINVAL),
+    (dict(seq_lens=[4, -1]), K.EINVAL), (dict(src_order=2), K.EINVAL),
+    (dict(head_dim=4), K.EINVAL),                       # 8-byte rows
+    (dict(head_dim=8, dst_dtype=3), K.EINVAL),          # 8-byte e4m3 rows
+    (dict(src_dtype=3), K.EUNSUPPORTED), (dict(src_dtype=2, dst_dtype=1), K.EUNSUPPORTED),
+    (dict(dst_dtype=9), K.EINVAL), (dict(head_dim=1024), K.EUNSUPPORTED),
+    (dict(num_kv_heads=512, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
+])
+def test_plan_rejects(over, status):
+    kw = dict(BASE)
+    kw.update(over)
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_plan(K.make_desc(**kw))
+    assert e.value.status == status
+    assert K.kvx_last_error()
+
+
+def test_plan_accepts_empty_batches():
+    for lens in ([], [0, 0]):
+        kw = dict(BASE, seq_lens=lens)
+        info = K.kvx_plan_info_get(K.kvx_plan(K.make_desc(**kw)))
+        assert info.num_items == 0 and info.read_bytes_repack == 0
+
+
+def test_segment_out_of_range():
+    plan = K.kvx_plan(K.make_desc(**BASE))
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_plan_segment(plan, 2)
+    assert e.value.status == K.EINVAL
+
+
+def test_launch_argument_errors_before_device():
+    """Pointer and shape errors are reported on the host, before any device
+    work (on a host without a GPU the plan is host-only: EDEVICE last)."""
+    plan = K.kvx_plan(K.make_desc(**BASE))        # fp16 -> bf16, TP1 -> TP2
+    good = 0x10000
+    cases = [
+        (lambda: K.kvx_repack(plan, [None], good, None, good, 3), K.EINVAL),   # NULL shard
+        (lambda: K.kvx_repack(plan, [good + 8], good, None, good, 3), K.EINVAL),  # misaligned
+        (lambda: K.kvx_repack(plan, [good], good + 4, None, good, 3), K.EINVAL),
+        (lambda: K.kvx_repack(plan, [good], good, good, good, 3), K.EINVAL),    # scales w/o fp8
+        (lambda: K.kvx_repack(plan, [good], good, None, None, 3), K.EINVAL),    # NULL table
+        (lambda: K.kvx_repack(plan, [good], good, None, good, 2), K.EINVAL),    # short stride
+        (lambda: K.kvx_unpack(plan, None, good, None, good, 3), K.EINVAL),
+        (lambda: K.kvx_pack(plan, [good], None), K.EINVAL),
+    ]
+    for call, status in cases:
+        with pytest.raises(K.KvxError) as e:
+            call()
+        assert e.value.status == status, K.kvx_last_error()
+    fp8 = K.kvx_plan(K.make_desc(**dict(BASE, dst_dtype=3)))
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_repack(fp8, [good], good, None, good, 3)                      # fp8 needs scales
+    assert e.value.status == K.EINVAL
+
+
+def test_merge_needs_every_overlapping_shard():
+    """Decode rank 1 of TP2 over prefill TP4 reads shards 2 and 3 only; a
+    missing or misaligned one of those is rejected, the others may be NULL.
+    (No call here passes validation, so nothing is ever launched.)"""
+    plan = K.kvx_plan(K.make_desc(**dict(BASE, src_tp=4, dst_tp=2, dst_rank=1)))
+    g = 0x10000
+    for shards in ([None, None, g, None], [None, None, None, g], [g, g, g + 2, g]):
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_repack(plan, shards, g, None, g, 0)
+        assert e.value.status == K.EINVAL
+        assert "src_shards[" in K.kvx_last_error()
+
+
+def test_check_block_table():
+    plan = K.kvx_plan(K.make_desc(**BASE))        # 40 and 7 tokens: 3 + 1 pages
+    ok = np.array([[5, 9, 63], [0, -1, -1]], dtype=np.int32)
+    K.kvx_check_block_table(plan, ok, 3)
+    for bad in ([[5, 9, 64], [0, -1, -1]], [[5, 9, 5], [0, -1, -1]], [[5, 9, 1], [-2, 0, 0]],
+                [[5, 9, 1], [9, 0, 0]]):
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_check_block_table(plan, np.array(bad, dtype=np.int32), 3)
+        assert e.value.status == K.EINVAL
+    with pytest.raises(K.KvxError):
+        K.kvx_check_block_table(plan, ok, 2)
+
+
+def test_workload_block_tables_are_valid():
+    for w in list(SMALL.values()) + [FULL["llama3_8b_bf16_bs16"]]:
+        lens = W.seq_lens(w)
+        bt, stride = W.block_table(w, lens)
+        K.kvx_check_block_table(K.kvx_plan(desc_for(w, lens)), bt, stride)

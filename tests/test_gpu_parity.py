@@ -1,0 +1,239 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, byte for
+byte (layout work and casts are exact, so the tolerance is 0 ULP).
+
+Small cases compare every byte of the destination pool (or transfer tensor),
+sentinels included.  Cast sweeps cover every fp16 pattern and every finite
+bf16 value under many row scales.  Full-size workloads run in the launch
+configuration the benchmark times and are checked on sampled requests and
+planes (every request in the first and last plane), plus sampled unused
+pages."""
+import numpy as np
+import pytest
+import torch
+
+from cases import FULL, SMALL, inputs, oracle_problem
+from gpu_util import (DEV, check_sampled, check_unused_pages, gpu_run, log, oracle_pool)
+
+import oracle as O
+import workload as W
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+@pytest.fixture(autouse=True)
+def _release_device_memory():
+    yield
+    import gc
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _eq(a, b):
+    return np.array_equal(np.asarray(a).view(np.uint8), np.asarray(b).view(np.uint8))
+
+
+# ---- small cases: whole pools ----------------------------------------------------
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_repack_small(name):
+    w = SMALL[name]
+    lens, bt, stride, shards = inputs(w)
+    log(f"repack {name} lens={list(lens)}")
+    cache, scales, _ = gpu_run("repack", w, lens, bt, stride, shards)
+    want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
+    assert _eq(cache.cpu().numpy(), want_c)
+    if want_s is not None:
+        assert _eq(scales.cpu().numpy(), want_s)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_pack_small(name):
+    w = SMALL[name]
+    lens, bt, stride, shards = inputs(w)
+    log(f"pack {name}")
+    _, _, wire = gpu_run("pack", w, lens, bt, stride, shards)
+    want = O.pack(oracle_problem(O, w, lens), shards)
+    got = wire.cpu().numpy()[:want.size]
+    assert _eq(got, want)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_unpack_small(name):
+    """Unpack alone, fed the oracle's transfer tensor."""
+    w = SMALL[name]
+    lens, bt, stride, shards = inputs(w)
+    wire = O.pack(oracle_problem(O, w, lens), shards)
+    log(f"unpack {name}")
+    cache, scales, _ = gpu_run("unpack", w, lens, bt, stride, None, wire_in=wire)
+    want_c, want_s = oracle_pool(w, lens, bt, stride, shards, op="unpack", wire=wire)
+    assert _eq(cache.cpu().numpy(), want_c)
+    if want_s is not None:
+        assert _eq(scales.cpu().numpy(), want_s)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama3_70b_small_r1", "qwen_htd_small", "fp8_small",
+                                  "fp16_e4m3_htd_empty"])
+def test_pack_then_unpack_equals_repack(name):
+    w = SMALL[name]
+    lens, bt, stride, shards = inputs(w)
+    log(f"pack+unpack {name}")
+    c1, s1, _ = gpu_run("pack_unpack", w, lens, bt, stride, shards)
+    c2, s2, _ = gpu_run("repack", w, lens, bt, stride, shards)
+    assert torch.equal(c1, c2)
+    if s1 is not None:
+        assert torch.equal(s1.view(torch.int32), s2.view(torch.int32))
+
+
+def test_page_ids_outside_the_pool_are_skipped():
+    """A block-table entry outside [0, num_blocks) is not a page: nothing is
+    written for it (the kernel's own bounds check), the other pages are."""
+    w = SMALL["llama3_8b_small"]
+    lens, bt, stride, shards = inputs(w)
+    bad = bt.copy()
+    bad[0, 1] = -1
+    bad[1, 0] = w.num_blocks + 5
+    log("repack with out-of-pool page ids")
+    cache, _, _ = gpu_run("repack", w, lens, bad, stride, shards)
+    want, _ = oracle_pool(w, lens, bt, stride, shards)
+    page = w.block_size * w.hd * w.head_dim * 2
+    want = want.reshape(w.layers, 2, w.num_blocks, page)
+    want[:, :, bt[0, 1]] = W.SENTINEL
+    want[:, :, bt[1, 0]] = W.SENTINEL
+    assert _eq(cache.cpu().numpy(), want.reshape(-1))
+
+
+def test_empty_batch_is_a_no_op():
+    w = SMALL["llama3_8b_small"].replace(lens_override=(0, 0), num_requests=2)
+    lens, bt, stride, shards = inputs(w)
+    cache, _, _ = gpu_run("repack", w, lens, bt, stride, shards)
+    assert bool((cache == W.SENTINEL).all())
+
+
+# ---- cast sweeps --------------------------------------------------------------------
+
+def _sweep_case(src, dst, rows_bits):
+    """One request whose 2*T rows (layer 0, k then v) are the given rows
+    (uint16 [2T, 128]); TP1, one head, 16-token pages in order."""
+    n = rows_bits.shape[0]
+    assert n % 32 == 0
+    T = n // 2
+    w = W.Workload("sweep", 1, 1, 1, 128, 1, 1, 0, src, dst, "thd", 16, T // 16, 1, T, T, seed=1)
+    lens = np.array([T], dtype=np.int32)
+    bt = np.arange(T // 16, dtype=np.int32)[None, :]
+    return w, lens, bt, [np.ascontiguousarray(rows_bits.reshape(-1))]
+
+
+def _pad_rows(rows):
+    n = -(-rows.shape[0] // 32) * 32
+    out = np.zeros((n, 128), dtype=np.uint16)
+    out[:rows.shape[0]] = rows
+    return out
+
+
+def test_fp16_to_bf16_every_pattern():
+    rows = np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(512, 128)
+    w, lens, bt, shards = _sweep_case("fp16", "bf16", rows)
+    log("fp16->bf16 all 65536 patterns")
+    cache, _, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
+    want, _ = oracle_pool(w, lens, bt, bt.shape[1], shards)
+    assert _eq(cache.cpu().numpy(), want)
+
+
+def _e4m3_rows(fmt, amaxes, rng):
+    """Rows [amax, x_1..x_127] covering every finite pattern x with |x| <= amax
+    (both signs) for each amax, plus NaN/Inf/zero rows."""
+    allp = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    inf = 0x7C00 if fmt == "fp16" else 0x7F80
+    mag = allp & 0x7FFF
+    finite = allp[mag < inf]
+    out = []
+    for a in amaxes:
+        xs = finite[(finite & 0x7FFF) <= a]
+        xs = rng.permutation(xs)
+        k = -(-xs.size // 127)
+        xs = np.concatenate([xs, np.zeros(k * 127 - xs.size, np.uint16)]).reshape(k, 127)
+        pos = rng.integers(0, 128, k)
+        rows = np.empty((k, 128), np.uint16)
+        for j in range(k):
+            rows[j] = np.insert(xs[j], pos[j], a | (rng.integers(0, 2) << 15))
+        out.append(rows)
+    special = np.zeros((6, 128), np.uint16)
+    special[1, :] = 0x8000                         # all -0
+    special[2, 5] = inf | 0x1                      # a NaN in a zero row
+    special[3, :] = 0x3C00 if fmt == "fp16" else 0x3F80
+    special[3, 7] = inf                            # +Inf sets the row maximum
+    special[4, :64] = (inf | 0x40) | 0x8000        # half NaN, rest zero
+    special[5, :] = rng.integers(0, 0x7800, 128)
+    special[5, 9] = inf | 0x200                    # one NaN among finite values
+    out.append(special)
+    return np.concatenate(out)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_e4m3_sweep(fmt):
+    rng = np.random.default_rng(2024)
+    if fmt == "bf16":
+        # row maxima over the whole bf16 range: subnormal, tiny, around 448,
+        # around the fast-path limits 2^-80 * 448 and 2^100 * 448, the largest
+        amaxes = sorted(set([0x0001, 0x0040, 0x0080, 0x00FF, 0x0100, 0x0F00, 0x1000, 0x1080,
+                             0x3F80, 0x3F81, 0x43E0, 0x43DF, 0x43E1, 0x4000, 0x7F7F, 0x7F00,
+                             0x7200, 0x71FF, 0x7201, 0x2000, 0x1F00, 0x1F80])
+                        | set(rng.integers(1, 0x7F80, 40).tolist()))
+    else:
+        amaxes = sorted(set([0x0001, 0x0200, 0x03FF, 0x0400, 0x3C00, 0x5F00, 0x5EFF, 0x7BFF,
+                             0x1000, 0x2000]) | set(rng.integers(1, 0x7C00, 24).tolist()))
+    rows = _pad_rows(_e4m3_rows(fmt, amaxes, rng))
+    w, lens, bt, shards = _sweep_case(fmt, "e4m3fn", rows)
+    log(f"{fmt}->e4m3fn sweep: {rows.shape[0]} rows, {len(amaxes)} row maxima")
+    cache, scales, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
+    want_c, want_s = oracle_pool(w, lens, bt, bt.shape[1], shards)
+    got_c = cache.cpu().numpy()
+    bad = np.nonzero(got_c != want_c)[0]
+    assert bad.size == 0, f"{bad.size} bytes differ, first at {bad[:8]}"
+    assert _eq(scales.cpu().numpy(), want_s)
+
+
+# ---- full-size workloads (the benchmark's launch configuration) ------------------
+
+def _full_case(name, layer0=0, nlayers=None, extra_planes=2, n_req=4):
+    w = FULL[name]
+    nlayers = nlayers or w.layers
+    rng = np.random.default_rng(7)
+    log(f"full {name}: generating layers {layer0}..{layer0 + nlayers - 1}")
+    lens = W.seq_lens(w)
+    bt, stride = W.block_table(w, lens)
+    shards = W.source_shards(w, lens, layer0, nlayers)
+    log(f"full {name}: repack on GPU ({int(lens.sum())} tokens)")
+    cache, scales, _ = gpu_run("repack", w, lens, bt, stride, shards, nlayers)
+    # every request in the first and the last plane; a few requests in random planes
+    edge = [(0, 0), (nlayers - 1, 1)]
+    n1 = check_sampled(w, lens, bt, shards, cache, scales, nlayers, edge, range(len(lens)), rng)
+    picks = rng.choice(len(lens), min(n_req, len(lens)), replace=False)
+    planes = [(int(rng.integers(nlayers)), int(rng.integers(2))) for _ in range(extra_planes)]
+    n2 = check_sampled(w, lens, bt, shards, cache, scales, nlayers, planes, picks, rng)
+    check_unused_pages(w, lens, bt, cache, nlayers, rng)
+    log(f"full {name}: {n1 + n2} rows checked")
+
+
+def test_full_llama3_8b():
+    _full_case("llama3_8b_bf16_bs16")
+
+
+def test_full_llama3_70b_shard():
+    _full_case("llama3_70b_tp4to2_bf16_bs32")
+
+
+def test_full_qwen7b_htd():
+    _full_case("qwen7b_htd_fp16_bf16_bs64")
+
+
+def test_full_tiny():
+    _full_case("tiny_tp1to2_fp16_bf16")
+
+
+@pytest.mark.parametrize("group", [0, 15])
+def test_full_fp8_decode_layer_group(group):
+    w = FULL["fp8_decode_61l_bf16_e4m3_bs16"]
+    l0, nl = w.group_layers(group)
+    _full_case(w.name, l0, nl, extra_planes=1, n_req=3)

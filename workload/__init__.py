@@ -54,6 +54,8 @@ def lib():
         L.wl_normal.restype = ctypes.c_double
         L.wl_normal.argtypes = [u64, u32, u64]
         L.wl_fill_normal.argtypes = [u64, u32, u64, i64, ctypes.c_double, vp, ctypes.c_int]
+        L.wl_fill_normal_blocks.argtypes = [u64, u32, vp, i64, i64, ctypes.c_double, vp,
+                                            ctypes.c_int]
         L.wl_fill_uniform.argtypes = [u64, u32, u64, i64, vp]
         L.wl_select.restype = i64
         L.wl_select.argtypes = [u64, u32, u64, i64, ctypes.c_double, vp]
@@ -188,31 +190,46 @@ def _request_value_base(w: Workload, lens: np.ndarray, r: int) -> int:
     return int(sum(w.total_layers * 2 * w.heads * int(t) * w.head_dim for t in lens[:r]))
 
 
-def logical_values(w: Workload, lens: np.ndarray, r: int, layer0: int, nlayers: int) -> np.ndarray:
-    """float32 values of request r, layers [layer0, layer0+nlayers), shaped
-    [layer][k/v][global head][token][dim]."""
+def logical_values(w: Workload, lens: np.ndarray, r: int, layer0: int, nlayers: int,
+                   heads: tuple[int, int] | None = None, out: np.ndarray | None = None
+                   ) -> np.ndarray:
+    """float32 values of request r, layers [layer0, layer0+nlayers), global
+    heads [g0, g1) (default all), shaped [layer][k/v][head][token][dim].
+
+    Element (l, kv, g, t, d) is draw number
+    base(r) + (((l*2 + kv)*H + g)*T + t)*D + d of the value stream, base(r)
+    being the element count of all earlier requests over all layers."""
     T = int(lens[r])
     H, D = w.heads, w.head_dim
-    n = nlayers * 2 * H * T * D
-    start = _request_value_base(w, lens, r) + layer0 * 2 * H * T * D
-    x = np.empty(n, dtype=np.float32)
-    if n:
-        lib().wl_fill_normal(w.seed, S_VALUES, start, n, w.sigma, x.ctypes.data, _threads())
-    x = x.reshape(nlayers, 2, H, T, D)
-    if w.head_scale_log10 is not None and n:
+    g0, g1 = heads if heads is not None else (0, H)
+    shape = (nlayers, 2, g1 - g0, T, D)
+    if out is not None:   # caller-provided scratch (reused, so no fresh pages per request)
+        x = out.reshape(-1)[:int(np.prod(shape))].reshape(shape)
+    else:
+        x = np.empty(shape, dtype=np.float32)
+    if x.size == 0:
+        return x
+    base = _request_value_base(w, lens, r)
+    n = T * D
+    # one block of T*D consecutive draws per (layer, k/v, head)
+    li, kv, g = np.meshgrid(np.arange(nlayers), np.arange(2), np.arange(g0, g1), indexing="ij")
+    starts = (base + (((layer0 + li) * 2 + kv) * H + g) * n).astype(np.uint64).reshape(-1)
+    lib().wl_fill_normal_blocks(w.seed, S_VALUES, starts.ctypes.data, starts.size, n, w.sigma,
+                                x.ctypes.data, _threads())
+    if w.outlier_frac > 0:
+        flat_all = x.reshape(starts.size, n)
+        idx = np.empty(n, dtype=np.int64)
+        for b, start in enumerate(starts.tolist()):
+            c = lib().wl_select(w.seed, S_OUTLIER, start, n, w.outlier_frac, idx.ctypes.data)
+            for k in idx[:c]:
+                neg = lib().wl_uniform(w.seed, S_OUTSIGN, start + int(k)) < 0.5
+                flat_all[b, k] = -w.outlier_value if neg else w.outlier_value
+    if w.head_scale_log10 is not None:
         lo, hi = w.head_scale_log10
         u = np.empty(w.total_layers * 2 * H, dtype=np.float64)
         lib().wl_fill_uniform(w.seed, S_HEADSCALE, 0, u.size, u.ctypes.data)
-        s = (10.0 ** (lo + (hi - lo) * u)).astype(np.float32).reshape(w.total_layers, 2, H)
-        x *= s[layer0:layer0 + nlayers, :, :, None, None]
-    if w.outlier_frac > 0 and n:
-        idx = np.empty(n, dtype=np.int64)
-        c = lib().wl_select(w.seed, S_OUTLIER, start, n, w.outlier_frac, idx.ctypes.data)
-        idx = idx[:c]
-        flat = x.reshape(-1)
-        for k in idx:
-            neg = lib().wl_uniform(w.seed, S_OUTSIGN, start + int(k)) < 0.5
-            flat[k] = -w.outlier_value if neg else w.outlier_value
+        sc = (10.0 ** (lo + (hi - lo) * u)).astype(np.float32).reshape(w.total_layers, 2, H)
+        x *= sc[layer0:layer0 + nlayers, :, g0:g1, None, None]
     return x
 
 
@@ -220,9 +237,12 @@ def _to_bits(x: np.ndarray, dtype: str) -> np.ndarray:
     """Round float32 to the 16-bit storage type (torch's round-to-nearest-even)
     and return the bit patterns as uint16."""
     import torch
-    tdt = {"fp16": torch.float16, "bf16": torch.bfloat16}[dtype]
-    t = torch.from_numpy(x).to(tdt)
+    t = torch.from_numpy(x).to(_TORCH_DTYPE[dtype]())
     return t.view(torch.int16).numpy().view(np.uint16)
+
+
+_TORCH_DTYPE = {"fp16": lambda: __import__("torch").float16,
+                "bf16": lambda: __import__("torch").bfloat16}
 
 
 def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int | None = None,
@@ -231,7 +251,9 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
 
     Shard j holds global heads [j*Hs, (j+1)*Hs); requests are stored back to
     back, each as [layer][k/v][token][head][dim] ("thd") or
-    [layer][k/v][head][token][dim] ("htd").  Shards not listed are None."""
+    [layer][k/v][head][token][dim] ("htd").  Values are rounded from float32
+    to the storage type by torch (round to nearest even).  Shards not listed
+    are None."""
     import torch
     if nlayers is None:
         nlayers = w.layers
@@ -241,19 +263,22 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
     per_shard = sum(nlayers * 2 * int(t) * Hs * D for t in lens)
     out: list[np.ndarray | None] = [None] * w.src_tp
     for j in shards:
-        out[j] = np.empty(per_shard, dtype=np.uint16)
+        out[j] = np.empty(per_shard, dtype=np.uint16)   # first touched by torch's copy below
+    scratch = np.empty(max([nlayers * 2 * int(t) * Hs * D for t in lens] + [1]), np.float32)
+    tdt = _TORCH_DTYPE[w.src_dtype]()
     off = 0
     for r in range(len(lens)):
         T = int(lens[r])
         n = nlayers * 2 * T * Hs * D
         if n == 0:
             continue
-        bits = _to_bits(logical_values(w, lens, r, layer0, nlayers), w.src_dtype)
-        tb = torch.from_numpy(bits.view(np.int16))
         for j in shards:
-            part = tb[:, :, j * Hs:(j + 1) * Hs]
+            vals = torch.from_numpy(
+                logical_values(w, lens, r, layer0, nlayers, (j * Hs, (j + 1) * Hs), scratch))
+            dst = torch.from_numpy(out[j][off:off + n].view(np.int16)).view(tdt)
             if w.src_order == "thd":
-                part = part.permute(0, 1, 3, 2, 4)
-            out[j][off:off + n] = part.contiguous().numpy().reshape(-1).view(np.uint16)
+                dst.view(nlayers, 2, T, Hs, D).copy_(vals.permute(0, 1, 3, 2, 4))
+            else:
+                dst.view(nlayers, 2, Hs, T, D).copy_(vals)
         off += n
     return out

@@ -14,6 +14,7 @@
  * Normals: Box-Muller on the uniform pair (2k, 2k+1); element 2k takes the
  * cosine branch and 2k+1 the sine branch.
  */
+#define _GNU_SOURCE
 #include <math.h>
 #include <pthread.h>
 #include <stdint.h>
@@ -36,68 +37,101 @@ double wl_uniform(uint64_t seed, uint32_t stream, uint64_t i)
     return (double)(wl_word(seed, stream, i) >> 11) * 0x1.0p-53;
 }
 
-double wl_normal(uint64_t seed, uint32_t stream, uint64_t i)
+
+/* One pair (2k, 2k+1) of the normal stream: Box-Muller, radius from 1 - u1
+ * in (0, 1]. */
+static inline void normal_pair(uint64_t seed, uint32_t stream, uint64_t k, double *z0, double *z1)
 {
-    uint64_t k = i >> 1;
     double u1 = wl_uniform(seed, stream, 2 * k);
     double u2 = wl_uniform(seed, stream, 2 * k + 1);
-    double rad = sqrt(-2.0 * log(1.0 - u1)); /* 1 - u1 in (0, 1] */
-    double ang = 6.283185307179586476925286766559 * u2;
-    return (i & 1) ? rad * sin(ang) : rad * cos(ang);
+    double rad = sqrt(-2.0 * log(1.0 - u1));
+    double sn, cs;
+    sincos(6.283185307179586476925286766559 * u2, &sn, &cs);
+    *z0 = rad * cs;
+    *z1 = rad * sn;
+}
+
+/* out[k] = sigma * normal(first + k) for k in [lo, hi) of a run */
+static void fill_run(uint64_t seed, uint32_t stream, uint64_t first, int64_t lo, int64_t hi,
+                     double sigma, float *out)
+{
+    int64_t k = lo;
+    double z0, z1;
+    if (k < hi && ((first + (uint64_t)k) & 1)) {
+        normal_pair(seed, stream, (first + (uint64_t)k) >> 1, &z0, &z1);
+        out[k] = (float)(sigma * z1);
+        ++k;
+    }
+    for (; k + 1 < hi; k += 2) {
+        normal_pair(seed, stream, (first + (uint64_t)k) >> 1, &z0, &z1);
+        out[k] = (float)(sigma * z0);
+        out[k + 1] = (float)(sigma * z1);
+    }
+    if (k < hi) {
+        normal_pair(seed, stream, (first + (uint64_t)k) >> 1, &z0, &z1);
+        out[k] = (float)(sigma * z0);
+    }
 }
 
 typedef struct {
     uint64_t seed;
     uint32_t stream;
-    uint64_t first;
-    int64_t lo, hi;
+    const uint64_t *starts;  /* first draw index of each block */
+    int64_t block_len;
+    int64_t lo, hi;          /* flat output range of this thread */
     double sigma;
     float *out;
 } fill_job;
 
-static void *fill_normal_worker(void *arg)
+static void *fill_worker(void *arg)
 {
     fill_job *j = (fill_job *)arg;
     int64_t k = j->lo;
-    /* leading odd element */
-    if (k < j->hi && ((j->first + (uint64_t)k) & 1)) {
-        j->out[k] = (float)(j->sigma * wl_normal(j->seed, j->stream, j->first + (uint64_t)k));
-        ++k;
+    while (k < j->hi) {
+        int64_t b = k / j->block_len, in = k - b * j->block_len;
+        int64_t end = (b + 1) * j->block_len < j->hi ? (b + 1) * j->block_len : j->hi;
+        fill_run(j->seed, j->stream, j->starts[b], in, in + (end - k), j->sigma,
+                 j->out + b * j->block_len);
+        k = end;
     }
-    for (; k + 1 < j->hi; k += 2) { /* both branches of one Box-Muller pair */
-        uint64_t i = j->first + (uint64_t)k;
-        double u1 = wl_uniform(j->seed, j->stream, i);
-        double u2 = wl_uniform(j->seed, j->stream, i + 1);
-        double rad = sqrt(-2.0 * log(1.0 - u1));
-        double ang = 6.283185307179586476925286766559 * u2;
-        j->out[k] = (float)(j->sigma * rad * cos(ang));
-        j->out[k + 1] = (float)(j->sigma * rad * sin(ang));
-    }
-    if (k < j->hi)
-        j->out[k] = (float)(j->sigma * wl_normal(j->seed, j->stream, j->first + (uint64_t)k));
     return NULL;
 }
 
-/* out[k] = sigma * normal(stream, first + k), k in [0, n) */
-void wl_fill_normal(uint64_t seed, uint32_t stream, uint64_t first, int64_t n, double sigma,
-                    float *out, int nthreads)
+/* out[b*block_len + k] = sigma * normal(starts[b] + k), b < nblocks, k < block_len */
+void wl_fill_normal_blocks(uint64_t seed, uint32_t stream, const uint64_t *starts, int64_t nblocks,
+                           int64_t block_len, double sigma, float *out, int nthreads)
 {
-    if (nthreads < 1) nthreads = 1;
+    int64_t n = nblocks * block_len;
     if (nthreads > 64) nthreads = 64;
-    if (n < (int64_t)1 << 20) nthreads = 1;
+    if (nthreads > n / 65536) nthreads = (int)(n / 65536); /* at least 64Ki draws per thread */
+    if (nthreads < 1) nthreads = 1;
     pthread_t th[64];
     fill_job jobs[64];
     int64_t per = (n + nthreads - 1) / nthreads;
-    per = (per + 1) & ~(int64_t)1;
     for (int t = 0; t < nthreads; ++t) {
-        jobs[t].seed = seed; jobs[t].stream = stream; jobs[t].first = first;
+        jobs[t].seed = seed; jobs[t].stream = stream; jobs[t].starts = starts;
+        jobs[t].block_len = block_len;
         jobs[t].lo = t * per < n ? t * per : n;
         jobs[t].hi = (t + 1) * per < n ? (t + 1) * per : n;
         jobs[t].sigma = sigma; jobs[t].out = out;
     }
-    if (nthreads == 1) { fill_normal_worker(&jobs[0]); return; }
-    for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, fill_normal_worker, &jobs[t]);
+    if (nthreads == 1) { fill_worker(&jobs[0]); return; }
+    for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, fill_worker, &jobs[t]);
     for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+}
+
+double wl_normal(uint64_t seed, uint32_t stream, uint64_t i)
+{
+    double z0, z1;
+    normal_pair(seed, stream, i >> 1, &z0, &z1);
+    return (i & 1) ? z1 : z0;
+}
+
+/* out[k] = sigma * normal(first + k), k in [0, n) */
+void wl_fill_normal(uint64_t seed, uint32_t stream, uint64_t first, int64_t n, double sigma,
+                    float *out, int nthreads)
+{
+    wl_fill_normal_blocks(seed, stream, &first, 1, n, sigma, out, nthreads);
 }
 
 /* out[k] = uniform(stream, first + k) */
