@@ -49,7 +49,8 @@
  *
  * Errors: every call returns a kvx_status; nothing is thrown and nothing
  * aborts.  kvx_last_error() gives a message for the calling thread's last
- * non-OK status.
+ * non-OK status.  A plan whose requests hold no tokens has nothing to move:
+ * its launch calls return KVX_OK without inspecting any pointer.
  */
 #ifndef KVX_H
 #define KVX_H

@@ -207,8 +207,13 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
             o[d] = (uint8_t)((sign << 7) | 0x7Fu);
         else if (sc == 0.0f)                /* all finite elements are zero */
             o[d] = (uint8_t)(sign << 7);
-        else
-            o[d] = orc_f32_to_e4m3fn(x[d] / sc);
+        else {
+            float v = x[d] / sc;
+            /* An invalid quotient (Inf / Inf, in a row whose maximum is
+             * infinite) has no defined sign; it takes the element's sign, as
+             * every other quotient does (the scale is positive). */
+            o[d] = isnan(v) ? (uint8_t)((sign << 7) | 0x7Fu) : orc_f32_to_e4m3fn(v);
+        }
     }
     free(x);
 }

@@ -304,6 +304,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     if (!p) return fail(KVX_EINVAL, "NULL plan");
     const bool fp8 = p->d.dst_dtype == KVX_FP8_E4M3FN;
     std::memset(&a, 0, sizeof a);
+    if (p->items.empty()) return KVX_OK;  // nothing to read or write: pointers are not used
     if (mode != kvx::kUnpack) {
         if (!shards) return fail(KVX_EINVAL, "NULL src_shards array");
         for (int k = 0; k < p->num_read_shards; ++k) {

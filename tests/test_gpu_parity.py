@@ -165,7 +165,8 @@ def _e4m3_rows(fmt, amaxes, rng):
     special[3, 7] = inf                            # +Inf sets the row maximum
     special[4, :64] = (inf | 0x40) | 0x8000        # half NaN, rest zero
     special[5, :] = rng.integers(0, 0x7800, 128)
-    special[5, 9] = inf | 0x200                    # one NaN among finite values
+    special[5, 9] = inf | 0x20                     # one NaN among finite values
+    special[5, 11] = inf | 0x8000                  # and -Inf: the row maximum is Inf
     out.append(special)
     return np.concatenate(out)
 

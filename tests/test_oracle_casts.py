@@ -201,3 +201,14 @@ def test_same_type_is_bit_copy():
     for f in (O.FP16, O.BF16):
         out, _ = O.convert_row(f, f, bits)
         assert np.array_equal(out.view(np.uint16), bits)
+
+
+def test_e4m3_infinite_row_maximum():
+    """A row holding +-Inf has scale Inf: finite elements give signed zeros,
+    the infinite ones an invalid quotient, whose NaN code takes the element's
+    sign (platform NaN signs differ; the reading fixes it)."""
+    row = torch.tensor([1.0, -2.0, float("inf"), float("-inf"), 0.0, -0.0, 3.0, 1.0],
+                       dtype=torch.float32).to(torch.bfloat16)
+    out, s = O.convert_row(O.BF16, O.E4M3FN, row.view(torch.int16).numpy().view(np.uint16))
+    assert np.isinf(s)
+    assert list(out) == [0x00, 0x80, 0x7F, 0xFF, 0x00, 0x80, 0x00, 0x00]
