@@ -63,6 +63,9 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="time the repack only (no pack/unpack/latency legs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calib-gib", type=float, default=4.0,
+                    help="size of the plain device copy timed as a ceiling (and used to "
+                         "calibrate rocprofv3 byte counters); 0 = skip")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -150,6 +153,22 @@ def main():
         "repack_kernel_ms": {"mean": round(k_mean, 4), "min": round(k_min, 4),
                              "median": round(k_med, 4)},
     }
+    if args.calib_gib > 0:
+        # plain device copies of known size (read N + write N bytes): the HIP
+        # runtime's copy kernel (hipMemcpyAsync device to device) and a torch
+        # elementwise kernel; the references for the byte counters
+        n = int(args.calib_gib * 2**30) // 4
+        a = torch.empty(n, dtype=torch.int32, device="cuda")
+        b = torch.empty_like(a)
+        out["copy_ceiling"] = {}
+        for kind, fn in (("hipMemcpy_d2d", lambda: b.copy_(a)),
+                         ("torch_elementwise", lambda: torch.bitwise_not(a, out=b))):
+            ms, km, _, _ = timed(fn, 10, 2)
+            out["copy_ceiling"][kind] = {"bytes": 8 * n, "kernel_ms": round(km, 4),
+                                         "GB/s": round(8 * n / (km * 1e-3) / 1e9, 1)}
+            log(f"plain copy ({kind}): {8 * n / (km * 1e-3) / 1e9:.0f} GB/s")
+        del a, b
+
     traffic = measured_traffic(w.name)
     out["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

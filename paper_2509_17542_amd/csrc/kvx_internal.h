@@ -8,25 +8,24 @@
 
 namespace kvx {
 
-constexpr int kThreads = 256;           // threads per workgroup (4 wave64)
 constexpr int kMaxHeadsPerRank = 128;   // Hd limit (kernel-argument head table)
 constexpr int kMaxReadShards = 64;      // source shards one decode rank may read
 constexpr int kMaxRowChunks = 64;       // 16-byte destination chunks per row (one wave)
-constexpr int kMaxItems = (1 << 24) - 1;  // workgroups along grid x (x * 256 threads < 2^32)
+constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
+// work units (pages x planes) of one launch; the 1-D grid is this rounded up to
+// a multiple of kXcds, and grid * threads stays below 2^32
+constexpr int64_t kMaxUnits = (int64_t(1) << 22) - kXcds;
 
-// Per request, device resident.
-struct ReqInfo {
+// One logical page of one request, device resident: the unit of work of a
+// workgroup in every (layer, k/v) plane.
+struct Item {
     int64_t src_base;    // element offset of the request in every source shard
-    int64_t wire_data;   // byte offset of its data region in the transfer tensor
+    int64_t wire_data;   // byte offset of the request's data region in the transfer tensor
     int64_t wire_scale;  // byte offset of its scale region, -1 without scales
+    int32_t req;         // request index (block-table row)
+    int32_t blk;         // page index within the request
     int32_t tokens;      // T_r
     int32_t pad;
-};
-
-// One logical page of one request: the unit of work of a workgroup (per plane).
-struct Item {
-    int32_t req;
-    int32_t blk;
 };
 
 enum Mode : int { kPack = 0, kUnpack = 1, kRepack = 2 };
@@ -47,11 +46,13 @@ struct KArgs {
     void* dst;                        // pack: transfer tensor; else cache
     float* dscale;                    // cache scales (unpack/repack, e4m3fn)
     const Item* items;
-    const ReqInfo* reqs;
     const int32_t* bt;
     int64_t num_blocks;
     int64_t plane_bytes;              // cache bytes per (layer, k/v) plane
     int64_t plane_scales;             // cache scales per plane
+    int32_t num_items;                // logical pages per plane
+    int32_t units;                    // num_items * planes
+    int32_t units_per_xcd;            // grid / kXcds
     int32_t bt_stride;
     int32_t block_size;
     int32_t hs;                       // heads per source shard
@@ -64,8 +65,10 @@ struct KArgs {
     uint32_t head_src[kMaxHeadsPerRank];  // (shard slot << 16) | head within shard
 };
 
-// Launch one conversion; returns a hipError_t value (0 = success).
-int launch(int mode, int conv, int order, const KArgs& a, int64_t num_items, int planes,
-           void* stream);
+// threads per workgroup for a conversion (16-bit destinations: 512, e4m3fn: 256)
+int threads_for(int conv);
+
+// Launch one conversion over a.units work units; returns a hipError_t value.
+int launch(int mode, int conv, int order, const KArgs& a, void* stream);
 
 }  // namespace kvx

@@ -2,13 +2,17 @@
 // tensor), unpack (transfer tensor -> paged cache) and the fused repack
 // (source shards -> paged cache).
 //
-// Work decomposition: one workgroup per (logical page of a request, (layer,
-// k/v) plane); grid = (pages over all requests, 2 * layers).  A page holds
-// ntok <= block_size tokens x Hd heads = "rows" of head_dim elements; its
-// destination rows are contiguous in both the paged cache and the transfer
+// Work decomposition: one workgroup per work unit = (logical page of a
+// request, (layer, k/v) plane).  Units are numbered plane-major, so
+// consecutive units read consecutive source bytes.  The 1-D grid is dealt to
+// the 8 XCDs round-robin (workgroup i runs on XCD i % 8); workgroup i is mapped
+// to unit (i % 8) * units_per_xcd + i / 8, so every XCD streams one contiguous
+// run of units through its own L2 instead of every eighth page of the whole
+// stream.  A page holds ntok <= block_size tokens x Hd heads = "rows" of
+// head_dim elements, contiguous in both the paged cache and the transfer
 // tensor.  Each row is covered by a power-of-two group of lanes, one 16-byte
-// destination vector per lane (global_load_dwordx4 / global_store_dwordx4);
-// a workgroup walks its rows in passes of 256 / lanes-per-row rows and keeps
+// destination vector per lane (global_load_dwordx4 / global_store_dwordx4); a
+// workgroup walks its rows in passes of threads / lanes-per-row rows and keeps
 // U rows of loads in flight per lane before the first store.
 //
 // The path is a gather/scatter stream with no reuse and no contraction: it is
@@ -136,8 +140,8 @@ __device__ __forceinline__ uint4 to_bf16x8(const uint4& v)
 
 // ---- the row kernel ----------------------------------------------------------
 
-template <int MODE, int CONV, int ORDER, int U>
-__global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
+template <int MODE, int CONV, int ORDER, int THREADS, int U>
+__device__ __forceinline__ void convert_rows(const KArgs& a)
 {
     constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;
     constexpr bool kScales = kFp8 || CONV == kCopy8;
@@ -145,23 +149,25 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
     constexpr int kSrcEsz = CONV == kCopy8 ? 1 : 2;
     constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;
 
-    const Item it = a.items[blockIdx.x];
-    const int plane = blockIdx.y;                            // layer * 2 + k/v
-    const ReqInfo rq = a.reqs[it.req];
-    const int T = rq.tokens;
+    // XCD-contiguous unit of this workgroup, then (plane, page)
+    const int unit = int(blockIdx.x % kXcds) * a.units_per_xcd + int(blockIdx.x / kXcds);
+    if (unit >= a.units) return;  // the grid is rounded up to a multiple of kXcds
+    const int plane = unit / a.num_items;                    // layer * 2 + k/v
+    const Item it = a.items[unit - plane * a.num_items];
+    const int T = it.tokens;
     const int t0 = it.blk * a.block_size;
     const int rows = min(a.block_size, T - t0) * a.hd;
     const int64_t row0 = (int64_t(plane) * T + t0) * a.hd;  // first row in transfer-tensor order
 
     char* dbase;
     float* sbase = nullptr;
+    int32_t b = 0;
     if constexpr (MODE == kPack) {
-        dbase = static_cast<char*>(a.dst) + rq.wire_data + row0 * a.row_dst_bytes;
+        dbase = static_cast<char*>(a.dst) + it.wire_data + row0 * a.row_dst_bytes;
         if constexpr (kScales)
-            sbase = reinterpret_cast<float*>(static_cast<char*>(a.dst) + rq.wire_scale) + row0;
+            sbase = reinterpret_cast<float*>(static_cast<char*>(a.dst) + it.wire_scale) + row0;
     } else {
-        const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
-        if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
+        b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
         const int64_t page_rows = int64_t(b) * a.block_size * a.hd;
         dbase = static_cast<char*>(a.dst) + plane * a.plane_bytes + page_rows * a.row_dst_bytes;
         if constexpr (kScales) sbase = a.dscale + plane * a.plane_scales + page_rows;
@@ -170,7 +176,7 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
     const int lg = a.lg_lpr;
     const int sub = threadIdx.x & ((1 << lg) - 1);          // 16-byte chunk within the row
     const int r0 = threadIdx.x >> lg;                        // first row of this lane group
-    const int rpp = kThreads >> lg;                          // rows per pass
+    const int rpp = THREADS >> lg;                           // rows per pass
     const bool lane_ok = sub < a.cpr;
     int s = r0 / a.hd;                                       // token within the page
     int i = r0 - s * a.hd;                                   // decode head
@@ -187,12 +193,12 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
             if (lane_ok && row < rows) {
                 const char* p;
                 if constexpr (MODE == kUnpack) {
-                    p = static_cast<const char*>(a.wire_in) + rq.wire_data +
+                    p = static_cast<const char*>(a.wire_in) + it.wire_data +
                         (row0 + row) * a.row_dst_bytes;
                     if constexpr (kScales)
                         if (sub == 0)
                             sc_in[u] = reinterpret_cast<const float*>(
-                                static_cast<const char*>(a.wire_in) + rq.wire_scale)[row0 + row];
+                                static_cast<const char*>(a.wire_in) + it.wire_scale)[row0 + row];
                 } else {
                     const uint32_t hs = a.head_src[i];
                     const int h = int(hs & 0xFFFFu);
@@ -202,7 +208,7 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
                     else
                         e = (int64_t(plane) * a.hs + h) * T + t0 + s;
                     p = static_cast<const char*>(a.src[hs >> 16]) +
-                        (rq.src_base + e * a.head_dim) * kSrcEsz;
+                        (it.src_base + e * a.head_dim) * kSrcEsz;
                 }
                 p += sub * (kLaneElems * kSrcEsz);
 #pragma unroll
@@ -215,6 +221,8 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
                 ++s;
             }
         }
+        if constexpr (MODE != kPack)
+            if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int row = pass + u * rpp + r0;
@@ -236,42 +244,88 @@ __global__ void __launch_bounds__(kThreads) convert_rows(const KArgs a)
     }
 }
 
-template <int MODE, int CONV, int ORDER>
-int go(const KArgs& a, int64_t items, int planes, void* stream)
+// One kernel name per operation, so traces tell them apart.
+template <int CONV, int ORDER, int THREADS, int U>
+__global__ void __launch_bounds__(THREADS) kvx_pack_kernel(const KArgs a)
 {
-    constexpr int U = (CONV == kBf16E4m3 || CONV == kF16E4m3) ? 4 : 8;
-    const void* fn = reinterpret_cast<const void*>(&convert_rows<MODE, CONV, ORDER, U>);
+    convert_rows<kPack, CONV, ORDER, THREADS, U>(a);
+}
+
+template <int CONV, int ORDER, int THREADS, int U>
+__global__ void __launch_bounds__(THREADS) kvx_unpack_kernel(const KArgs a)
+{
+    convert_rows<kUnpack, CONV, ORDER, THREADS, U>(a);
+}
+
+template <int CONV, int ORDER, int THREADS, int U>
+__global__ void __launch_bounds__(THREADS) kvx_repack_kernel(const KArgs a)
+{
+    convert_rows<kRepack, CONV, ORDER, THREADS, U>(a);
+}
+
+template <int CONV>
+struct Shape {
+    static constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;
+    // 16-bit rows: 512 threads, 4 rows of 16-byte loads in flight per lane;
+    // e4m3fn rows (two 16-byte loads per lane and row, VALU-heavy): 256 x 4
+    static constexpr int kThreads = kFp8 ? 256 : 512;
+    static constexpr int kU = 4;
+};
+
+template <int MODE, int CONV, int ORDER>
+int go(const KArgs& a, void* stream)
+{
+    using S = Shape<CONV>;
+    const void* fn;
+    if constexpr (MODE == kPack)
+        fn = reinterpret_cast<const void*>(&kvx_pack_kernel<CONV, ORDER, S::kThreads, S::kU>);
+    else if constexpr (MODE == kUnpack)
+        fn = reinterpret_cast<const void*>(&kvx_unpack_kernel<CONV, ORDER, S::kThreads, S::kU>);
+    else
+        fn = reinterpret_cast<const void*>(&kvx_repack_kernel<CONV, ORDER, S::kThreads, S::kU>);
     void* args[] = {const_cast<KArgs*>(&a)};
-    return int(hipLaunchKernel(fn, dim3(unsigned(items), unsigned(planes)), dim3(kThreads), args, 0,
+    const unsigned grid = unsigned(a.units_per_xcd) * kXcds;
+    return int(hipLaunchKernel(fn, dim3(grid), dim3(S::kThreads), args, 0,
                                static_cast<hipStream_t>(stream)));
 }
 
 template <int MODE, int ORDER>
-int go_conv(int conv, const KArgs& a, int64_t items, int planes, void* stream)
+int go_conv(int conv, const KArgs& a, void* stream)
 {
     switch (conv) {
-    case kCopy16: return go<MODE, kCopy16, ORDER>(a, items, planes, stream);
-    case kF16Bf16: return go<MODE, kF16Bf16, ORDER>(a, items, planes, stream);
-    case kBf16E4m3: return go<MODE, kBf16E4m3, ORDER>(a, items, planes, stream);
-    case kF16E4m3: return go<MODE, kF16E4m3, ORDER>(a, items, planes, stream);
+    case kCopy16: return go<MODE, kCopy16, ORDER>(a, stream);
+    case kF16Bf16: return go<MODE, kF16Bf16, ORDER>(a, stream);
+    case kBf16E4m3: return go<MODE, kBf16E4m3, ORDER>(a, stream);
+    case kF16E4m3: return go<MODE, kF16E4m3, ORDER>(a, stream);
     default: return int(hipErrorInvalidValue);
     }
 }
 
 }  // namespace
 
-int launch(int mode, int conv, int order, const KArgs& a, int64_t items, int planes, void* stream)
+int threads_for(int conv)
+{
+    switch (conv) {
+    case kBf16E4m3: return Shape<kBf16E4m3>::kThreads;
+    case kF16E4m3: return Shape<kF16E4m3>::kThreads;
+    case kCopy8: return Shape<kCopy8>::kThreads;
+    case kF16Bf16: return Shape<kF16Bf16>::kThreads;
+    default: return Shape<kCopy16>::kThreads;
+    }
+}
+
+int launch(int mode, int conv, int order, const KArgs& a, void* stream)
 {
     if (mode == kUnpack) {
-        if (conv == kCopy16) return go<kUnpack, kCopy16, KVX_THD>(a, items, planes, stream);
-        if (conv == kCopy8) return go<kUnpack, kCopy8, KVX_THD>(a, items, planes, stream);
+        if (conv == kCopy16) return go<kUnpack, kCopy16, KVX_THD>(a, stream);
+        if (conv == kCopy8) return go<kUnpack, kCopy8, KVX_THD>(a, stream);
         return int(hipErrorInvalidValue);
     }
     if (mode == kPack)
-        return order == KVX_THD ? go_conv<kPack, KVX_THD>(conv, a, items, planes, stream)
-                                : go_conv<kPack, KVX_HTD>(conv, a, items, planes, stream);
-    return order == KVX_THD ? go_conv<kRepack, KVX_THD>(conv, a, items, planes, stream)
-                            : go_conv<kRepack, KVX_HTD>(conv, a, items, planes, stream);
+        return order == KVX_THD ? go_conv<kPack, KVX_THD>(conv, a, stream)
+                                : go_conv<kPack, KVX_HTD>(conv, a, stream);
+    return order == KVX_THD ? go_conv<kRepack, KVX_THD>(conv, a, stream)
+                            : go_conv<kRepack, KVX_HTD>(conv, a, stream);
 }
 
 }  // namespace kvx

@@ -15,12 +15,11 @@
 #include "kvx_internal.h"
 
 using kvx::Item;
-using kvx::ReqInfo;
 
 struct kvx_plan_s {
     kvx_desc d;                   // seq_lens points into lens
     std::vector<int32_t> lens;
-    std::vector<ReqInfo> reqs;
+    std::vector<int64_t> wire_data, wire_scale;  // per request, transfer-tensor offsets
     std::vector<Item> items;
     int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
     int first_shard = 0, num_read_shards = 0;
@@ -31,9 +30,8 @@ struct kvx_plan_s {
     int64_t total_tokens = 0;
     int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
     int device = -1;
-    void* dev_table = nullptr;    // [items][reqs]
+    void* dev_table = nullptr;    // device copy of items
     const Item* dev_items = nullptr;
-    const ReqInfo* dev_reqs = nullptr;
 };
 
 namespace {
@@ -159,71 +157,64 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
     const int64_t L2 = int64_t(d.num_layers) * 2;
     int64_t src_off = 0, wire = 0, nitems = 0;
-    p->reqs.resize(std::max(d.num_requests, 1));
+    p->wire_data.resize(d.num_requests);
+    p->wire_scale.resize(d.num_requests);
+    std::vector<int64_t> src_base(d.num_requests);
     for (int r = 0; r < d.num_requests; ++r) {
         const int64_t T = p->lens[r];
         const int64_t rows = L2 * T * p->hd;
-        ReqInfo& q = p->reqs[r];
-        q.src_base = src_off;
-        q.tokens = int32_t(T);
-        q.pad = 0;
+        src_base[r] = src_off;
         src_off += L2 * T * p->hs * d.head_dim;
         wire = align256(wire);
-        q.wire_data = wire;
+        p->wire_data[r] = wire;
         wire += rows * d.head_dim * p->esz_dst;
         if (fp8) {
             wire = align256(wire);
-            q.wire_scale = wire;
+            p->wire_scale[r] = wire;
             wire += rows * 4;
         } else {
-            q.wire_scale = -1;
+            p->wire_scale[r] = -1;
         }
         const int64_t nb = (T + d.block_size - 1) / d.block_size;
-        p->max_blocks = std::max<int64_t>(p->max_blocks, nb);
+        p->max_blocks = int32_t(std::max<int64_t>(p->max_blocks, nb));
         nitems += nb;
         p->total_tokens += T;
         p->elems_rows += rows;
     }
     p->wire_bytes = uint64_t(align256(wire));
-    if (nitems > kvx::kMaxItems) {
+    if (nitems * L2 > kvx::kMaxUnits) {
         delete p;
-        return fail(KVX_EUNSUPPORTED, "more than %d logical pages", kvx::kMaxItems);
+        return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers)",
+                    (long long)kvx::kMaxUnits);
     }
     p->items.reserve(size_t(std::max<int64_t>(nitems, 1)));
     for (int r = 0; r < d.num_requests; ++r) {
         const int nb = (p->lens[r] + d.block_size - 1) / d.block_size;
-        for (int k = 0; k < nb; ++k) p->items.push_back(Item{r, k});
+        for (int k = 0; k < nb; ++k)
+            p->items.push_back(Item{src_base[r], p->wire_data[r], p->wire_scale[r], r, k,
+                                    p->lens[r], 0});
     }
-    if (p->items.empty()) p->items.push_back(Item{0, 0});  // keeps the table non-empty
 
     // device table on the current device, when one is usable
     int dev = -1;
-    if (hipGetDevice(&dev) == hipSuccess && dev >= 0) {
+    if (!p->items.empty() && hipGetDevice(&dev) == hipSuccess && dev >= 0) {
         const size_t ib = p->items.size() * sizeof(Item);
-        const size_t rb = p->reqs.size() * sizeof(ReqInfo);
-        const size_t ioff = 0, roff = (ib + 255) & ~size_t(255);
         void* t = nullptr;
-        if (hipMalloc(&t, roff + rb) != hipSuccess) {
+        if (hipMalloc(&t, ib) != hipSuccess) {
             delete p;
             return fail(KVX_ENOMEM, "device table allocation failed");
         }
-        if (hipMemcpy(static_cast<char*>(t) + ioff, p->items.data(), ib, hipMemcpyHostToDevice) !=
-                hipSuccess ||
-            hipMemcpy(static_cast<char*>(t) + roff, p->reqs.data(), rb, hipMemcpyHostToDevice) !=
-                hipSuccess) {
+        if (hipMemcpy(t, p->items.data(), ib, hipMemcpyHostToDevice) != hipSuccess) {
             (void)hipFree(t);
             delete p;
             return fail(KVX_EDEVICE, "device table upload failed");
         }
         p->device = dev;
         p->dev_table = t;
-        p->dev_items = reinterpret_cast<const Item*>(static_cast<char*>(t) + ioff);
-        p->dev_reqs = reinterpret_cast<const ReqInfo*>(static_cast<char*>(t) + roff);
-    } else {
+        p->dev_items = static_cast<const Item*>(t);
+    } else if (!p->items.empty()) {
         (void)hipGetLastError();  // no device: host-only plan
     }
-    // the real item count (the placeholder item is never launched)
-    if (nitems == 0) p->items.clear();
     *out = p;
     return KVX_OK;
 }
@@ -255,8 +246,8 @@ kvx_status kvx_plan_segment(const kvx_plan_t* p, int32_t r, int64_t* data_off, i
     if (!p) return fail(KVX_EINVAL, "NULL plan");
     if (r < 0 || r >= p->d.num_requests)
         return fail(KVX_EINVAL, "request %d outside [0, %d)", r, p->d.num_requests);
-    if (data_off) *data_off = p->reqs[r].wire_data;
-    if (scale_off) *scale_off = p->reqs[r].wire_scale;
+    if (data_off) *data_off = p->wire_data[r];
+    if (scale_off) *scale_off = p->wire_scale[r];
     return KVX_OK;
 }
 
@@ -296,6 +287,12 @@ kvx_status kvx_check_block_table(const kvx_plan_t* p, const int32_t* bt, int32_t
 }  // extern "C"
 
 namespace {
+
+int conv_for(const kvx_plan_t* p, int mode)
+{
+    if (mode == kvx::kUnpack) return p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
+    return p->conv;
+}
 
 // Shared argument checks of the launch calls; fills the kernel arguments.
 kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, const void* wire,
@@ -340,8 +337,11 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.dst = dst;
     a.dscale = scales;
     a.items = p->dev_items;
-    a.reqs = p->dev_reqs;
     a.bt = bt;
+    a.num_items = int32_t(p->items.size());
+    const int64_t units = int64_t(p->items.size()) * 2 * d.num_layers;
+    a.units = int32_t(units);
+    a.units_per_xcd = int32_t((units + kvx::kXcds - 1) / kvx::kXcds);
     a.num_blocks = d.num_blocks;
     a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_dst;
     a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
@@ -353,7 +353,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.row_dst_bytes = d.head_dim * p->esz_dst;
     a.cpr = p->cpr;
     a.lg_lpr = p->lg_lpr;
-    const int rpp = kvx::kThreads >> p->lg_lpr;
+    const int rpp = kvx::threads_for(conv_for(p, mode)) >> p->lg_lpr;
     a.dq = rpp / p->hd;
     a.dr = rpp % p->hd;
     std::memcpy(a.head_src, p->head_src, sizeof a.head_src);
@@ -363,10 +363,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
 kvx_status run(const kvx_plan_t* p, int mode, const kvx::KArgs& a, void* stream)
 {
     if (p->items.empty()) return KVX_OK;
-    int conv = p->conv;
-    if (mode == kvx::kUnpack) conv = p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
-    const int err = kvx::launch(mode, conv, p->d.src_order, a, int64_t(p->items.size()),
-                                2 * p->d.num_layers, stream);
+    const int err = kvx::launch(mode, conv_for(p, mode), p->d.src_order, a, stream);
     if (err != 0)
         return fail(KVX_EDEVICE, "kernel launch failed: %s", hipGetErrorString(hipError_t(err)));
     return KVX_OK;
