@@ -63,10 +63,16 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="time the repack only (no pack/unpack/latency legs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--calib-gib", type=float, default=4.0,
-                    help="size of the plain device copy timed as a ceiling (and used to "
-                         "calibrate rocprofv3 byte counters); 0 = skip")
+    ap.add_argument("--calib-gib", type=float, default=2.0,
+                    help="bytes read (= bytes written) by the plain copies timed as ceilings "
+                         "and as the reference of the rocprofv3 byte counters; 0 = skip")
+    ap.add_argument("--derive-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of "
+                         "this benchmark into profiles/traffic.json and exit")
     args = ap.parse_args()
+    if args.derive_traffic:
+        derive_traffic(*args.derive_traffic, workload=args.workload, calib_gib=args.calib_gib)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -154,20 +160,7 @@ def main():
                              "median": round(k_med, 4)},
     }
     if args.calib_gib > 0:
-        # plain device copies of known size (read N + write N bytes): the HIP
-        # runtime's copy kernel (hipMemcpyAsync device to device) and a torch
-        # elementwise kernel; the references for the byte counters
-        n = int(args.calib_gib * 2**30) // 4
-        a = torch.empty(n, dtype=torch.int32, device="cuda")
-        b = torch.empty_like(a)
-        out["copy_ceiling"] = {}
-        for kind, fn in (("hipMemcpy_d2d", lambda: b.copy_(a)),
-                         ("torch_elementwise", lambda: torch.bitwise_not(a, out=b))):
-            ms, km, _, _ = timed(fn, 10, 2)
-            out["copy_ceiling"][kind] = {"bytes": 8 * n, "kernel_ms": round(km, 4),
-                                         "GB/s": round(8 * n / (km * 1e-3) / 1e9, 1)}
-            log(f"plain copy ({kind}): {8 * n / (km * 1e-3) / 1e9:.0f} GB/s")
-        del a, b
+        out["copy_ceiling"] = copy_legs(K, torch, args.calib_gib, timed, stream)
 
     traffic = measured_traffic(w.name)
     out["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -223,6 +216,70 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lens, shards, args.cpu_seconds, value)
     print(json.dumps(out), flush=True)
+
+
+CALIB_TOKENS_PER_GIB = 1 << 18   # 1 layer, 8 heads, dim 128, bf16: 2 x 8 x 256 B per token
+
+
+def copy_legs(K, torch, gib, timed, stream):
+    """Plain copies of known size: the identity layout through kvx (one request,
+    TP1 -> TP1, bf16, pages 0, 1, 2, ... in order: a memcpy of `gib` GiB done
+    by the repack kernel, the reference for the counters), the HIP runtime's
+    device copy and a torch elementwise kernel."""
+    import numpy as np
+    T = int(gib * CALIB_TOKENS_PER_GIB)
+    nbytes = T * 2 * 8 * 128 * 2                     # read = written
+    src = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    bt = torch.arange(T // 16, dtype=torch.int32, device="cuda")
+    plan = K.kvx_plan(K.make_desc(1, 8, 128, 1, 1, 0, K.BF16, K.BF16, K.THD, 16, T // 16, [T]))
+    legs = {}
+    for kind, fn in (
+            ("kvx_identity_memcpy", lambda: K.kvx_repack(plan, [src], dst, None, bt, T // 16,
+                                                         stream)),
+            ("hipMemcpy_d2d", lambda: dst.view(torch.int16).copy_(src)),
+            ("torch_elementwise", lambda: torch.bitwise_not(src, out=dst.view(torch.int16)))):
+        ms, km, _, _ = timed(fn, 10, 2)
+        legs[kind] = {"bytes_read": nbytes, "bytes_written": nbytes, "kernel_ms": round(km, 4),
+                      "GB/s": round(2 * nbytes / (km * 1e-3) / 1e9, 1)}
+        log(f"plain copy ({kind}): {2 * nbytes / (km * 1e-3) / 1e9:.0f} GB/s")
+    legs["kvx_identity_memcpy"]["grid_units"] = (T // 16) * 2
+    del src, dst, bt, np
+    return legs
+
+
+def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
+    """HBM bytes per repack launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch), each scaled by the ratio of known bytes to counted
+    bytes of the identity-memcpy repack in the same run (calib_gib GiB read and
+    as many written).  Dispatches are told apart by grid size."""
+    import csv
+    w_tokens = int(calib_gib * CALIB_TOKENS_PER_GIB)
+    calib_bytes = w_tokens * 2 * 8 * 128 * 2
+
+    def per_grid(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter and "kvx_repack_kernel" in r["Kernel_Name"]:
+                vals.setdefault(int(r["Grid_Size"]), []).append(float(r["Counter_Value"]) * 1024)
+        return {g: statistics.median(v) for g, v in vals.items()}
+
+    f, wr = per_grid(fetch_csv, "FETCH_SIZE"), per_grid(write_csv, "WRITE_SIZE")
+    calib_grid = (w_tokens // 16) * 2 * 512                 # units x 512 threads (xcd-rounded)
+    calib_grid = ((calib_grid // 512 + 7) // 8) * 8 * 512
+    others = [g for g in f if g != calib_grid]
+    assert calib_grid in f and calib_grid in wr and len(others) == 1, (sorted(f), calib_grid)
+    g = others[0]
+    kf, kw = calib_bytes / f[calib_grid], calib_bytes / wr[calib_grid]
+    rec = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+           "fetch_factor": round(kf, 4), "write_factor": round(kw, 4),
+           "fetch_bytes_per_launch": round(f[g] * kf), "write_bytes_per_launch": round(wr[g] * kw),
+           "bytes_per_launch": round(f[g] * kf + wr[g] * kw),
+           "sources": [os.path.basename(fetch_csv), os.path.basename(write_csv)]}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec))
 
 
 def cpu_baseline(w, lens, shards, budget_s, gpu_value):

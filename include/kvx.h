@@ -122,7 +122,7 @@ typedef struct {
  * an unknown order; head_dim * element size not a multiple of 16 bytes on
  * either side.  KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16,
  * bf16->bf16, fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row
- * (head_dim * dst size) above 1024 bytes; more than 128 heads per decode
+ * (head_dim * dst size) above 1024 bytes; more than 1024 heads per decode
  * rank; more than 65535 source heads per shard; 2*L > 65535; more than 2^24-1
  * logical pages (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if the table cannot be allocated. */
 kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);

@@ -8,13 +8,22 @@
 
 namespace kvx {
 
-constexpr int kMaxHeadsPerRank = 128;   // Hd limit (kernel-argument head table)
+constexpr int kThreads = 256;           // threads per workgroup (4 wave64)
+constexpr int kMaxHeadsPerRank = 1024;  // Hd limit
 constexpr int kMaxReadShards = 64;      // source shards one decode rank may read
 constexpr int kMaxRowChunks = 64;       // 16-byte destination chunks per row (one wave)
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
-// work units (pages x planes) of one launch; the 1-D grid is this rounded up to
-// a multiple of kXcds, and grid * threads stays below 2^32
-constexpr int64_t kMaxUnits = (int64_t(1) << 22) - kXcds;
+// work units of one launch; the 1-D grid is this rounded up to a multiple of
+// kXcds, and grid * kThreads stays below 2^32
+constexpr int64_t kMaxUnits = (int64_t(1) << 24) - kXcds;
+
+// Division by an invariant divisor d >= 1 (Granlund and Montgomery, 1994):
+// n / d = (mulhi(n, mul) + n) >> shift for every 32-bit n, with
+// shift = ceil(log2 d) and mul = floor(2^32 (2^shift - d) / d) + 1.
+struct FastDiv {
+    uint32_t mul;
+    uint32_t shift;
+};
 
 // One logical page of one request, device resident: the unit of work of a
 // workgroup in every (layer, k/v) plane.
@@ -39,9 +48,20 @@ enum Conv : int {
     kCopy8 = 4      // 8-bit bits unchanged (+ scale copy), unpack of e4m3fn
 };
 
+// A run of the decode rank's heads that comes from one source shard: decode
+// heads [i0, i0 + n) are heads [h0, h0 + n) of shard slot `slot`.
+struct Segment {
+    int32_t slot;
+    int32_t h0;
+    int32_t i0;
+    int32_t n;
+    FastDiv div_n;
+};
+
 // Kernel arguments (passed by value through the kernel-argument segment).
 struct KArgs {
     const void* src[kMaxReadShards];  // shard first_shard + k at src[k]
+    Segment seg[kMaxReadShards];      // pack/repack: one per shard read; unpack: one, all heads
     const void* wire_in;              // unpack source
     void* dst;                        // pack: transfer tensor; else cache
     float* dscale;                    // cache scales (unpack/repack, e4m3fn)
@@ -50,9 +70,13 @@ struct KArgs {
     int64_t num_blocks;
     int64_t plane_bytes;              // cache bytes per (layer, k/v) plane
     int64_t plane_scales;             // cache scales per plane
-    int32_t num_items;                // logical pages per plane
-    int32_t units;                    // num_items * planes
-    int32_t units_per_xcd;            // grid / kXcds
+    uint32_t units;                   // work units: planes x pages x segments x parts
+    uint32_t units_per_xcd;           // grid / kXcds
+    uint32_t num_items;               // logical pages per plane
+    uint32_t planes;                  // 2 x layers
+    uint32_t num_segs;
+    uint32_t parts;                   // workgroup passes per (page, segment)
+    FastDiv div_parts, div_segs, div_items;
     int32_t bt_stride;
     int32_t block_size;
     int32_t hs;                       // heads per source shard
@@ -61,14 +85,11 @@ struct KArgs {
     int32_t row_dst_bytes;            // head_dim * dst element size
     int32_t cpr;                      // 16-byte destination chunks per row
     int32_t lg_lpr;                   // log2(lanes per row), lanes per row >= cpr
-    int32_t dq, dr;                   // (rows per pass) / hd and % hd
-    uint32_t head_src[kMaxHeadsPerRank];  // (shard slot << 16) | head within shard
 };
-
-// threads per workgroup for a conversion (16-bit destinations: 512, e4m3fn: 256)
-int threads_for(int conv);
 
 // Launch one conversion over a.units work units; returns a hipError_t value.
 int launch(int mode, int conv, int order, const KArgs& a, void* stream);
+
+FastDiv make_fastdiv(uint32_t d);
 
 }  // namespace kvx

@@ -2,18 +2,23 @@
 // tensor), unpack (transfer tensor -> paged cache) and the fused repack
 // (source shards -> paged cache).
 //
-// Work decomposition: one workgroup per work unit = (logical page of a
-// request, (layer, k/v) plane).  Units are numbered plane-major, so
-// consecutive units read consecutive source bytes.  The 1-D grid is dealt to
-// the 8 XCDs round-robin (workgroup i runs on XCD i % 8); workgroup i is mapped
-// to unit (i % 8) * units_per_xcd + i / 8, so every XCD streams one contiguous
-// run of units through its own L2 instead of every eighth page of the whole
-// stream.  A page holds ntok <= block_size tokens x Hd heads = "rows" of
-// head_dim elements, contiguous in both the paged cache and the transfer
-// tensor.  Each row is covered by a power-of-two group of lanes, one 16-byte
-// destination vector per lane (global_load_dwordx4 / global_store_dwordx4); a
-// workgroup walks its rows in passes of threads / lanes-per-row rows and keeps
-// U rows of loads in flight per lane before the first store.
+// Work decomposition: a work unit is one pass over part of a page's rows of
+// one head segment: (layer, k/v plane) x (logical page of a request) x (head
+// segment: the decode heads that come from one source shard) x (part).  A page
+// holds ntok <= block_size tokens; a segment of n heads gives it ntok * n
+// "rows" of head_dim elements.  Each row is covered by a power-of-two group of
+// lanes, one 16-byte destination vector per lane (global_load_dwordx4 /
+// global_store_dwordx4), so a 256-thread workgroup covers 256 / lanes-per-row
+// rows: one part.  The shard, its first head and the segment's place in the
+// decode row are the same for the whole workgroup (scalar registers), so a
+// lane's load address needs no table lookup; every lane issues its load(s),
+// converts and stores once.
+//
+// Units are numbered plane-major, page, segment, then part, so consecutive
+// units read consecutive source bytes.  The 1-D grid is dealt to the 8 XCDs
+// round-robin (workgroup i runs on XCD i % 8); workgroup i takes unit
+// (i % 8) * units_per_xcd + i / 8, so every XCD streams one contiguous run of
+// units through its own L2 instead of every eighth unit of the whole stream.
 //
 // The path is a gather/scatter stream with no reuse and no contraction: it is
 // bound by HBM bandwidth, so there is no MFMA and no LDS staging (every row is
@@ -140,152 +145,131 @@ __device__ __forceinline__ uint4 to_bf16x8(const uint4& v)
 
 // ---- the row kernel ----------------------------------------------------------
 
-template <int MODE, int CONV, int ORDER, int THREADS, int U>
-__device__ __forceinline__ void convert_rows(const KArgs& a)
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f)
+{
+    return uint32_t((uint64_t(__umulhi(n, f.mul)) + n) >> f.shift);
+}
+
+template <int MODE, int CONV, int ORDER>
+__device__ __forceinline__ void convert_part(const KArgs& a)
 {
     constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;
     constexpr bool kScales = kFp8 || CONV == kCopy8;
-    constexpr int kVecs = kFp8 ? 2 : 1;                       // 16-byte loads per lane per row
+    constexpr int kVecs = kFp8 ? 2 : 1;                       // 16-byte loads per lane
     constexpr int kSrcEsz = CONV == kCopy8 ? 1 : 2;
     constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;
 
-    // XCD-contiguous unit of this workgroup, then (plane, page)
-    const int unit = int(blockIdx.x % kXcds) * a.units_per_xcd + int(blockIdx.x / kXcds);
+    // XCD-contiguous unit of this workgroup -> (plane, page, segment, part)
+    const uint32_t unit = (blockIdx.x % kXcds) * a.units_per_xcd + blockIdx.x / kXcds;
     if (unit >= a.units) return;  // the grid is rounded up to a multiple of kXcds
-    const int plane = unit / a.num_items;                    // layer * 2 + k/v
-    const Item it = a.items[unit - plane * a.num_items];
+    const uint32_t q1 = fdiv(unit, a.div_parts);
+    const uint32_t part = unit - q1 * a.parts;
+    const uint32_t q2 = fdiv(q1, a.div_segs);
+    const uint32_t sg = q1 - q2 * a.num_segs;
+    const uint32_t plane = fdiv(q2, a.div_items);           // layer * 2 + k/v
+    const uint32_t item = q2 - plane * a.num_items;
+    if (plane >= a.planes || item >= a.num_items || sg >= a.num_segs || part >= a.parts) return;
+    const Segment seg = a.seg[sg];
+    const Item it = a.items[item];
     const int T = it.tokens;
     const int t0 = it.blk * a.block_size;
-    const int rows = min(a.block_size, T - t0) * a.hd;
+    const int seg_rows = min(a.block_size, T - t0) * seg.n;
     const int64_t row0 = (int64_t(plane) * T + t0) * a.hd;  // first row in transfer-tensor order
+
+    const int lg = a.lg_lpr;
+    const int sub = threadIdx.x & ((1 << lg) - 1);          // 16-byte chunk within the row
+    const int r = int(part) * (kThreads >> lg) + (threadIdx.x >> lg);  // row within the segment
+    const bool ok = sub < a.cpr && r < seg_rows;
+    const int s = int(fdiv(uint32_t(r), seg.div_n));       // token within the page
+    const int ii = r - s * seg.n;                           // head within the segment
+    const int row = s * a.hd + seg.i0 + ii;                 // row within the page
+
+    uint4 v[kVecs];
+#pragma unroll
+    for (int k = 0; k < kVecs; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
+    float sc = 0.0f;
+    if (ok) {
+        const char* p;
+        if constexpr (MODE == kUnpack) {
+            p = static_cast<const char*>(a.wire_in) + it.wire_data + (row0 + row) * a.row_dst_bytes;
+            if constexpr (kScales)
+                if (sub == 0)
+                    sc = reinterpret_cast<const float*>(static_cast<const char*>(a.wire_in) +
+                                                        it.wire_scale)[row0 + row];
+        } else {
+            const int h = seg.h0 + ii;                       // head within the shard
+            int64_t e;
+            if constexpr (ORDER == KVX_THD)
+                e = (int64_t(plane) * T + t0 + s) * a.hs + h;
+            else
+                e = (int64_t(plane) * a.hs + h) * T + t0 + s;
+            p = static_cast<const char*>(a.src[seg.slot]) + (it.src_base + e * a.head_dim) * kSrcEsz;
+        }
+        p += sub * (kLaneElems * kSrcEsz);
+#pragma unroll
+        for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+    }
 
     char* dbase;
     float* sbase = nullptr;
-    int32_t b = 0;
     if constexpr (MODE == kPack) {
         dbase = static_cast<char*>(a.dst) + it.wire_data + row0 * a.row_dst_bytes;
         if constexpr (kScales)
             sbase = reinterpret_cast<float*>(static_cast<char*>(a.dst) + it.wire_scale) + row0;
     } else {
-        b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
+        const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
+        if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
         const int64_t page_rows = int64_t(b) * a.block_size * a.hd;
         dbase = static_cast<char*>(a.dst) + plane * a.plane_bytes + page_rows * a.row_dst_bytes;
         if constexpr (kScales) sbase = a.dscale + plane * a.plane_scales + page_rows;
     }
 
-    const int lg = a.lg_lpr;
-    const int sub = threadIdx.x & ((1 << lg) - 1);          // 16-byte chunk within the row
-    const int r0 = threadIdx.x >> lg;                        // first row of this lane group
-    const int rpp = THREADS >> lg;                           // rows per pass
-    const bool lane_ok = sub < a.cpr;
-    int s = r0 / a.hd;                                       // token within the page
-    int i = r0 - s * a.hd;                                   // decode head
-
-    for (int pass = 0; pass < rows; pass += U * rpp) {      // uniform over the workgroup
-        uint4 v[U][kVecs];
-        float sc_in[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int row = pass + u * rpp + r0;
-#pragma unroll
-            for (int k = 0; k < kVecs; ++k) v[u][k] = make_uint4(0u, 0u, 0u, 0u);
-            sc_in[u] = 0.0f;
-            if (lane_ok && row < rows) {
-                const char* p;
-                if constexpr (MODE == kUnpack) {
-                    p = static_cast<const char*>(a.wire_in) + it.wire_data +
-                        (row0 + row) * a.row_dst_bytes;
-                    if constexpr (kScales)
-                        if (sub == 0)
-                            sc_in[u] = reinterpret_cast<const float*>(
-                                static_cast<const char*>(a.wire_in) + it.wire_scale)[row0 + row];
-                } else {
-                    const uint32_t hs = a.head_src[i];
-                    const int h = int(hs & 0xFFFFu);
-                    int64_t e;
-                    if constexpr (ORDER == KVX_THD)
-                        e = (int64_t(plane) * T + t0 + s) * a.hs + h;
-                    else
-                        e = (int64_t(plane) * a.hs + h) * T + t0 + s;
-                    p = static_cast<const char*>(a.src[hs >> 16]) +
-                        (it.src_base + e * a.head_dim) * kSrcEsz;
-                }
-                p += sub * (kLaneElems * kSrcEsz);
-#pragma unroll
-                for (int k = 0; k < kVecs; ++k) v[u][k] = reinterpret_cast<const uint4*>(p)[k];
-            }
-            s += a.dq;
-            i += a.dr;
-            if (i >= a.hd) {
-                i -= a.hd;
-                ++s;
-            }
-        }
-        if constexpr (MODE != kPack)
-            if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int row = pass + u * rpp + r0;
-            const bool ok = lane_ok && row < rows;
-            uint4 out;
-            float sc = sc_in[u];
-            if constexpr (kFp8)
-                out = to_e4m3<CONV>(v[u], lg, sc);
-            else if constexpr (CONV == kF16Bf16)
-                out = to_bf16x8(v[u][0]);
-            else
-                out = v[u][0];
-            if (ok) {
-                *reinterpret_cast<uint4*>(dbase + int64_t(row) * a.row_dst_bytes + sub * 16) = out;
-                if constexpr (kScales)
-                    if (sub == 0) sbase[row] = sc;
-            }
-        }
+    uint4 out;
+    if constexpr (kFp8)
+        out = to_e4m3<CONV>(v, lg, sc);  // every lane takes part in the row reduction
+    else if constexpr (CONV == kF16Bf16)
+        out = to_bf16x8(v[0]);
+    else
+        out = v[0];
+    if (ok) {
+        *reinterpret_cast<uint4*>(dbase + int64_t(row) * a.row_dst_bytes + sub * 16) = out;
+        if constexpr (kScales)
+            if (sub == 0) sbase[row] = sc;
     }
 }
 
 // One kernel name per operation, so traces tell them apart.
-template <int CONV, int ORDER, int THREADS, int U>
-__global__ void __launch_bounds__(THREADS) kvx_pack_kernel(const KArgs a)
+template <int CONV, int ORDER>
+__global__ void __launch_bounds__(kThreads) kvx_pack_kernel(const KArgs a)
 {
-    convert_rows<kPack, CONV, ORDER, THREADS, U>(a);
+    convert_part<kPack, CONV, ORDER>(a);
 }
 
-template <int CONV, int ORDER, int THREADS, int U>
-__global__ void __launch_bounds__(THREADS) kvx_unpack_kernel(const KArgs a)
+template <int CONV, int ORDER>
+__global__ void __launch_bounds__(kThreads) kvx_unpack_kernel(const KArgs a)
 {
-    convert_rows<kUnpack, CONV, ORDER, THREADS, U>(a);
+    convert_part<kUnpack, CONV, ORDER>(a);
 }
 
-template <int CONV, int ORDER, int THREADS, int U>
-__global__ void __launch_bounds__(THREADS) kvx_repack_kernel(const KArgs a)
+template <int CONV, int ORDER>
+__global__ void __launch_bounds__(kThreads) kvx_repack_kernel(const KArgs a)
 {
-    convert_rows<kRepack, CONV, ORDER, THREADS, U>(a);
+    convert_part<kRepack, CONV, ORDER>(a);
 }
-
-template <int CONV>
-struct Shape {
-    static constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;
-    // 16-bit rows: 512 threads, 4 rows of 16-byte loads in flight per lane;
-    // e4m3fn rows (two 16-byte loads per lane and row, VALU-heavy): 256 x 4
-    static constexpr int kThreads = kFp8 ? 256 : 512;
-    static constexpr int kU = 4;
-};
 
 template <int MODE, int CONV, int ORDER>
 int go(const KArgs& a, void* stream)
 {
-    using S = Shape<CONV>;
     const void* fn;
     if constexpr (MODE == kPack)
-        fn = reinterpret_cast<const void*>(&kvx_pack_kernel<CONV, ORDER, S::kThreads, S::kU>);
+        fn = reinterpret_cast<const void*>(&kvx_pack_kernel<CONV, ORDER>);
     else if constexpr (MODE == kUnpack)
-        fn = reinterpret_cast<const void*>(&kvx_unpack_kernel<CONV, ORDER, S::kThreads, S::kU>);
+        fn = reinterpret_cast<const void*>(&kvx_unpack_kernel<CONV, ORDER>);
     else
-        fn = reinterpret_cast<const void*>(&kvx_repack_kernel<CONV, ORDER, S::kThreads, S::kU>);
+        fn = reinterpret_cast<const void*>(&kvx_repack_kernel<CONV, ORDER>);
     void* args[] = {const_cast<KArgs*>(&a)};
-    const unsigned grid = unsigned(a.units_per_xcd) * kXcds;
-    return int(hipLaunchKernel(fn, dim3(grid), dim3(S::kThreads), args, 0,
+    const unsigned grid = a.units_per_xcd * kXcds;
+    return int(hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, 0,
                                static_cast<hipStream_t>(stream)));
 }
 
@@ -302,17 +286,6 @@ int go_conv(int conv, const KArgs& a, void* stream)
 }
 
 }  // namespace
-
-int threads_for(int conv)
-{
-    switch (conv) {
-    case kBf16E4m3: return Shape<kBf16E4m3>::kThreads;
-    case kF16E4m3: return Shape<kF16E4m3>::kThreads;
-    case kCopy8: return Shape<kCopy8>::kThreads;
-    case kF16Bf16: return Shape<kF16Bf16>::kThreads;
-    default: return Shape<kCopy16>::kThreads;
-    }
-}
 
 int launch(int mode, int conv, int order, const KArgs& a, void* stream)
 {

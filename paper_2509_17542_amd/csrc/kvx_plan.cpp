@@ -23,8 +23,8 @@ struct kvx_plan_s {
     std::vector<Item> items;
     int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
     int first_shard = 0, num_read_shards = 0;
-    int cpr = 0, lg_lpr = 0;
-    uint32_t head_src[kvx::kMaxHeadsPerRank] = {};
+    int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
+    std::vector<kvx::Segment> segs;  // head runs of the decode rank, one per shard read
     int32_t max_blocks = 0;
     uint64_t wire_bytes = 0;
     int64_t total_tokens = 0;
@@ -144,9 +144,11 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         delete p;
         return fail(KVX_EUNSUPPORTED, "decode rank reads more than %d shards", kvx::kMaxReadShards);
     }
-    for (int i = 0; i < p->hd; ++i) {
-        const int g = g0 + i;
-        p->head_src[i] = (uint32_t(g / p->hs - p->first_shard) << 16) | uint32_t(g % p->hs);
+    for (int k = 0; k < p->num_read_shards; ++k) {
+        const int j = p->first_shard + k;
+        const int lo = std::max(g0, j * p->hs), hi = std::min(g0 + p->hd, (j + 1) * p->hs);
+        p->segs.push_back(kvx::Segment{k, lo - j * p->hs, lo - g0, hi - lo, {0, 0}});
+        p->segs.back().div_n = kvx::make_fastdiv(uint32_t(hi - lo));
     }
 
     // lanes per row: the smallest power of two covering the row's 16-byte chunks
@@ -182,9 +184,15 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         p->elems_rows += rows;
     }
     p->wire_bytes = uint64_t(align256(wire));
-    if (nitems * L2 > kvx::kMaxUnits) {
+    const int64_t rpp = kvx::kThreads >> p->lg_lpr;  // rows per workgroup pass
+    int max_n = 0;
+    for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
+    p->parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
+    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp - 1) / rpp);
+    if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * p->num_read_shards,
+                                        p->parts_unpack) > kvx::kMaxUnits) {
         delete p;
-        return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers)",
+        return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers x parts)",
                     (long long)kvx::kMaxUnits);
     }
     p->items.reserve(size_t(std::max<int64_t>(nitems, 1)));
@@ -288,6 +296,18 @@ kvx_status kvx_check_block_table(const kvx_plan_t* p, const int32_t* bt, int32_t
 
 namespace {
 
+}  // namespace
+
+kvx::FastDiv kvx::make_fastdiv(uint32_t d)
+{
+    uint32_t shift = 0;
+    while ((uint64_t(1) << shift) < d) ++shift;
+    const uint64_t mul = ((uint64_t(1) << 32) * ((uint64_t(1) << shift) - d)) / d + 1;
+    return FastDiv{uint32_t(mul), shift};
+}
+
+namespace {
+
 int conv_for(const kvx_plan_t* p, int mode)
 {
     if (mode == kvx::kUnpack) return p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
@@ -338,10 +358,23 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.dscale = scales;
     a.items = p->dev_items;
     a.bt = bt;
-    a.num_items = int32_t(p->items.size());
-    const int64_t units = int64_t(p->items.size()) * 2 * d.num_layers;
-    a.units = int32_t(units);
-    a.units_per_xcd = int32_t((units + kvx::kXcds - 1) / kvx::kXcds);
+    a.num_items = uint32_t(p->items.size());
+    a.planes = uint32_t(2 * d.num_layers);
+    if (mode == kvx::kUnpack) {  // transfer-tensor rows are already in decode order
+        a.num_segs = 1;
+        a.parts = uint32_t(p->parts_unpack);
+        a.seg[0] = kvx::Segment{0, 0, 0, p->hd, kvx::make_fastdiv(uint32_t(p->hd))};
+    } else {
+        a.num_segs = uint32_t(p->segs.size());
+        a.parts = uint32_t(p->parts);
+        for (size_t k = 0; k < p->segs.size(); ++k) a.seg[k] = p->segs[k];
+    }
+    const int64_t units = int64_t(p->items.size()) * a.planes * a.num_segs * a.parts;
+    a.units = uint32_t(units);
+    a.units_per_xcd = uint32_t((units + kvx::kXcds - 1) / kvx::kXcds);
+    a.div_parts = kvx::make_fastdiv(a.parts);
+    a.div_segs = kvx::make_fastdiv(a.num_segs);
+    a.div_items = kvx::make_fastdiv(a.num_items);
     a.num_blocks = d.num_blocks;
     a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_dst;
     a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
@@ -353,10 +386,6 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.row_dst_bytes = d.head_dim * p->esz_dst;
     a.cpr = p->cpr;
     a.lg_lpr = p->lg_lpr;
-    const int rpp = kvx::threads_for(conv_for(p, mode)) >> p->lg_lpr;
-    a.dq = rpp / p->hd;
-    a.dr = rpp % p->hd;
-    std::memcpy(a.head_src, p->head_src, sizeof a.head_src);
     return KVX_OK;
 }
 

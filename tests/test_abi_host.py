@@ -80,7 +80,7 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(head_dim=8, dst_dtype=3), K.EINVAL),          # 8-byte e4m3 rows
     (dict(src_dtype=3), K.EUNSUPPORTED), (dict(src_dtype=2, dst_dtype=1), K.EUNSUPPORTED),
     (dict(dst_dtype=9), K.EINVAL), (dict(head_dim=1024), K.EUNSUPPORTED),
-    (dict(num_kv_heads=512, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
+    (dict(num_kv_heads=4096, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
 ])
 def test_plan_rejects(over, status):
     kw = dict(BASE)
