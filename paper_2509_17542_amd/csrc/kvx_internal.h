@@ -76,7 +76,7 @@ struct KArgs {
     uint32_t planes;                  // 2 x layers
     uint32_t num_segs;
     uint32_t parts;                   // workgroup passes per (page, segment)
-    FastDiv div_parts, div_segs, div_items;
+    FastDiv div_parts, div_segs, div_items, div_bs;
     int32_t bt_stride;
     int32_t block_size;
     int32_t hs;                       // heads per source shard

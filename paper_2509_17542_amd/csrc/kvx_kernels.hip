@@ -87,15 +87,16 @@ struct SrcFmt {
     }
 };
 
-// One lane's 16 source elements (two 16-byte vectors) -> 16 e4m3fn bytes.
-// The row maximum is reduced over the lanes-per-row group (2^lg lanes,
-// consecutive, so xor shuffles stay inside the group); every lane of the
-// wave must execute this.
+// General path: one lane's 16 source elements (two 16-byte vectors) -> 16
+// e4m3fn bytes, every case of the definition (NaN elements, zero rows, scales
+// too small or too large for the two-step divide), element by element in
+// software.  The row maximum is reduced over the lanes-per-row group (2^lg
+// lanes, consecutive, so xor shuffles stay inside the group); every lane of the
+// wave must execute the reduction.
 template <int CONV>
-__device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& scale_out)
+__device__ __forceinline__ uint4 to_e4m3_general(const uint32_t (&w)[8], int lg, float& scale_out)
 {
     using F = SrcFmt<CONV>;
-    const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
     uint32_t m = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -129,6 +130,47 @@ __device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& sca
             code = q != q ? 0x7Fu : e4m3_code(q);
         }
         out[k >> 2] |= (code | ((h >> 8) & 0x80u)) << ((k & 3) * 8);
+    }
+    return make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+// One lane's 16 source elements -> 16 e4m3fn bytes.  Fast path for rows with
+// no NaN and a scale in [2^-80, 2^100]: the row maximum from packed 16-bit
+// maxima, the exact quotient |x| / s, the element's sign set on it, and the
+// hardware conversion v_cvt_pk_fp8_f32 (round to nearest even, OCP e4m3fn on
+// gfx950; it equals e4m3_code on every fp32 magnitude up to 448, and a
+// quotient cannot round above 448 because |x| <= amax).  Other rows take the
+// general path.  Every lane of the wave must execute this.
+template <int CONV>
+__device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& scale_out)
+{
+    using F = SrcFmt<CONV>;
+    typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+    const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+    us2 mm = {0, 0};
+#pragma unroll
+    for (int k = 0; k < 8; ++k)  // magnitudes, NaN included
+        mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
+    uint32_t m = max(uint32_t(mm.x), uint32_t(mm.y));
+    for (int o = 1; o < (1 << lg); o <<= 1)
+        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    const float s = F::widen(m) / 448.0f;  // IEEE divide; NaN if the row holds a NaN
+    if (!(s >= 0x1p-80f && s <= 0x1p100f)) return to_e4m3_general<CONV>(w, lg, scale_out);
+    scale_out = s;
+    const float r0 = __builtin_amdgcn_rcpf(s);
+    const float r = __builtin_fmaf(__builtin_fmaf(-s, r0, 1.0f), r0, r0);
+    uint32_t out[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {  // output dword d = elements 4d .. 4d+3 = source words 2d, 2d+1
+        float q[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t h = (w[2 * d + (e >> 1)] >> ((e & 1) * 16)) & 0xFFFFu;
+            q[e] = __uint_as_float(__float_as_uint(quotient(F::widen(h & 0x7FFFu), s, r)) |
+                                   ((h & 0x8000u) << 16));
+        }
+        const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+        out[d] = uint32_t(__builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true));
     }
     return make_uint4(out[0], out[1], out[2], out[3]);
 }
@@ -179,9 +221,19 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     const int lg = a.lg_lpr;
     const int sub = threadIdx.x & ((1 << lg) - 1);          // 16-byte chunk within the row
     const int r = int(part) * (kThreads >> lg) + (threadIdx.x >> lg);  // row within the segment
-    const bool ok = sub < a.cpr && r < seg_rows;
-    const int s = int(fdiv(uint32_t(r), seg.div_n));       // token within the page
-    const int ii = r - s * seg.n;                           // head within the segment
+    int s, ii;  // token within the page, head within the segment
+    bool ok;
+    if constexpr (ORDER == KVX_HTD && MODE != kUnpack) {
+        // head-major rows: consecutive lane groups read consecutive tokens of one
+        // head, contiguous in a [head][token][dim] source
+        ii = int(fdiv(uint32_t(r), a.div_bs));
+        s = r - ii * a.block_size;
+        ok = sub < a.cpr && ii < seg.n && s < seg_rows / seg.n;
+    } else {
+        s = int(fdiv(uint32_t(r), seg.div_n));
+        ii = r - s * seg.n;
+        ok = sub < a.cpr && r < seg_rows;
+    }
     const int row = s * a.hd + seg.i0 + ii;                 // row within the page
 
     uint4 v[kVecs];

@@ -375,6 +375,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.div_parts = kvx::make_fastdiv(a.parts);
     a.div_segs = kvx::make_fastdiv(a.num_segs);
     a.div_items = kvx::make_fastdiv(a.num_items);
+    a.div_bs = kvx::make_fastdiv(uint32_t(d.block_size));
     a.num_blocks = d.num_blocks;
     a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_dst;
     a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
