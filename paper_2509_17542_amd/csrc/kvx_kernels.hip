@@ -175,13 +175,33 @@ __device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& sca
     return make_uint4(out[0], out[1], out[2], out[3]);
 }
 
+// 8 fp16 -> 8 bf16.  Without NaN (the usual case): exact widening and the
+// hardware v_cvt_pk_bf16_f32 (round to nearest even, the C semantics of a
+// float -> bfloat conversion).  A NaN anywhere in the 8 sends them through
+// f16_to_bf16, which fixes the NaN payload rule.
 __device__ __forceinline__ uint4 to_bf16x8(const uint4& v)
 {
+    typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[4];
+    us2 mm = {0, 0};
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-        o[k] = f16_to_bf16(w[k] & 0xFFFFu) | (f16_to_bf16(w[k] >> 16) << 16);
+        mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
+    uint32_t o[4];
+    if (max(uint32_t(mm.x), uint32_t(mm.y)) <= 0x7C00u) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const f2 f = __builtin_convertvector(__builtin_bit_cast(h2, w[k]), f2);
+            o[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, b2));
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            o[k] = f16_to_bf16(w[k] & 0xFFFFu) | (f16_to_bf16(w[k] >> 16) << 16);
+    }
     return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
