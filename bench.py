@@ -265,12 +265,13 @@ def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
         return {g: statistics.median(v) for g, v in vals.items()}
 
     f, wr = per_grid(fetch_csv, "FETCH_SIZE"), per_grid(write_csv, "WRITE_SIZE")
-    calib_grid = (w_tokens // 16) * 2 * 512                 # units x 512 threads (xcd-rounded)
-    calib_grid = ((calib_grid // 512 + 7) // 8) * 8 * 512
-    others = [g for g in f if g != calib_grid]
-    assert calib_grid in f and calib_grid in wr and len(others) == 1, (sorted(f), calib_grid)
-    g = others[0]
-    kf, kw = calib_bytes / f[calib_grid], calib_bytes / wr[calib_grid]
+    # the calibration dispatches are the ones whose written bytes are the
+    # memcpy's (WRITE_SIZE counts 64-byte write requests exactly)
+    calib = [g for g in wr if abs(wr[g] - calib_bytes) < 0.01 * calib_bytes]
+    others = [g for g in f if g not in calib]
+    assert len(calib) == 1 and calib[0] in f and len(others) == 1, (sorted(wr.items()), calib_bytes)
+    g, cg = others[0], calib[0]
+    kf, kw = calib_bytes / f[cg], calib_bytes / wr[cg]
     rec = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
            "fetch_factor": round(kf, 4), "write_factor": round(kw, 4),
            "fetch_bytes_per_launch": round(f[g] * kf), "write_bytes_per_launch": round(wr[g] * kw),
