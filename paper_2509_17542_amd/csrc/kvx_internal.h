@@ -13,6 +13,7 @@ constexpr int kMaxHeadsPerRank = 1024;  // Hd limit
 constexpr int kMaxReadShards = 64;      // source shards one decode rank may read
 constexpr int kMaxRowChunks = 64;       // 16-byte destination chunks per row (one wave)
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
+constexpr int kPrefetchPages = 32;      // pages ahead whose address translation a workgroup warms
 // work units of one launch; the 1-D grid is this rounded up to a multiple of
 // kXcds, and grid * kThreads stays below 2^32
 constexpr int64_t kMaxUnits = (int64_t(1) << 24) - kXcds;

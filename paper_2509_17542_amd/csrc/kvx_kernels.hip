@@ -20,6 +20,14 @@
 // (i % 8) * units_per_xcd + i / 8, so every XCD streams one contiguous run of
 // units through its own L2 instead of every eighth unit of the whole stream.
 //
+// Destination pages of the paged cache are scattered over a pool of tens to
+// hundreds of GiB, so their first touch often waits for an address
+// translation.  The first workgroup of each page (part 0, segment 0) therefore
+// also reads one dword of the destination page kPrefetchPages pages further
+// along its XCD's run; the value is discarded, and the translation is cached by
+// the time that page's workgroups store to it.  Stores are non-temporal: the
+// destination is not read again by this launch.
+//
 // The path is a gather/scatter stream with no reuse and no contraction: it is
 // bound by HBM bandwidth, so there is no MFMA and no LDS staging (every row is
 // at least 128 contiguous bytes, i.e. whole cache lines on both sides, so a
@@ -212,6 +220,25 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f)
     return uint32_t((uint64_t(__umulhi(n, f.mul)) + n) >> f.shift);
 }
 
+// Read one dword at the start of the destination page of the unit
+// kPrefetchPages pages after `unit` (same plane-major order), so that its
+// address translation is cached before that page's workgroups store to it.
+// The value is discarded; ids outside the pool are ignored.
+__device__ __forceinline__ void warm_translation(const KArgs& a, uint32_t unit)
+{
+    const uint32_t fu = unit + uint32_t(kPrefetchPages) * a.parts * a.num_segs;
+    if (fu >= a.units) return;
+    const uint32_t page_unit = fdiv(fdiv(fu, a.div_parts), a.div_segs);
+    const uint32_t plane = fdiv(page_unit, a.div_items);
+    const Item it = a.items[page_unit - plane * a.num_items];
+    const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
+    if (b < 0 || b >= a.num_blocks) return;
+    const volatile uint32_t* q = reinterpret_cast<const volatile uint32_t*>(
+        static_cast<const char*>(a.dst) + plane * a.plane_bytes +
+        int64_t(b) * a.block_size * a.hd * a.row_dst_bytes);
+    (void)*q;
+}
+
 template <int MODE, int CONV, int ORDER>
 __device__ __forceinline__ void convert_part(const KArgs& a)
 {
@@ -290,6 +317,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
             sbase = reinterpret_cast<float*>(static_cast<char*>(a.dst) + it.wire_scale) + row0;
     } else {
         const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
+        if (part == 0 && sg == 0 && threadIdx.x == 0) warm_translation(a, unit);
         if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
         const int64_t page_rows = int64_t(b) * a.block_size * a.hd;
         dbase = static_cast<char*>(a.dst) + plane * a.plane_bytes + page_rows * a.row_dst_bytes;
@@ -304,9 +332,12 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     else
         out = v[0];
     if (ok) {
-        *reinterpret_cast<uint4*>(dbase + int64_t(row) * a.row_dst_bytes + sub * 16) = out;
+        typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+        __builtin_nontemporal_store(__builtin_bit_cast(v4u, out),
+                                    reinterpret_cast<v4u*>(dbase + int64_t(row) * a.row_dst_bytes +
+                                                           sub * 16));
         if constexpr (kScales)
-            if (sub == 0) sbase[row] = sc;
+            if (sub == 0) __builtin_nontemporal_store(sc, sbase + row);
     }
 }
 
