@@ -165,7 +165,7 @@ def main():
     traffic = measured_traffic(w.name)
     out["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                       "traffic": traffic, "kernel": "kvx convert_rows<repack>",
+                       "traffic": traffic, "kernel": "kvx_repack_kernel",
                        "algorithmic_bytes_per_launch": rep_bytes}
 
     if not args.no_extras:
@@ -251,28 +251,33 @@ def copy_legs(K, torch, gib, timed, stream):
 def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
     """HBM bytes per repack launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
     (KiB per dispatch), each scaled by the ratio of known bytes to counted
-    bytes of the identity-memcpy repack in the same run (calib_gib GiB read and
-    as many written).  Dispatches are told apart by grid size."""
+    bytes of a plain copy kernel in the same run: torch's elementwise
+    bitwise_not over calib_gib GiB (read once, written once, nothing else).
+    The repack batch is the kvx_repack_kernel dispatch whose written bytes are
+    not the identity-layout copy's; dispatches are told apart by grid size."""
     import csv
-    w_tokens = int(calib_gib * CALIB_TOKENS_PER_GIB)
-    calib_bytes = w_tokens * 2 * 8 * 128 * 2
+    calib_bytes = int(calib_gib * CALIB_TOKENS_PER_GIB) * 2 * 8 * 128 * 2
 
-    def per_grid(path, counter):
+    def per_grid(path, counter, name):
         vals = {}
         for r in csv.DictReader(open(path)):
-            if r["Counter_Name"] == counter and "kvx_repack_kernel" in r["Kernel_Name"]:
+            if r["Counter_Name"] == counter and name in r["Kernel_Name"]:
                 vals.setdefault(int(r["Grid_Size"]), []).append(float(r["Counter_Value"]) * 1024)
         return {g: statistics.median(v) for g, v in vals.items()}
 
-    f, wr = per_grid(fetch_csv, "FETCH_SIZE"), per_grid(write_csv, "WRITE_SIZE")
-    # the calibration dispatches are the ones whose written bytes are the
-    # memcpy's (WRITE_SIZE counts 64-byte write requests exactly)
-    calib = [g for g in wr if abs(wr[g] - calib_bytes) < 0.01 * calib_bytes]
-    others = [g for g in f if g not in calib]
-    assert len(calib) == 1 and calib[0] in f and len(others) == 1, (sorted(wr.items()), calib_bytes)
-    g, cg = others[0], calib[0]
-    kf, kw = calib_bytes / f[cg], calib_bytes / wr[cg]
+    cf = per_grid(fetch_csv, "FETCH_SIZE", "bitwise_not")
+    cw = per_grid(write_csv, "WRITE_SIZE", "bitwise_not")
+    assert len(cf) == 1 and len(cw) == 1, (cf, cw)
+    kf, kw = calib_bytes / next(iter(cf.values())), calib_bytes / next(iter(cw.values()))
+    f = per_grid(fetch_csv, "FETCH_SIZE", "kvx_repack_kernel")
+    wr = per_grid(write_csv, "WRITE_SIZE", "kvx_repack_kernel")
+    # the identity-layout copy writes exactly calib_bytes; WRITE_SIZE counts
+    # 64-byte write requests exactly
+    batch = [g for g in wr if abs(wr[g] * kw - calib_bytes) > 0.01 * calib_bytes]
+    assert len(batch) == 1 and batch[0] in f, (sorted(wr.items()), calib_bytes)
+    g = batch[0]
     rec = {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+           "calibration": f"torch bitwise_not copy, {calib_bytes} bytes read and written",
            "fetch_factor": round(kf, 4), "write_factor": round(kw, 4),
            "fetch_bytes_per_launch": round(f[g] * kf), "write_bytes_per_launch": round(wr[g] * kw),
            "bytes_per_launch": round(f[g] * kf + wr[g] * kw),
