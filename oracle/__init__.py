@@ -22,7 +22,7 @@ _SRC = os.path.join(_HERE, "kvx_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 FP16, BF16, E4M3FN = 1, 2, 3
-TOKEN_MAJOR, HEAD_MAJOR = 0, 1
+TOKEN_MAJOR, HEAD_MAJOR, PAGED = 0, 1, 2
 FMT_SIZE = {FP16: 2, BF16: 2, E4M3FN: 1}
 
 GCC_CMD = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-fPIC", "-shared",
@@ -90,18 +90,28 @@ class Problem(ctypes.Structure):
         ("src_fmt", ctypes.c_int32), ("dst_fmt", ctypes.c_int32), ("src_order", ctypes.c_int32),
         ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int64),
         ("num_requests", ctypes.c_int32), ("seq_lens", ctypes.POINTER(ctypes.c_int32)),
+        ("src_block_size", ctypes.c_int32), ("src_num_blocks", ctypes.c_int64),
+        ("src_block_table", ctypes.POINTER(ctypes.c_int32)), ("src_bt_stride", ctypes.c_int32),
     ]
 
 
 class OracleProblem:
-    """Problem description plus the seq_lens array it points into."""
+    """Problem description plus the arrays it points into (seq_lens, and for a
+    PAGED source the source block table [num_requests][src_bt_stride])."""
 
     def __init__(self, layers, heads, head_dim, src_tp, dst_tp, dst_rank, src_fmt, dst_fmt,
-                 src_order, block_size, num_blocks, seq_lens):
+                 src_order, block_size, num_blocks, seq_lens, src_block_size=0,
+                 src_num_blocks=0, src_block_table=None, src_bt_stride=0):
         self.seq_lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32))
+        self.src_block_table = None
+        sbt = ctypes.POINTER(ctypes.c_int32)()
+        if src_block_table is not None:
+            self.src_block_table = np.ascontiguousarray(np.asarray(src_block_table, dtype=np.int32))
+            sbt = self.src_block_table.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
         self.c = Problem(layers, heads, head_dim, src_tp, dst_tp, dst_rank, src_fmt, dst_fmt,
                          src_order, block_size, num_blocks, len(self.seq_lens),
-                         self.seq_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+                         self.seq_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                         src_block_size, src_num_blocks, sbt, src_bt_stride)
 
     def __getattr__(self, name):
         return getattr(self.__dict__["c"], name)
@@ -238,11 +248,13 @@ def repack(p: OracleProblem, shards, cache, scales, block_table, bt_stride):
     return cache, scales
 
 
-def expected_rows(p: OracleProblem, shards, r, l, kv, t0, nt):
-    """Expected destination rows (nt*Hd, D*esize bytes) and scales (or None)."""
+def expected_rows(p: OracleProblem, shards, r, l, kv, t0, nt, sentinel=0xA5):
+    """Expected destination rows (nt*Hd, D*esize bytes) and scales (or None).
+    Rows with no source (a source page outside the source pool) keep the
+    sentinel bytes, as the destination does."""
     row_bytes = p.head_dim * p.dst_size
-    out = np.empty((nt * p.hd, row_bytes), dtype=np.uint8)
-    sc = np.zeros(nt * p.hd, dtype=np.float32)
+    out = np.full((nt * p.hd, row_bytes), sentinel, dtype=np.uint8)
+    sc = np.full(nt * p.hd * 4, sentinel, dtype=np.uint8).view(np.float32)
     _check(lib().orc_expected_rows(p.ref(), _shard_ptrs(shards), r, l, kv, t0, nt, _ptr(out),
                                    _ptr(sc)))
     return out, (sc if p.dst_fmt == E4M3FN else None)

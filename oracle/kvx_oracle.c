@@ -233,7 +233,16 @@ int orc_validate(const orc_problem *p)
     if (p->num_requests < 0 || (p->num_requests > 0 && !p->seq_lens)) return -1;
     for (int r = 0; r < p->num_requests; ++r)
         if (p->seq_lens[r] < 0) return -1;
-    if (p->src_order != ORC_TOKEN_MAJOR && p->src_order != ORC_HEAD_MAJOR) return -1;
+    if (p->src_order != ORC_TOKEN_MAJOR && p->src_order != ORC_HEAD_MAJOR &&
+        p->src_order != ORC_PAGED)
+        return -1;
+    if (p->src_order == ORC_PAGED) {
+        if (p->src_block_size <= 0 || p->src_num_blocks <= 0) return -1;
+        for (int r = 0; r < p->num_requests; ++r) {
+            int64_t nb = ((int64_t)p->seq_lens[r] + p->src_block_size - 1) / p->src_block_size;
+            if (nb > 0 && (!p->src_block_table || p->src_bt_stride < nb)) return -1;
+        }
+    }
     int sf = p->src_fmt, df = p->dst_fmt;
     if (sf != ORC_FP16 && sf != ORC_BF16) return -2;
     if (sf == df) return 0;
@@ -259,6 +268,7 @@ int64_t orc_src_request_base(const orc_problem *p, int r)
 {
     int64_t Hs = p->heads / p->src_tp;
     int64_t base = 0;
+    if (p->src_order == ORC_PAGED) return 0; /* pages, not back-to-back requests */
     for (int q = 0; q < r; ++q)
         base += (int64_t)p->layers * 2 * p->seq_lens[q] * Hs * p->head_dim;
     return base;
@@ -276,6 +286,14 @@ static int64_t src_index_from(const orc_problem *p, int64_t base, int r, int l, 
     int64_t T = p->seq_lens[r];
     int64_t D = p->head_dim;
     int64_t plane = (int64_t)l * 2 + kv;
+    if (p->src_order == ORC_PAGED) {
+        /* the prefill side's paged cache: token t sits in page
+         * src_block_table[r][t / src_block_size], slot t % src_block_size */
+        int64_t blk = p->src_block_table[(int64_t)r * p->src_bt_stride + t / p->src_block_size];
+        int64_t slot = t % p->src_block_size;
+        if (blk < 0 || blk >= p->src_num_blocks) return -1;
+        return (((plane * p->src_num_blocks + blk) * p->src_block_size + slot) * Hs + h) * D + d;
+    }
     if (p->src_order == ORC_TOKEN_MAJOR)
         return base + ((plane * T + t) * Hs + h) * D + d;
     return base + ((plane * Hs + h) * T + t) * D + d;
@@ -329,17 +347,21 @@ int64_t orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_
     return align256(off);
 }
 
-/* Gather source row (r, l, kv, t, i) element by element and convert it. */
-static void source_row_converted(const orc_problem *p, const void *const *shards, int64_t base,
-                                 int r, int l, int kv, int t, int i, uint16_t *tmp, void *out_row,
-                                 float *scale)
+/* Gather source row (r, l, kv, t, i) element by element and convert it.
+ * Returns 0, writing nothing, when the row has no source (a source page id
+ * outside the source pool). */
+static int source_row_converted(const orc_problem *p, const void *const *shards, int64_t base,
+                                int r, int l, int kv, int t, int i, uint16_t *tmp, void *out_row,
+                                float *scale)
 {
     for (int d = 0; d < p->head_dim; ++d) {
         int j;
         int64_t idx = src_index_from(p, base, r, l, kv, t, i, d, &j);
+        if (idx < 0) return 0;
         tmp[d] = ((const uint16_t *)shards[j])[idx];
     }
     orc_convert_row(p->src_fmt, p->dst_fmt, p->head_dim, tmp, out_row, scale);
+    return 1;
 }
 
 int orc_pack(const orc_problem *p, const void *const *shards, void *wire)
@@ -362,9 +384,9 @@ int orc_pack(const orc_problem *p, const void *const *shards, void *wire)
                     for (int i = 0; i < Hd; ++i) {
                         int64_t row = (((int64_t)l * 2 + kv) * T + t) * Hd + i;
                         float sc = 0.0f;
-                        source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
-                                             w + doff[r] + row * D * esz, &sc);
-                        if (p->dst_fmt == ORC_E4M3FN)
+                        if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
+                                                 w + doff[r] + row * D * esz, &sc) &&
+                            p->dst_fmt == ORC_E4M3FN)
                             memcpy(w + soff[r] + row * 4, &sc, 4);
                     }
     }
@@ -391,6 +413,7 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
                 for (int t = 0; t < T; ++t) {
                     int64_t b = block_table[(int64_t)r * bt_stride + t / bs];
                     int slot = t % bs;
+                    if (b < 0 || b >= p->num_blocks) continue;  /* not a page of the pool */
                     for (int i = 0; i < Hd; ++i) {
                         int64_t row = (((int64_t)l * 2 + kv) * T + t) * Hd + i;
                         memcpy(c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
@@ -422,12 +445,13 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
                 for (int t = 0; t < T; ++t) {
                     int64_t b = block_table[(int64_t)r * bt_stride + t / bs];
                     int slot = t % bs;
+                    if (b < 0 || b >= p->num_blocks) continue;  /* not a page of the pool */
                     for (int i = 0; i < Hd; ++i) {
                         float sc = 0.0f;
-                        source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
-                                             c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
-                                             &sc);
-                        if (p->dst_fmt == ORC_E4M3FN)
+                        if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
+                                                 c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
+                                                 &sc) &&
+                            p->dst_fmt == ORC_E4M3FN)
                             scales[orc_cache_scale_index(p, b, l, kv, slot, i)] = sc;
                     }
                 }
@@ -452,8 +476,9 @@ int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, in
         for (int i = 0; i < Hd; ++i) {
             int64_t row = (int64_t)(t - t0) * Hd + i;
             float sc = 0.0f;
-            source_row_converted(p, shards, base, r, l, kv, t, i, tmp, o + row * D * esz, &sc);
-            if (p->dst_fmt == ORC_E4M3FN && out_scales) out_scales[row] = sc;
+            if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, o + row * D * esz, &sc) &&
+                p->dst_fmt == ORC_E4M3FN && out_scales)
+                out_scales[row] = sc;
         }
     free(tmp);
     return 0;

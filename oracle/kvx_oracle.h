@@ -26,8 +26,14 @@ extern "C" {
 
 /* element formats */
 enum { ORC_FP16 = 1, ORC_BF16 = 2, ORC_E4M3FN = 3 };
-/* source storage orders of one (layer, k/v) plane of a request */
-enum { ORC_TOKEN_MAJOR = 0 /* [token][head][dim] */, ORC_HEAD_MAJOR = 1 /* [head][token][dim] */ };
+/* source storage orders: one (layer, k/v) plane of a request stored
+ * contiguously, or the prefill side's own paged cache */
+enum {
+    ORC_TOKEN_MAJOR = 0, /* request r: [layer][k/v][token][head][dim] */
+    ORC_HEAD_MAJOR = 1,  /* request r: [layer][k/v][head][token][dim] */
+    ORC_PAGED = 2        /* shard pool [layer][k/v][src_num_blocks][src_block_size][head][dim],
+                            token t of request r in page src_block_table[r][t / src_block_size] */
+};
 
 typedef struct {
     int32_t layers;      /* L */
@@ -43,6 +49,11 @@ typedef struct {
     int64_t num_blocks;  /* pages in the destination pool (per plane) */
     int32_t num_requests;
     const int32_t *seq_lens; /* [num_requests], tokens per request */
+    /* ORC_PAGED sources only (ignored otherwise): the prefill side's pages */
+    int32_t src_block_size;
+    int64_t src_num_blocks;
+    const int32_t *src_block_table; /* [num_requests][src_bt_stride] */
+    int32_t src_bt_stride;
 } orc_problem;
 
 /* ---- casts (precision alignment) ---- */
@@ -61,7 +72,9 @@ void     orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row,
 /* ---- index maps (parallel-strategy and VRAM-management alignment) ---- */
 int      orc_validate(const orc_problem *p);             /* 0 ok, -1 invalid, -2 unsupported */
 void     orc_head_source(const orc_problem *p, int i, int *shard, int *head);
-int64_t  orc_src_request_base(const orc_problem *p, int r);  /* elements */
+int64_t  orc_src_request_base(const orc_problem *p, int r);  /* elements; 0 for ORC_PAGED */
+/* element index in shard *shard, or -1 when the token's source page id lies
+ * outside [0, src_num_blocks) (ORC_PAGED): such a row is never written */
 int64_t  orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, int d, int *shard);
 int64_t  orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d);
 int64_t  orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i);
@@ -69,7 +82,9 @@ int64_t  orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int k
 int64_t  orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off);
 int      orc_fmt_size(int fmt);
 
-/* ---- the three operations ---- */
+/* ---- the three operations ----
+ * A destination page id outside [0, num_blocks) is skipped, and so is a row
+ * whose source page id lies outside the source pool: neither writes a byte. */
 int orc_pack(const orc_problem *p, const void *const *shards, void *wire);
 int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scales,
                const int32_t *block_table, int32_t bt_stride);
@@ -77,7 +92,8 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
                const int32_t *block_table, int32_t bt_stride);
 
 /* expected destination rows of request r, plane (l, kv), tokens [t0, t0+nt):
- * nt*Hd rows in (token, head) order, plus nt*Hd scales for e4m3fn */
+ * nt*Hd rows in (token, head) order, plus nt*Hd scales for e4m3fn; rows whose
+ * source page lies outside the source pool are left as the caller filled them */
 int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, int l, int kv,
                       int t0, int nt, void *out_rows, float *out_scales);
 

@@ -17,6 +17,8 @@ L8B = FULL["llama3_8b_bf16_bs16"]
 L70B = FULL["llama3_70b_tp4to2_bf16_bs32"]
 QWEN = FULL["qwen7b_htd_fp16_bf16_bs64"]
 FP8 = FULL["fp8_decode_61l_bf16_e4m3_bs16"]
+P8B = FULL["llama3_8b_paged16_bf16_bs64"]
+P70B = FULL["llama3_70b_paged16_tp4to2_bf16_bs32"]
 
 SMALL = {
     "tiny": TINY,
@@ -50,6 +52,31 @@ SMALL = {
                                         num_blocks=16, seed=99),
 }
 
+# Paged sources (the prefill side's own paged cache), same shapes as the two
+# full paged workloads plus page-size ratios that do not divide each other.
+SMALL_PAGED = {
+    "paged16_bs64_small": P8B.replace(name="paged16_bs64_small", layers=2, total_layers=2,
+                                      num_requests=3, len_lo=17, len_hi=150, num_blocks=16,
+                                      src_num_blocks=48),
+    "paged16_tp4to2_bs32_small": P70B.replace(name="paged16_tp4to2_bs32_small", layers=2,
+                                              total_layers=2, num_requests=2, len_lo=33,
+                                              len_hi=90, num_blocks=16, src_num_blocks=24),
+    # 24-token prefill pages -> 16-token decode pages (neither divides the other)
+    "paged24_bs16_r1": P70B.replace(name="paged24_bs16_r1", layers=1, total_layers=1,
+                                    dst_rank=1, num_requests=3, len_lo=1, len_hi=80,
+                                    block_size=16, num_blocks=32, src_block_size=24,
+                                    src_num_blocks=16),
+    # 16 -> 24-token pages, bf16 -> e4m3fn, one empty request
+    "paged16_e4m3_bs24": FP8.replace(name="paged16_e4m3_bs24", src_order="paged", layers=2,
+                                     total_layers=3, num_requests=3, lens_override=(50, 0, 7),
+                                     block_size=24, num_blocks=16, src_block_size=16,
+                                     src_num_blocks=16),
+    # fp16 -> bf16 split TP1 -> TP2 rank 0 from 5-token prefill pages
+    "paged5_fp16_split": TINY.replace(name="paged5_fp16_split", src_order="paged", num_requests=2,
+                                      len_lo=3, len_hi=40, lens_override=None,
+                                      src_block_size=5, src_num_blocks=24),
+}
+
 
 def fmt_codes(mod):
     """dtype name -> the integer code used by `mod` (oracle or GPU binding)."""
@@ -60,12 +87,20 @@ def dst_size(w):
     return 1 if w.dst_dtype == "e4m3fn" else 2
 
 
-def oracle_problem(O, w, lens, layers=None):
+def oracle_problem(O, w, lens, layers=None, sbt=None):
+    """The oracle's problem for workload w; a paged source takes the
+    generator's source block table unless `sbt` ([R, stride] int32) is given."""
     f = fmt_codes(O)
-    order = O.TOKEN_MAJOR if w.src_order == "thd" else O.HEAD_MAJOR
+    order = {"thd": O.TOKEN_MAJOR, "htd": O.HEAD_MAJOR, "paged": O.PAGED}[w.src_order]
+    extra = {}
+    if w.src_order == "paged":
+        if sbt is None:
+            sbt, _ = W.src_block_table(w, lens)
+        extra = dict(src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
+                     src_block_table=sbt, src_bt_stride=sbt.shape[1])
     return O.OracleProblem(layers or w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp,
                            w.dst_rank, f[w.src_dtype], f[w.dst_dtype], order, w.block_size,
-                           w.num_blocks, lens)
+                           w.num_blocks, lens, **extra)
 
 
 def inputs(w, layer0=0, nlayers=None):

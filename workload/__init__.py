@@ -9,7 +9,8 @@ values.
 
 The C core (``gen.c``) is a counter-based splitmix64 stream; see its header.
 Streams: 1 sequence lengths, 2 block-table permutation, 3 values,
-4 outlier mask, 5 outlier sign, 6 per-(layer, k/v, head) scale.
+4 outlier mask, 5 outlier sign, 6 per-(layer, k/v, head) scale, 7 the
+prefill side's own block-table permutation (paged sources).
 """
 from __future__ import annotations
 
@@ -29,7 +30,7 @@ GCC_CMD = ["gcc", "-std=c99", "-O2", "-Wall", "-fPIC", "-shared", "-pthread", "-
 
 SENTINEL = 0xA5
 
-S_LENS, S_TABLE, S_VALUES, S_OUTLIER, S_OUTSIGN, S_HEADSCALE = 1, 2, 3, 4, 5, 6
+S_LENS, S_TABLE, S_VALUES, S_OUTLIER, S_OUTSIGN, S_HEADSCALE, S_SRC_TABLE = 1, 2, 3, 4, 5, 6, 7
 
 
 def build() -> str:
@@ -80,7 +81,8 @@ class Workload:
     dst_rank: int
     src_dtype: str         # "fp16" | "bf16"
     dst_dtype: str         # "fp16" | "bf16" | "e4m3fn"
-    src_order: str         # "thd" = [token][head][dim], "htd" = [head][token][dim]
+    src_order: str         # "thd" = [token][head][dim], "htd" = [head][token][dim],
+                           # "paged" = the prefill side's own paged cache
     block_size: int
     num_blocks: int
     num_requests: int
@@ -92,6 +94,8 @@ class Workload:
     outlier_value: float = 0.0
     head_scale_log10: tuple | None = None
     lens_override: tuple | None = None   # explicit tokens per request (edge cases)
+    src_block_size: int = 0  # "paged" sources: tokens per prefill-side page
+    src_num_blocks: int = 0  # "paged" sources: pages per (layer, k/v) plane of each shard's pool
 
     @property
     def hs(self):
@@ -149,6 +153,17 @@ WORKLOADS = {
         # pages of a 2^20-page pool
         Workload("fp8_decode_61l_bf16_e4m3_bs16", 4, 61, 8, 128, 1, 1, 0, "bf16", "e4m3fn", "thd",
                  16, 1 << 20, 64, 256, 16384, seed=17546, head_scale_log10=(-2.0, 2.0)),
+        # paged -> paged, Llama-3-8B KV shape: the prefill side's own cache of
+        # 16-token pages (4096-page pool) re-paged into 64-token decode pages
+        # (4096-page pool); 16 requests of 512..4096 tokens, bf16
+        Workload("llama3_8b_paged16_bf16_bs64", 32, 32, 8, 128, 1, 1, 0, "bf16", "bf16", "paged",
+                 64, 4096, 16, 512, 4096, seed=17547, src_block_size=16, src_num_blocks=4096),
+        # paged -> paged with a TP change, Llama-3-70B shard: prefill TP4 caches
+        # of 16-token pages (4096-page pool per shard) -> decode TP2 rank 0 with
+        # 32-token pages (16384-page pool); 8 requests of 1024..8192 tokens, bf16
+        Workload("llama3_70b_paged16_tp4to2_bf16_bs32", 80, 80, 8, 128, 4, 2, 0, "bf16", "bf16",
+                 "paged", 32, 16384, 8, 1024, 8192, seed=17548, src_block_size=16,
+                 src_num_blocks=4096),
     ]
 }
 
@@ -184,6 +199,26 @@ def block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
         bt[r, :n] = perm[pos:pos + n]
         pos += n
     return bt, stride
+
+
+def src_block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
+    """The prefill side's pages for each request ("paged" sources), drawn in
+    order from a seeded permutation of its pool (stream 7).  The same table
+    serves every prefill shard.  Returns ([R, stride] int32, -1 in unused
+    entries, stride)."""
+    sbs = w.src_block_size
+    nblk = [(int(t) + sbs - 1) // sbs for t in lens]
+    stride = max(nblk + [1])
+    need = sum(nblk)
+    if need > w.src_num_blocks:
+        raise ValueError(f"{w.name}: {need} source pages needed, pool has {w.src_num_blocks}")
+    perm = permutation(w.seed, w.src_num_blocks, S_SRC_TABLE)
+    sbt = np.full((len(lens), stride), -1, dtype=np.int32)
+    pos = 0
+    for r, n in enumerate(nblk):
+        sbt[r, :n] = perm[pos:pos + n]
+        pos += n
+    return sbt, stride
 
 
 def _request_value_base(w: Workload, lens: np.ndarray, r: int) -> int:
@@ -251,15 +286,20 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
 
     Shard j holds global heads [j*Hs, (j+1)*Hs); requests are stored back to
     back, each as [layer][k/v][token][head][dim] ("thd") or
-    [layer][k/v][head][token][dim] ("htd").  Values are rounded from float32
-    to the storage type by torch (round to nearest even).  Shards not listed
-    are None."""
+    [layer][k/v][head][token][dim] ("htd").  A "paged" shard is instead the
+    prefill side's pool [layer][k/v][src_num_blocks][src_block_size][head][dim]:
+    token t of request r sits in page src_block_table(w, lens)[r][t //
+    src_block_size], slot t % src_block_size; slots holding no token keep the
+    sentinel bytes.  Values are rounded from float32 to the storage type by
+    torch (round to nearest even).  Shards not listed are None."""
     import torch
     if nlayers is None:
         nlayers = w.layers
     if shards is None:
         shards = w.read_shards()
     Hs, D = w.hs, w.head_dim
+    if w.src_order == "paged":
+        return _paged_source_shards(w, lens, layer0, nlayers, shards)
     per_shard = sum(nlayers * 2 * int(t) * Hs * D for t in lens)
     out: list[np.ndarray | None] = [None] * w.src_tp
     for j in shards:
@@ -281,4 +321,33 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
             else:
                 dst.view(nlayers, 2, Hs, T, D).copy_(vals)
         off += n
+    return out
+
+
+def _paged_source_shards(w: Workload, lens: np.ndarray, layer0: int, nlayers: int,
+                         shards: list[int]) -> list[np.ndarray | None]:
+    import torch
+    Hs, D, sbs, nbs = w.hs, w.head_dim, w.src_block_size, w.src_num_blocks
+    sbt, _ = src_block_table(w, lens)
+    out: list[np.ndarray | None] = [None] * w.src_tp
+    for j in shards:
+        out[j] = np.full(nlayers * 2 * nbs * sbs * Hs * D, SENTINEL * 0x0101, dtype=np.uint16)
+    scratch = np.empty(max([nlayers * 2 * int(t) * Hs * D for t in lens] + [1]), np.float32)
+    tdt = _TORCH_DTYPE[w.src_dtype]()
+    for r in range(len(lens)):
+        T = int(lens[r])
+        if T == 0 or nlayers == 0:
+            continue
+        nb = (T + sbs - 1) // sbs
+        full = T // sbs
+        for j in shards:
+            vals = torch.from_numpy(
+                logical_values(w, lens, r, layer0, nlayers, (j * Hs, (j + 1) * Hs), scratch))
+            x = vals.permute(0, 1, 3, 2, 4).to(tdt).view(torch.int16).numpy()  # [l][kv][t][h][d]
+            pool = out[j].view(np.int16).reshape(nlayers, 2, nbs, sbs, Hs, D)
+            ids = sbt[r, :nb]
+            if full:
+                pool[:, :, ids[:full]] = x[:, :, :full * sbs].reshape(nlayers, 2, full, sbs, Hs, D)
+            if T > full * sbs:
+                pool[:, :, ids[full], :T - full * sbs] = x[:, :, full * sbs:]
     return out
