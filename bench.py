@@ -102,11 +102,18 @@ def main():
     dshards = [None if s is None else torch.from_numpy(s.view(np.int16)).cuda() for s in shards]
     bt_d = torch.from_numpy(bt).cuda()
     F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
-    order = K.THD if w.src_order == "thd" else K.HTD
+    order = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order]
+    paged = w.src_order == "paged"
+    sbt = sbt_d = None
+    sstride = 0
+    if paged:   # the prefill side's own paged cache and its block table
+        sbt, sstride = W.src_block_table(w, lens)
+        sbt_d = torch.from_numpy(sbt).cuda()
 
     def desc(seq):
         return K.make_desc(w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
-                           F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks, seq)
+                           F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks, seq,
+                           w.src_block_size, w.src_num_blocks)
 
     plan = K.kvx_plan(desc(list(lens)))
     info = K.kvx_plan_info_get(plan)
@@ -136,7 +143,10 @@ def main():
         return wall * 1e3, statistics.mean(kern), min(kern), statistics.median(kern)
 
     def repack():
-        K.kvx_repack(plan, dshards, cache, scales, bt_d, stride, stream)
+        if paged:
+            K.kvx_repack_paged(plan, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream)
+        else:
+            K.kvx_repack(plan, dshards, cache, scales, bt_d, stride, stream)
 
     log(f"repack: {args.warmup} warm-up + {args.steps} timed steps")
     ms_step, k_mean, k_min, k_med = timed(repack, args.steps, args.warmup)
@@ -155,6 +165,8 @@ def main():
                    "src_dtype": w.src_dtype, "dst_dtype": w.dst_dtype,
                    "src_order": w.src_order, "block_size": w.block_size,
                    "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes},
+        **({"src_pages": {"block_size": w.src_block_size, "pool_blocks": w.src_num_blocks}}
+           if paged else {}),
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "repack_kernel_ms": {"mean": round(k_mean, 4), "min": round(k_min, 4),
                              "median": round(k_med, 4)},
@@ -172,7 +184,10 @@ def main():
         wire = torch.empty(int(info.wire_bytes), dtype=torch.uint8, device="cuda")
 
         def pack():
-            K.kvx_pack(plan, dshards, wire, stream)
+            if paged:
+                K.kvx_pack_paged(plan, dshards, sbt_d, sstride, wire, stream)
+            else:
+                K.kvx_pack(plan, dshards, wire, stream)
 
         def unpack():
             K.kvx_unpack(plan, wire, cache, scales, bt_d, stride, stream)
@@ -191,16 +206,26 @@ def main():
         src_off = 0
         for r, T in enumerate(lens.tolist()):
             p1 = K.kvx_plan(desc([T]))
-            sh = [None if s is None else s[src_off:] for s in dshards]
-            src_off += w.layers * 2 * T * w.hs * w.head_dim
             row = bt_d[r:r + 1]
+            if paged:   # the same pools, this request's row of the source block table
+                srow = sbt_d[r:r + 1]
+
+                def one():
+                    K.kvx_repack_paged(p1, dshards, srow, sstride, cache, scales, row, stride,
+                                       stream)
+            else:
+                sh = [None if s is None else s[src_off:] for s in dshards]
+
+                def one():
+                    K.kvx_repack(p1, sh, cache, scales, row, stride, stream)
+            src_off += w.layers * 2 * T * w.hs * w.head_dim
             ev = torch.cuda.Event()
-            K.kvx_repack(p1, sh, cache, scales, row, stride, stream)   # warm
+            one()   # warm
             torch.cuda.synchronize()
             reps = []
             for _ in range(5):
                 t = time.perf_counter()
-                K.kvx_repack(p1, sh, cache, scales, row, stride, stream)
+                one()
                 ev.record(stream)
                 ev.synchronize()
                 reps.append((time.perf_counter() - t) * 1e3)
@@ -214,7 +239,7 @@ def main():
         log(f"latency p50 {out['latency_ms_per_request']['p50']} ms")
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, lens, shards, args.cpu_seconds, value)
+        out["cpu_baseline"] = cpu_baseline(w, lens, shards, args.cpu_seconds, value, sbt)
     print(json.dumps(out), flush=True)
 
 
@@ -288,16 +313,17 @@ def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
     print(json.dumps(rec))
 
 
-def cpu_baseline(w, lens, shards, budget_s, gpu_value):
+def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None):
     """The oracle as it stands (single thread), on whole requests of the same
-    workload until about budget_s seconds of CPU work; pages renumbered into a
-    compact host pool (same rows, same bytes)."""
+    workload until about budget_s seconds of CPU work; decode pages renumbered
+    into a compact host pool (same rows, same bytes).  A paged source is read
+    in place through the request's row of the source block table."""
     import numpy as np
 
     import oracle as O
 
     f = {"fp16": O.FP16, "bf16": O.BF16, "e4m3fn": O.E4M3FN}
-    order = O.TOKEN_MAJOR if w.src_order == "thd" else O.HEAD_MAJOR
+    order = {"thd": O.TOKEN_MAJOR, "htd": O.HEAD_MAJOR, "paged": O.PAGED}[w.src_order]
     esz = 1 if w.dst_dtype == "e4m3fn" else 2
     done_bytes = 0
     spent = 0.0
@@ -308,10 +334,18 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value):
         if spent >= budget_s:
             break
         nb = (T + w.block_size - 1) // w.block_size
+        extra = {}
+        if sbt is not None:
+            extra = dict(src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
+                         src_block_table=sbt[r:r + 1], src_bt_stride=sbt.shape[1])
         p = O.OracleProblem(w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
-                            f[w.src_dtype], f[w.dst_dtype], order, w.block_size, max(nb, 1), [T])
+                            f[w.src_dtype], f[w.dst_dtype], order, w.block_size, max(nb, 1), [T],
+                            **extra)
         cnt = w.layers * 2 * T * w.hs * w.head_dim
-        part = [None if s is None else np.ascontiguousarray(s[off:off + cnt]) for s in shards]
+        if sbt is not None:
+            part = shards
+        else:
+            part = [None if s is None else np.ascontiguousarray(s[off:off + cnt]) for s in shards]
         off += cnt
         cache = np.empty(O.cache_bytes(p), dtype=np.uint8)
         sc = np.empty(O.scale_count(p), dtype=np.float32) if esz == 1 else None

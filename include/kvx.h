@@ -25,7 +25,12 @@
  *   source shard j (j = 0..src_tp-1) holds global heads [j*Hs, (j+1)*Hs),
  *     Hs = num_kv_heads / src_tp; requests are stored back to back, request r
  *     as [layer][k/v][token][Hs][dim] (KVX_THD) or [layer][k/v][Hs][token][dim]
- *     (KVX_HTD), T_r tokens;
+ *     (KVX_HTD), T_r tokens; or (KVX_PAGED) the shard is the prefill side's
+ *     own paged cache [layer][k/v][src_num_blocks][src_block_size][Hs][dim]:
+ *     token t of request r sits in page
+ *     src_block_table[r*src_bt_stride + t/src_block_size], slot
+ *     t % src_block_size, one source block table for all shards (both sides
+ *     of Sec. III-B-2 use paged attention, each with its own page size);
  *   decode rank dst_rank holds global heads [dst_rank*Hd, (dst_rank+1)*Hd),
  *     Hd = num_kv_heads / dst_tp;
  *   cache:  [layer][k/v][num_blocks][block_size][Hd][dim] in dst_dtype; token
@@ -37,13 +42,17 @@
  *     next 256-byte boundary [layer][k/v][token][Hd] fp32 scales.
  * Bytes outside these positions (slots past the end of a request's last page,
  * pages not in a block-table row, transfer-tensor padding) are never written.
+ * A page id outside its pool names no page: a decode page id outside
+ * [0, num_blocks) writes nothing, and a row whose source page id lies outside
+ * [0, src_num_blocks) is written neither to the cache nor to the transfer
+ * tensor (nor its scale).
  *
  * Ownership: every buffer is caller-owned device memory; the library never
  * allocates or frees it.  A plan is library-owned: kvx_plan copies seq_lens
  * and allocates a small device table on the device current at that time.
  *
- * Streams: kvx_pack / kvx_unpack / kvx_repack only enqueue work on the given
- * hipStream_t (passed as void*, NULL = default stream) and return; buffers must
+ * Streams: kvx_pack / kvx_unpack / kvx_repack (and the _paged forms) only
+ * enqueue work on the given hipStream_t (passed as void*, NULL = default stream) and return; buffers must
  * stay alive until the stream reaches that point.  A plan is immutable and may
  * be used concurrently on several streams of its device.
  *
@@ -62,7 +71,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 1
+#define KVX_ABI_VERSION 2
 
 typedef enum {
     KVX_OK = 0,
@@ -75,8 +84,9 @@ typedef enum {
 typedef enum { KVX_FP16 = 1, KVX_BF16 = 2, KVX_FP8_E4M3FN = 3 } kvx_dtype;
 
 typedef enum {
-    KVX_THD = 0, /* [token][head][dim] within one (layer, k/v) plane of a request */
-    KVX_HTD = 1  /* [head][token][dim] */
+    KVX_THD = 0,  /* [token][head][dim] within one (layer, k/v) plane of a request */
+    KVX_HTD = 1,  /* [head][token][dim] */
+    KVX_PAGED = 2 /* the prefill side's paged cache (kvx_pack_paged / kvx_repack_paged) */
 } kvx_order;
 
 typedef struct kvx_plan_s kvx_plan_t; /* opaque, library-owned */
@@ -99,6 +109,9 @@ typedef struct {
     int64_t num_blocks;     /* pages per (layer, k/v) plane of the pool, >= 1 */
     int32_t num_requests;   /* >= 0 */
     const int32_t *seq_lens;/* host array [num_requests], T_r >= 0; copied */
+    /* KVX_PAGED sources only (ignored otherwise): */
+    int32_t src_block_size; /* tokens per prefill-side page, >= 1 */
+    int64_t src_num_blocks; /* pages per (layer, k/v) plane of each shard's pool, >= 1 */
 } kvx_desc;
 
 typedef struct {
@@ -110,7 +123,7 @@ typedef struct {
     int32_t max_blocks_per_request; /* minimum valid bt_stride */
     int32_t num_items;              /* logical pages over all requests (per plane) */
     int32_t device;                 /* HIP device of the plan's tables, -1 = none */
-    int32_t reserved;
+    int32_t max_src_blocks_per_request; /* KVX_PAGED: minimum valid src_bt_stride; else 0 */
 } kvx_plan_info;
 
 /* Validate the problem and build a plan (host tables, plus a device table on
@@ -119,12 +132,14 @@ typedef struct {
  * Returns KVX_EINVAL for: NULL desc/out; a dimension <= 0; H % src_tp != 0 or
  * H % dst_tp != 0; dst_rank outside [0, dst_tp); block_size <= 0;
  * num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
- * an unknown order; head_dim * element size not a multiple of 16 bytes on
- * either side.  KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16,
- * bf16->bf16, fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row
- * (head_dim * dst size) above 1024 bytes; more than 1024 heads per decode
- * rank; more than 65535 source heads per shard; 2*L > 65535; more than 2^24-1
- * logical pages (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if the table cannot be allocated. */
+ * an unknown order; for KVX_PAGED, src_block_size <= 0 or src_num_blocks <= 0;
+ * head_dim * element size not a multiple of 16 bytes on either side.
+ * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
+ * fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row (head_dim * dst
+ * size) above 1024 bytes; more than 1024 heads per decode rank; more than
+ * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
+ * (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if
+ * the table cannot be allocated. */
 kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);
 
 kvx_status kvx_plan_info_get(const kvx_plan_t *plan, kvx_plan_info *info);
@@ -145,9 +160,9 @@ kvx_status kvx_plan_destroy(kvx_plan_t *plan);
  *               the layout above; shards the decode rank does not read may be
  *               NULL.  Each read pointer must be 16-byte aligned.
  *   wire:       device, >= wire_bytes, 16-byte aligned.
- * KVX_EINVAL for a NULL plan/array, a NULL or misaligned needed pointer;
- * KVX_EDEVICE for a host-only plan, a current device other than the plan's,
- * or a launch error. */
+ * KVX_EINVAL for a NULL plan/array, a NULL or misaligned needed pointer, a
+ * KVX_PAGED plan (use kvx_pack_paged); KVX_EDEVICE for a host-only plan, a
+ * current device other than the plan's, or a launch error. */
 kvx_status kvx_pack(const kvx_plan_t *plan, const void *const *src_shards, void *wire,
                     void *hip_stream);
 
@@ -169,15 +184,45 @@ kvx_status kvx_unpack(const kvx_plan_t *plan, const void *wire, void *cache, flo
                       const int32_t *block_table, int32_t bt_stride, void *hip_stream);
 
 /* Repack: kvx_pack followed by kvx_unpack in one pass with no transfer tensor;
- * the cache and scales it writes are bit-identical to that pair's. */
+ * the cache and scales it writes are bit-identical to that pair's.
+ * KVX_EINVAL for a KVX_PAGED plan (use kvx_repack_paged). */
 kvx_status kvx_repack(const kvx_plan_t *plan, const void *const *src_shards, void *cache,
                       float *scales, const int32_t *block_table, int32_t bt_stride,
                       void *hip_stream);
+
+/* Pack and repack from paged sources (plans with src_order KVX_PAGED): the
+ * prefill side's own paged caches, one per shard, with their own page size
+ * and block table (Sec. III-B-2), re-paged (and re-sharded and cast) into the
+ * decode layout.  Results are those of the contiguous source the pages
+ * describe.
+ *   src_shards:      as kvx_pack; shard j points to its pool
+ *                    [L][2][src_num_blocks][src_block_size][Hs][D].
+ *   src_block_table: device int32 [num_requests][src_bt_stride]; the first
+ *                    ceil(T_r/src_block_size) entries of row r are used.  A
+ *                    page may appear in several rows (a shared prefix); an
+ *                    id outside [0, src_num_blocks) leaves its rows unwritten.
+ *   src_bt_stride:   >= max_src_blocks_per_request.
+ * Errors as kvx_pack / kvx_repack, plus KVX_EINVAL for a plan whose source is
+ * not KVX_PAGED, a NULL source block table with tokens to move, or a short
+ * src_bt_stride. */
+kvx_status kvx_pack_paged(const kvx_plan_t *plan, const void *const *src_shards,
+                          const int32_t *src_block_table, int32_t src_bt_stride, void *wire,
+                          void *hip_stream);
+kvx_status kvx_repack_paged(const kvx_plan_t *plan, const void *const *src_shards,
+                            const int32_t *src_block_table, int32_t src_bt_stride, void *cache,
+                            float *scales, const int32_t *block_table, int32_t bt_stride,
+                            void *hip_stream);
 
 /* Host-side check of a block table: every used entry in [0, num_blocks) and no
  * page used twice.  KVX_EINVAL (with a message) otherwise. */
 kvx_status kvx_check_block_table(const kvx_plan_t *plan, const int32_t *host_block_table,
                                  int32_t bt_stride);
+
+/* Host-side check of a source block table (KVX_PAGED plans): every used entry
+ * in [0, src_num_blocks) and src_bt_stride >= max_src_blocks_per_request.
+ * Pages shared between requests are allowed.  KVX_EINVAL otherwise. */
+kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host_src_block_table,
+                                     int32_t src_bt_stride);
 
 /* Message for the calling thread's last non-OK status ("" if none). */
 const char *kvx_last_error(void);

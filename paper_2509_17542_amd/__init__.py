@@ -26,7 +26,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 OK, EINVAL, EUNSUPPORTED, ENOMEM, EDEVICE = 0, -1, -2, -3, -4
 FP16, BF16, E4M3FN = 1, 2, 3
-THD, HTD = 0, 1
+THD, HTD, PAGED = 0, 1, 2
 _STATUS = {0: "KVX_OK", -1: "KVX_EINVAL", -2: "KVX_EUNSUPPORTED", -3: "KVX_ENOMEM",
            -4: "KVX_EDEVICE"}
 
@@ -45,6 +45,7 @@ class kvx_desc(ctypes.Structure):
         ("dst_dtype", ctypes.c_int32), ("src_order", ctypes.c_int32),
         ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int64),
         ("num_requests", ctypes.c_int32), ("seq_lens", ctypes.POINTER(ctypes.c_int32)),
+        ("src_block_size", ctypes.c_int32), ("src_num_blocks", ctypes.c_int64),
     ]
 
 
@@ -55,7 +56,7 @@ class kvx_plan_info(ctypes.Structure):
         ("read_bytes_unpack", ctypes.c_int64), ("write_bytes_unpack", ctypes.c_int64),
         ("read_bytes_repack", ctypes.c_int64), ("write_bytes_repack", ctypes.c_int64),
         ("max_blocks_per_request", ctypes.c_int32), ("num_items", ctypes.c_int32),
-        ("device", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("device", ctypes.c_int32), ("max_src_blocks_per_request", ctypes.c_int32),
     ]
 
 
@@ -76,15 +77,22 @@ _lib.kvx_unpack.restype = ctypes.c_int
 _lib.kvx_unpack.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp]
 _lib.kvx_repack.restype = ctypes.c_int
 _lib.kvx_repack.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp]
+_lib.kvx_pack_paged.restype = ctypes.c_int
+_lib.kvx_pack_paged.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp]
+_lib.kvx_repack_paged.restype = ctypes.c_int
+_lib.kvx_repack_paged.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp]
 _lib.kvx_check_block_table.restype = ctypes.c_int
 _lib.kvx_check_block_table.argtypes = [_vp, _vp, _i32]
+_lib.kvx_check_src_block_table.restype = ctypes.c_int
+_lib.kvx_check_src_block_table.argtypes = [_vp, _vp, _i32]
 _lib.kvx_last_error.restype = ctypes.c_char_p
 _lib.kvx_last_error.argtypes = []
 _lib.kvx_abi_version.restype = ctypes.c_int32
 _lib.kvx_abi_version.argtypes = []
 
 EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_destroy", "kvx_pack",
-           "kvx_unpack", "kvx_repack", "kvx_check_block_table", "kvx_last_error",
+           "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged",
+           "kvx_check_block_table", "kvx_check_src_block_table", "kvx_last_error",
            "kvx_abi_version")
 
 
@@ -129,12 +137,14 @@ class Plan:
 
 
 def make_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype, dst_dtype,
-              src_order, block_size, num_blocks, seq_lens):
-    """kvx_desc plus the int32 array its seq_lens points into."""
+              src_order, block_size, num_blocks, seq_lens, src_block_size=0, src_num_blocks=0):
+    """kvx_desc plus the int32 array its seq_lens points into (the last two
+    fields matter only for a PAGED source)."""
     lens = (ctypes.c_int32 * max(len(seq_lens), 1))(*[int(t) for t in seq_lens])
     d = kvx_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype,
                  dst_dtype, src_order, block_size, num_blocks, len(seq_lens),
-                 ctypes.cast(lens, ctypes.POINTER(ctypes.c_int32)))
+                 ctypes.cast(lens, ctypes.POINTER(ctypes.c_int32)), src_block_size,
+                 src_num_blocks)
     d._lens = lens
     return d
 
@@ -184,17 +194,41 @@ def kvx_repack(plan: Plan, src_shards, cache, scales, block_table, bt_stride: in
                            _addr(block_table), bt_stride, _stream(stream)))
 
 
+def kvx_pack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int, wire,
+                   stream=None) -> None:
+    _check(_lib.kvx_pack_paged(plan, _shard_array(src_shards), _addr(src_block_table),
+                               src_bt_stride, _addr(wire), _stream(stream)))
+
+
+def kvx_repack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int, cache, scales,
+                     block_table, bt_stride: int, stream=None) -> None:
+    _check(_lib.kvx_repack_paged(plan, _shard_array(src_shards), _addr(src_block_table),
+                                 src_bt_stride, _addr(cache), _addr(scales), _addr(block_table),
+                                 bt_stride, _stream(stream)))
+
+
+def _host_table(table):
+    """(keep-alive object, address) of a contiguous int32 host table."""
+    if isinstance(table, torch.Tensor):
+        assert table.device.type == "cpu" and table.dtype == torch.int32
+        keep = table.contiguous()
+        return keep, keep.data_ptr()
+    import numpy as np
+    keep = np.ascontiguousarray(table, dtype=np.int32)
+    return keep, keep.ctypes.data
+
+
 def kvx_check_block_table(plan: Plan, host_block_table, bt_stride: int) -> None:
     """host_block_table: a contiguous int32 numpy array or CPU tensor."""
-    if isinstance(host_block_table, torch.Tensor):
-        assert host_block_table.device.type == "cpu" and host_block_table.dtype == torch.int32
-        keep = host_block_table.contiguous()
-        ptr = keep.data_ptr()
-    else:
-        import numpy as np
-        keep = np.ascontiguousarray(host_block_table, dtype=np.int32)
-        ptr = keep.ctypes.data
+    keep, ptr = _host_table(host_block_table)
     _check(_lib.kvx_check_block_table(plan, ptr, bt_stride))
+    del keep
+
+
+def kvx_check_src_block_table(plan: Plan, host_src_block_table, src_bt_stride: int) -> None:
+    """host_src_block_table: a contiguous int32 numpy array or CPU tensor."""
+    keep, ptr = _host_table(host_src_block_table)
+    _check(_lib.kvx_check_src_block_table(plan, ptr, src_bt_stride))
     del keep
 
 

@@ -29,7 +29,7 @@ struct FastDiv {
 // One logical page of one request, device resident: the unit of work of a
 // workgroup in every (layer, k/v) plane.
 struct Item {
-    int64_t src_base;    // element offset of the request in every source shard
+    int64_t src_base;    // element offset of the request in every source shard (0 if paged)
     int64_t wire_data;   // byte offset of the request's data region in the transfer tensor
     int64_t wire_scale;  // byte offset of its scale region, -1 without scales
     int32_t req;         // request index (block-table row)
@@ -86,6 +86,12 @@ struct KArgs {
     int32_t row_dst_bytes;            // head_dim * dst element size
     int32_t cpr;                      // 16-byte destination chunks per row
     int32_t lg_lpr;                   // log2(lanes per row), lanes per row >= cpr
+    // paged sources: the prefill side's pages
+    const int32_t* sbt;               // source block table [requests][sbt_stride]
+    int64_t src_num_blocks;           // pages per plane of each shard's pool
+    int32_t sbt_stride;
+    int32_t src_block_size;
+    FastDiv div_sbs;
 };
 
 // Launch one conversion over a.units work units; returns a hipError_t value.

@@ -20,6 +20,11 @@
 // (i % 8) * units_per_xcd + i / 8, so every XCD streams one contiguous run of
 // units through its own L2 instead of every eighth unit of the whole stream.
 //
+// A paged source (the prefill side's own paged cache, with its own page size
+// and block table) adds one lookup per row: the page of the row's token in
+// the source block table.  Rows of one token are contiguous in a source page,
+// as in a token-major source, so the unit and row order are the same.
+//
 // Destination pages of the paged cache are scattered over a pool of tens to
 // hundreds of GiB, so their first touch often waits for an address
 // translation.  The first workgroup of each page (part 0, segment 0) therefore
@@ -298,15 +303,27 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         } else {
             const int h = seg.h0 + ii;                       // head within the shard
             int64_t e;
-            if constexpr (ORDER == KVX_THD)
+            if constexpr (ORDER == KVX_THD) {
                 e = (int64_t(plane) * T + t0 + s) * a.hs + h;
-            else
+            } else if constexpr (ORDER == KVX_HTD) {
                 e = (int64_t(plane) * a.hs + h) * T + t0 + s;
+            } else {
+                // the prefill side's own page of this token; a row whose page
+                // id lies outside the source pool is neither read nor written
+                const uint32_t t = uint32_t(t0 + s);
+                const uint32_t q = fdiv(t, a.div_sbs);
+                const int32_t sb = a.sbt[int64_t(it.req) * a.sbt_stride + q];
+                ok = sb >= 0 && sb < a.src_num_blocks;
+                e = ((int64_t(plane) * a.src_num_blocks + sb) * a.src_block_size +
+                     int64_t(t - q * uint32_t(a.src_block_size))) * a.hs + h;
+            }
             p = static_cast<const char*>(a.src[seg.slot]) + (it.src_base + e * a.head_dim) * kSrcEsz;
         }
         p += sub * (kLaneElems * kSrcEsz);
+        if (ok) {
 #pragma unroll
-        for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+            for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+        }
     }
 
     char* dbase;
@@ -397,11 +414,14 @@ int launch(int mode, int conv, int order, const KArgs& a, void* stream)
         if (conv == kCopy8) return go<kUnpack, kCopy8, KVX_THD>(a, stream);
         return int(hipErrorInvalidValue);
     }
-    if (mode == kPack)
-        return order == KVX_THD ? go_conv<kPack, KVX_THD>(conv, a, stream)
-                                : go_conv<kPack, KVX_HTD>(conv, a, stream);
-    return order == KVX_THD ? go_conv<kRepack, KVX_THD>(conv, a, stream)
-                            : go_conv<kRepack, KVX_HTD>(conv, a, stream);
+    if (mode == kPack) {
+        if (order == KVX_THD) return go_conv<kPack, KVX_THD>(conv, a, stream);
+        if (order == KVX_HTD) return go_conv<kPack, KVX_HTD>(conv, a, stream);
+        return go_conv<kPack, KVX_PAGED>(conv, a, stream);
+    }
+    if (order == KVX_THD) return go_conv<kRepack, KVX_THD>(conv, a, stream);
+    if (order == KVX_HTD) return go_conv<kRepack, KVX_HTD>(conv, a, stream);
+    return go_conv<kRepack, KVX_PAGED>(conv, a, stream);
 }
 
 }  // namespace kvx

@@ -26,6 +26,7 @@ struct kvx_plan_s {
     int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
     std::vector<kvx::Segment> segs;  // head runs of the decode rank, one per shard read
     int32_t max_blocks = 0;
+    int32_t max_src_blocks = 0;   // paged sources: pages per request on the prefill side
     uint64_t wire_bytes = 0;
     int64_t total_tokens = 0;
     int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
@@ -84,8 +85,10 @@ kvx_status validate(const kvx_desc* d)
     if (d->num_requests > 0 && !d->seq_lens) return fail(KVX_EINVAL, "seq_lens is NULL");
     for (int r = 0; r < d->num_requests; ++r)
         if (d->seq_lens[r] < 0) return fail(KVX_EINVAL, "seq_lens[%d] < 0", r);
-    if (d->src_order != KVX_THD && d->src_order != KVX_HTD)
+    if (d->src_order != KVX_THD && d->src_order != KVX_HTD && d->src_order != KVX_PAGED)
         return fail(KVX_EINVAL, "unknown src_order %d", d->src_order);
+    if (d->src_order == KVX_PAGED && (d->src_block_size <= 0 || d->src_num_blocks <= 0))
+        return fail(KVX_EINVAL, "a paged source needs src_block_size >= 1 and src_num_blocks >= 1");
     if (d->src_dtype != KVX_FP16 && d->src_dtype != KVX_BF16 && d->src_dtype != KVX_FP8_E4M3FN)
         return fail(KVX_EINVAL, "unknown src_dtype %d", d->src_dtype);
     if (d->dst_dtype != KVX_FP16 && d->dst_dtype != KVX_BF16 && d->dst_dtype != KVX_FP8_E4M3FN)
@@ -157,6 +160,7 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
 
     // requests: source offsets, transfer-tensor segments, work items
     const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
+    const bool paged = d.src_order == KVX_PAGED;
     const int64_t L2 = int64_t(d.num_layers) * 2;
     int64_t src_off = 0, wire = 0, nitems = 0;
     p->wire_data.resize(d.num_requests);
@@ -165,8 +169,11 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     for (int r = 0; r < d.num_requests; ++r) {
         const int64_t T = p->lens[r];
         const int64_t rows = L2 * T * p->hd;
-        src_base[r] = src_off;
+        src_base[r] = paged ? 0 : src_off;  // a paged source is addressed through its pages
         src_off += L2 * T * p->hs * d.head_dim;
+        if (paged)
+            p->max_src_blocks = int32_t(std::max<int64_t>(
+                p->max_src_blocks, (T + d.src_block_size - 1) / d.src_block_size));
         wire = align256(wire);
         p->wire_data[r] = wire;
         wire += rows * d.head_dim * p->esz_dst;
@@ -246,6 +253,7 @@ kvx_status kvx_plan_info_get(const kvx_plan_t* p, kvx_plan_info* info)
     info->max_blocks_per_request = p->max_blocks;
     info->num_items = int32_t(p->items.size());
     info->device = p->device;
+    info->max_src_blocks_per_request = p->max_src_blocks;
     return KVX_OK;
 }
 
@@ -292,11 +300,28 @@ kvx_status kvx_check_block_table(const kvx_plan_t* p, const int32_t* bt, int32_t
     return KVX_OK;
 }
 
+kvx_status kvx_check_src_block_table(const kvx_plan_t* p, const int32_t* sbt, int32_t sbt_stride)
+{
+    if (!p) return fail(KVX_EINVAL, "NULL plan");
+    if (p->d.src_order != KVX_PAGED) return fail(KVX_EINVAL, "the plan's source is not paged");
+    if (p->items.empty()) return KVX_OK;
+    if (!sbt) return fail(KVX_EINVAL, "NULL source block table");
+    if (sbt_stride < p->max_src_blocks)
+        return fail(KVX_EINVAL, "src_bt_stride %d < max_src_blocks_per_request %d", sbt_stride,
+                    p->max_src_blocks);
+    for (int r = 0; r < p->d.num_requests; ++r) {
+        const int nb = (p->lens[r] + p->d.src_block_size - 1) / p->d.src_block_size;
+        for (int k = 0; k < nb; ++k) {
+            const int32_t b = sbt[int64_t(r) * sbt_stride + k];
+            if (b < 0 || b >= p->d.src_num_blocks)
+                return fail(KVX_EINVAL, "src_block_table[%d][%d] = %d outside [0, %lld)", r, k, b,
+                            (long long)p->d.src_num_blocks);
+        }
+    }
+    return KVX_OK;
+}
+
 }  // extern "C"
-
-namespace {
-
-}  // namespace
 
 kvx::FastDiv kvx::make_fastdiv(uint32_t d)
 {
@@ -315,13 +340,26 @@ int conv_for(const kvx_plan_t* p, int mode)
 }
 
 // Shared argument checks of the launch calls; fills the kernel arguments.
-kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, const void* wire,
-                   void* dst, float* scales, const int32_t* bt, int32_t bt_stride, kvx::KArgs& a)
+// `paged_call` tells whether the entry point is a _paged one; it must match
+// the plan's source order (the unpack reads no source and takes either).
+kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* const* shards,
+                   const int32_t* sbt, int32_t sbt_stride, const void* wire, void* dst,
+                   float* scales, const int32_t* bt, int32_t bt_stride, kvx::KArgs& a)
 {
     if (!p) return fail(KVX_EINVAL, "NULL plan");
     const bool fp8 = p->d.dst_dtype == KVX_FP8_E4M3FN;
+    const bool paged = p->d.src_order == KVX_PAGED;
     std::memset(&a, 0, sizeof a);
+    if (mode != kvx::kUnpack && paged != paged_call)
+        return fail(KVX_EINVAL, paged ? "the plan's source is paged: use kvx_pack_paged / kvx_repack_paged"
+                                      : "the plan's source is not paged: use kvx_pack / kvx_repack");
     if (p->items.empty()) return KVX_OK;  // nothing to read or write: pointers are not used
+    if (mode != kvx::kUnpack && paged) {
+        if (!sbt) return fail(KVX_EINVAL, "NULL source block table");
+        if (sbt_stride < p->max_src_blocks)
+            return fail(KVX_EINVAL, "src_bt_stride %d < max_src_blocks_per_request %d", sbt_stride,
+                        p->max_src_blocks);
+    }
     if (mode != kvx::kUnpack) {
         if (!shards) return fail(KVX_EINVAL, "NULL src_shards array");
         for (int k = 0; k < p->num_read_shards; ++k) {
@@ -387,6 +425,13 @@ kvx_status prepare(const kvx_plan_t* p, int mode, const void* const* shards, con
     a.row_dst_bytes = d.head_dim * p->esz_dst;
     a.cpr = p->cpr;
     a.lg_lpr = p->lg_lpr;
+    if (mode != kvx::kUnpack && paged) {
+        a.sbt = sbt;
+        a.sbt_stride = sbt_stride;
+        a.src_block_size = d.src_block_size;
+        a.src_num_blocks = d.src_num_blocks;
+        a.div_sbs = kvx::make_fastdiv(uint32_t(d.src_block_size));
+    }
     return KVX_OK;
 }
 
@@ -406,7 +451,8 @@ extern "C" {
 kvx_status kvx_pack(const kvx_plan_t* p, const void* const* shards, void* wire, void* stream)
 {
     kvx::KArgs a;
-    kvx_status st = prepare(p, kvx::kPack, shards, nullptr, wire, nullptr, nullptr, 0, a);
+    kvx_status st = prepare(p, kvx::kPack, false, shards, nullptr, 0, nullptr, wire, nullptr,
+                            nullptr, 0, a);
     return st != KVX_OK ? st : run(p, kvx::kPack, a, stream);
 }
 
@@ -414,7 +460,8 @@ kvx_status kvx_unpack(const kvx_plan_t* p, const void* wire, void* cache, float*
                       const int32_t* bt, int32_t bt_stride, void* stream)
 {
     kvx::KArgs a;
-    kvx_status st = prepare(p, kvx::kUnpack, nullptr, wire, cache, scales, bt, bt_stride, a);
+    kvx_status st = prepare(p, kvx::kUnpack, false, nullptr, nullptr, 0, wire, cache, scales, bt,
+                            bt_stride, a);
     return st != KVX_OK ? st : run(p, kvx::kUnpack, a, stream);
 }
 
@@ -422,7 +469,27 @@ kvx_status kvx_repack(const kvx_plan_t* p, const void* const* shards, void* cach
                       const int32_t* bt, int32_t bt_stride, void* stream)
 {
     kvx::KArgs a;
-    kvx_status st = prepare(p, kvx::kRepack, shards, nullptr, cache, scales, bt, bt_stride, a);
+    kvx_status st = prepare(p, kvx::kRepack, false, shards, nullptr, 0, nullptr, cache, scales,
+                            bt, bt_stride, a);
+    return st != KVX_OK ? st : run(p, kvx::kRepack, a, stream);
+}
+
+kvx_status kvx_pack_paged(const kvx_plan_t* p, const void* const* shards, const int32_t* sbt,
+                          int32_t sbt_stride, void* wire, void* stream)
+{
+    kvx::KArgs a;
+    kvx_status st = prepare(p, kvx::kPack, true, shards, sbt, sbt_stride, nullptr, wire, nullptr,
+                            nullptr, 0, a);
+    return st != KVX_OK ? st : run(p, kvx::kPack, a, stream);
+}
+
+kvx_status kvx_repack_paged(const kvx_plan_t* p, const void* const* shards, const int32_t* sbt,
+                            int32_t sbt_stride, void* cache, float* scales, const int32_t* bt,
+                            int32_t bt_stride, void* stream)
+{
+    kvx::KArgs a;
+    kvx_status st = prepare(p, kvx::kRepack, true, shards, sbt, sbt_stride, nullptr, cache, scales,
+                            bt, bt_stride, a);
     return st != KVX_OK ? st : run(p, kvx::kRepack, a, stream);
 }
 

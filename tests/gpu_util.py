@@ -20,10 +20,13 @@ def log(msg: str) -> None:
     print(msg, flush=True)
 
 
+_ORDER = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}
+
+
 def desc_for(w, lens, layers=None):
     return K.make_desc(layers or w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
-                       _F[w.src_dtype], _F[w.dst_dtype], K.THD if w.src_order == "thd" else K.HTD,
-                       w.block_size, w.num_blocks, list(lens))
+                       _F[w.src_dtype], _F[w.dst_dtype], _ORDER[w.src_order], w.block_size,
+                       w.num_blocks, list(lens), w.src_block_size, w.src_num_blocks)
 
 
 def dev_u16(a):
@@ -40,38 +43,58 @@ def pool(w, layers, fill=W.SENTINEL):
     return cache, scales
 
 
-def check_shapes(w, lens, bt, stride, dshards, layers):
+def check_shapes(w, lens, bt, stride, dshards, layers, sbt=None):
     """Host-side check that every buffer the kernels will touch has the size
     the plan assumes (run before each launch)."""
     Hs, D = w.hs, w.head_dim
-    need = sum(layers * 2 * int(t) * Hs * D for t in lens)
+    if w.src_order == "paged":
+        need = layers * 2 * w.src_num_blocks * w.src_block_size * Hs * D
+        snb = max([(int(t) + w.src_block_size - 1) // w.src_block_size for t in lens] + [0])
+        assert len(lens) == 0 or (sbt.shape[0] == len(lens) and sbt.shape[1] >= snb)
+    else:
+        need = sum(layers * 2 * int(t) * Hs * D for t in lens)
     for j in w.read_shards():
         assert dshards[j] is not None and dshards[j].numel() >= need, (j, need)
     assert len(lens) == 0 or (bt.shape[0] == len(lens) and bt.shape[1] >= stride)
-    # page ids outside [0, num_blocks) are allowed: the kernel skips them
+    # page ids outside [0, num_blocks) or [0, src_num_blocks) are allowed:
+    # the kernel skips them
 
 
-def gpu_run(op, w, lens, bt, stride, shards, layers=None, wire_in=None):
+def gpu_run(op, w, lens, bt, stride, shards, layers=None, wire_in=None, sbt=None):
     """Run 'repack', 'pack', 'pack_unpack' or 'unpack' (of wire_in) on the GPU.
-    Returns (cache, scales, wire) device tensors (None where not produced)."""
+    A paged source uses the generator's source block table unless `sbt` is
+    given.  Returns (cache, scales, wire) device tensors (None where not
+    produced)."""
     layers = layers or w.layers
     plan = K.kvx_plan(desc_for(w, lens, layers))
     info = K.kvx_plan_info_get(plan)
     dshards = [dev_u16(s) for s in shards] if shards is not None else None
     bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    paged = w.src_order == "paged"
+    sbt_d = None
+    if paged:
+        if sbt is None:
+            sbt, _ = W.src_block_table(w, lens)
+        sbt = np.ascontiguousarray(sbt, dtype=np.int32)
+        sbt_d = torch.from_numpy(sbt).to(DEV)
     if dshards is not None:
-        check_shapes(w, lens, bt, stride, dshards, layers)
+        check_shapes(w, lens, bt, stride, dshards, layers, sbt)
     cache = scales = wire = None
     if op in ("pack", "pack_unpack"):
         wire = torch.full((max(int(info.wire_bytes), 16),), W.SENTINEL, dtype=torch.uint8,
                           device=DEV)
-        K.kvx_pack(plan, dshards, wire)
+        if paged:
+            K.kvx_pack_paged(plan, dshards, sbt_d, sbt.shape[1], wire)
+        else:
+            K.kvx_pack(plan, dshards, wire)
     if op == "unpack":
         wire = torch.from_numpy(wire_in).to(DEV)
         assert wire.numel() >= info.wire_bytes
     if op in ("repack", "pack_unpack", "unpack"):
         cache, scales = pool(w, layers)
-        if op == "repack":
+        if op == "repack" and paged:
+            K.kvx_repack_paged(plan, dshards, sbt_d, sbt.shape[1], cache, scales, bt_d, stride)
+        elif op == "repack":
             K.kvx_repack(plan, dshards, cache, scales, bt_d, stride)
         else:
             K.kvx_unpack(plan, wire, cache, scales, bt_d, stride)
@@ -79,9 +102,9 @@ def gpu_run(op, w, lens, bt, stride, shards, layers=None, wire_in=None):
     return cache, scales, wire
 
 
-def oracle_pool(w, lens, bt, stride, shards, layers=None, op="repack", wire=None):
+def oracle_pool(w, lens, bt, stride, shards, layers=None, op="repack", wire=None, sbt=None):
     layers = layers or w.layers
-    p = oracle_problem(O, w, lens, layers)
+    p = oracle_problem(O, w, lens, layers, sbt=sbt)
     cache = np.full(O.cache_bytes(p), W.SENTINEL, dtype=np.uint8)
     scales = None
     if w.dst_dtype == "e4m3fn":

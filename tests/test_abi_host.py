@@ -8,7 +8,7 @@ import re
 import numpy as np
 import pytest
 
-from cases import SMALL, FULL, oracle_problem
+from cases import SMALL, SMALL_PAGED, FULL, oracle_problem
 from conftest import ROOT
 
 import oracle as O
@@ -26,26 +26,28 @@ def declared_entry_points():
 
 def test_every_declared_symbol_is_exported():
     names = declared_entry_points()
-    assert len(names) == 10, names
+    assert len(names) == 13, names
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 1
+    assert K.kvx_abi_version() == 2
 
 
 def desc_for(w, lens, **over):
     f = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
     kw = dict(num_layers=w.layers, num_kv_heads=w.heads, head_dim=w.head_dim, src_tp=w.src_tp,
               dst_tp=w.dst_tp, dst_rank=w.dst_rank, src_dtype=f[w.src_dtype],
-              dst_dtype=f[w.dst_dtype], src_order=K.THD if w.src_order == "thd" else K.HTD,
-              block_size=w.block_size, num_blocks=w.num_blocks, seq_lens=list(lens))
+              dst_dtype=f[w.dst_dtype],
+              src_order={"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order],
+              block_size=w.block_size, num_blocks=w.num_blocks, seq_lens=list(lens),
+              src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks)
     kw.update(over)
     return K.make_desc(**kw)
 
 
-@pytest.mark.parametrize("name", list(SMALL) + list(FULL))
+@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_PAGED) + list(FULL))
 def test_plan_bytes_and_segments(name):
-    w = (SMALL | FULL)[name]
+    w = (SMALL | SMALL_PAGED | FULL)[name]
     lens = W.seq_lens(w)
     plan = K.kvx_plan(desc_for(w, lens))
     info = K.kvx_plan_info_get(plan)
@@ -60,6 +62,11 @@ def test_plan_bytes_and_segments(name):
     assert info.max_blocks_per_request == max(nb + [0])
     assert info.num_items == sum(nb)
     assert info.total_tokens == int(lens.sum())
+    if w.src_order == "paged":
+        snb = [(int(t) + w.src_block_size - 1) // w.src_block_size for t in lens]
+        assert info.max_src_blocks_per_request == max(snb + [0])
+    else:
+        assert info.max_src_blocks_per_request == 0
     # transfer-tensor segments agree with the oracle's layout
     doff, soff, total = O.wire_layout(oracle_problem(O, w, lens))
     assert info.wire_bytes == total
@@ -75,7 +82,10 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(num_layers=0), K.EINVAL), (dict(num_kv_heads=0), K.EINVAL), (dict(head_dim=-64), K.EINVAL),
     (dict(src_tp=3), K.EINVAL), (dict(dst_tp=3), K.EINVAL), (dict(dst_rank=2), K.EINVAL),
     (dict(dst_rank=-1), K.EINVAL), (dict(block_size=0), K.EINVAL), (dict(num_blocks=0), K.EINVAL),
-    (dict(seq_lens=[4, -1]), K.EINVAL), (dict(src_order=2), K.EINVAL),
+    (dict(seq_lens=[4, -1]), K.EINVAL), (dict(src_order=3), K.EINVAL),
+    (dict(src_order=2), K.EINVAL),                      # paged without a page size
+    (dict(src_order=2, src_block_size=16), K.EINVAL),   # paged without a pool
+    (dict(src_order=2, src_block_size=0, src_num_blocks=8), K.EINVAL),
     (dict(head_dim=4), K.EINVAL),                       # 8-byte rows
     (dict(head_dim=8, dst_dtype=3), K.EINVAL),          # 8-byte e4m3 rows
     (dict(src_dtype=3), K.EUNSUPPORTED), (dict(src_dtype=2, dst_dtype=1), K.EUNSUPPORTED),
@@ -102,6 +112,11 @@ def test_plan_accepts_empty_batches():
         K.kvx_repack(plan, [None], None, None, None, 0)
         K.kvx_pack(plan, [None], None)
         K.kvx_unpack(plan, None, None, None, None, 0)
+        paged = K.kvx_plan(K.make_desc(**dict(kw, src_order=K.PAGED, src_block_size=16,
+                                              src_num_blocks=4)))
+        K.kvx_repack_paged(paged, [None], None, 0, None, None, None, 0)
+        K.kvx_pack_paged(paged, [None], None, 0, None)
+        K.kvx_unpack(paged, None, None, None, None, 0)
 
 
 def test_segment_out_of_range():
@@ -167,3 +182,55 @@ def test_workload_block_tables_are_valid():
         lens = W.seq_lens(w)
         bt, stride = W.block_table(w, lens)
         K.kvx_check_block_table(K.kvx_plan(desc_for(w, lens)), bt, stride)
+
+
+PAGED = dict(BASE, src_order=2, src_block_size=24, src_num_blocks=32)   # 40 and 7 tokens: 2 + 1 source pages
+
+
+def test_paged_entry_points_match_the_plan():
+    """A paged plan is served by the _paged calls only, a contiguous-source
+    plan by the others; the source block table and its stride are checked."""
+    g = 0x10000
+    plain = K.kvx_plan(K.make_desc(**BASE))
+    paged = K.kvx_plan(K.make_desc(**PAGED))
+    assert K.kvx_plan_info_get(paged).max_src_blocks_per_request == 2
+    cases = [
+        (lambda: K.kvx_repack(paged, [g], g, None, g, 3), "kvx_repack_paged"),
+        (lambda: K.kvx_pack(paged, [g], g), "kvx_pack_paged"),
+        (lambda: K.kvx_repack_paged(plain, [g], g, 2, g, None, g, 3), "not paged"),
+        (lambda: K.kvx_pack_paged(plain, [g], g, 2, g), "not paged"),
+        (lambda: K.kvx_repack_paged(paged, [g], None, 2, g, None, g, 3), "NULL source block table"),
+        (lambda: K.kvx_repack_paged(paged, [g], g, 1, g, None, g, 3), "src_bt_stride"),
+        (lambda: K.kvx_pack_paged(paged, [g], g, 1, g), "src_bt_stride"),
+        (lambda: K.kvx_repack_paged(paged, [None], g, 2, g, None, g, 3), "src_shards["),
+        (lambda: K.kvx_repack_paged(paged, [g], g, 2, g, None, g, 2), "bt_stride"),
+    ]
+    for call, msg in cases:
+        with pytest.raises(K.KvxError) as e:
+            call()
+        assert e.value.status == K.EINVAL and msg in K.kvx_last_error(), K.kvx_last_error()
+
+
+def test_check_src_block_table():
+    paged = K.kvx_plan(K.make_desc(**PAGED))
+    ok = np.array([[5, 31], [5, -1]], dtype=np.int32)        # a shared page is allowed
+    K.kvx_check_src_block_table(paged, ok, 2)
+    for bad in ([[5, 32], [0, -1]], [[-1, 3], [0, 0]], [[1, 2], [40, 0]]):
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_check_src_block_table(paged, np.array(bad, dtype=np.int32), 2)
+        assert e.value.status == K.EINVAL
+    with pytest.raises(K.KvxError):
+        K.kvx_check_src_block_table(paged, ok, 1)
+    with pytest.raises(K.KvxError):
+        K.kvx_check_src_block_table(K.kvx_plan(K.make_desc(**BASE)), ok, 2)
+
+
+def test_workload_source_block_tables_are_valid():
+    for w in list(SMALL_PAGED.values()) + [FULL["llama3_8b_paged16_bf16_bs64"],
+                                           FULL["llama3_70b_paged16_tp4to2_bf16_bs32"]]:
+        lens = W.seq_lens(w)
+        sbt, sstride = W.src_block_table(w, lens)
+        bt, stride = W.block_table(w, lens)
+        plan = K.kvx_plan(desc_for(w, lens))
+        K.kvx_check_src_block_table(plan, sbt, sstride)
+        K.kvx_check_block_table(plan, bt, stride)
