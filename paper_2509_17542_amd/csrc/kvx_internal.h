@@ -92,6 +92,8 @@ struct KArgs {
     int32_t sbt_stride;
     int32_t src_block_size;
     FastDiv div_sbs;
+    int32_t sbt_uniform;              // every part lies in one source page
+    int32_t pad_;
 };
 
 // Launch one conversion over a.units work units; returns a hipError_t value.

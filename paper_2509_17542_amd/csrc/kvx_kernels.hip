@@ -252,6 +252,15 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     constexpr int kVecs = kFp8 ? 2 : 1;                       // 16-byte loads per lane
     constexpr int kSrcEsz = CONV == kCopy8 ? 1 : 2;
     constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;
+    // Issue order.  "Early": the page lookups are scalar loads issued before
+    // any lane-dependent branch and every lane issues its row load
+    // unconditionally (lanes without a row read the buffer's first vector), so
+    // the lookups, the row loads and the paged source's page lookup overlap
+    // instead of following one another.  Measured faster for paged sources
+    // (+11%) and 16-bit token-major rows (+2%); the head-major and e4m3fn
+    // paths measure 2-4% faster with the row load inside the branch.
+    constexpr bool kEarly =
+        ORDER == KVX_PAGED || (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16));
 
     // XCD-contiguous unit of this workgroup -> (plane, page, segment, part)
     const uint32_t unit = (blockIdx.x % kXcds) * a.units_per_xcd + blockIdx.x / kXcds;
@@ -269,8 +278,24 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     const int t0 = it.blk * a.block_size;
     const int seg_rows = min(a.block_size, T - t0) * seg.n;
     const int64_t row0 = (int64_t(plane) * T + t0) * a.hd;  // first row in transfer-tensor order
-
     const int lg = a.lg_lpr;
+
+    int32_t b = 0;  // destination page (unpack, repack)
+    if constexpr (kEarly && MODE != kPack) b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
+    // Paged source whose parts never span two source pages: one page per
+    // workgroup, looked up once (the part's first token must exist).
+    int32_t sb_u = -1;
+    uint32_t q_u = 0;
+    if constexpr (ORDER == KVX_PAGED && MODE != kUnpack) {
+        if (a.sbt_uniform) {
+            const uint32_t tf = uint32_t(t0) + fdiv(part * uint32_t(kThreads >> lg), seg.div_n);
+            if (tf < uint32_t(T)) {
+                q_u = fdiv(tf, a.div_sbs);
+                sb_u = a.sbt[int64_t(it.req) * a.sbt_stride + q_u];
+            }
+        }
+    }
+
     const int sub = threadIdx.x & ((1 << lg) - 1);          // 16-byte chunk within the row
     const int r = int(part) * (kThreads >> lg) + (threadIdx.x >> lg);  // row within the segment
     int s, ii;  // token within the page, head within the segment
@@ -288,42 +313,66 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     }
     const int row = s * a.hd + seg.i0 + ii;                 // row within the page
 
-    uint4 v[kVecs];
-#pragma unroll
-    for (int k = 0; k < kVecs; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
-    float sc = 0.0f;
-    if (ok) {
-        const char* p;
-        if constexpr (MODE == kUnpack) {
-            p = static_cast<const char*>(a.wire_in) + it.wire_data + (row0 + row) * a.row_dst_bytes;
-            if constexpr (kScales)
-                if (sub == 0)
-                    sc = reinterpret_cast<const float*>(static_cast<const char*>(a.wire_in) +
-                                                        it.wire_scale)[row0 + row];
+    // source address of this lane's row (meaningful where ok)
+    const char* base;
+    const char* p = nullptr;
+    const float* sp = nullptr;
+    if constexpr (MODE == kUnpack) {
+        base = static_cast<const char*>(a.wire_in);
+        p = base + it.wire_data + (row0 + row) * a.row_dst_bytes + sub * 16;
+        if constexpr (kScales)
+            sp = reinterpret_cast<const float*>(base + it.wire_scale) + row0 + row;
+    } else {
+        base = static_cast<const char*>(a.src[seg.slot]);
+        const int h = seg.h0 + ii;                           // head within the shard
+        int64_t e = 0;
+        if constexpr (ORDER == KVX_THD) {
+            e = (int64_t(plane) * T + t0 + s) * a.hs + h;
+        } else if constexpr (ORDER == KVX_HTD) {
+            e = (int64_t(plane) * a.hs + h) * T + t0 + s;
         } else {
-            const int h = seg.h0 + ii;                       // head within the shard
-            int64_t e;
-            if constexpr (ORDER == KVX_THD) {
-                e = (int64_t(plane) * T + t0 + s) * a.hs + h;
-            } else if constexpr (ORDER == KVX_HTD) {
-                e = (int64_t(plane) * a.hs + h) * T + t0 + s;
-            } else {
-                // the prefill side's own page of this token; a row whose page
-                // id lies outside the source pool is neither read nor written
-                const uint32_t t = uint32_t(t0 + s);
-                const uint32_t q = fdiv(t, a.div_sbs);
-                const int32_t sb = a.sbt[int64_t(it.req) * a.sbt_stride + q];
-                ok = sb >= 0 && sb < a.src_num_blocks;
-                e = ((int64_t(plane) * a.src_num_blocks + sb) * a.src_block_size +
-                     int64_t(t - q * uint32_t(a.src_block_size))) * a.hs + h;
+            // the prefill side's own page of this token; a row whose page id
+            // lies outside the source pool is neither read nor written
+            const uint32_t t = uint32_t(t0 + s);
+            int32_t sb = sb_u;
+            uint32_t q = q_u;
+            if (!a.sbt_uniform && ok) {
+                q = fdiv(t, a.div_sbs);
+                sb = a.sbt[int64_t(it.req) * a.sbt_stride + q];
             }
-            p = static_cast<const char*>(a.src[seg.slot]) + (it.src_base + e * a.head_dim) * kSrcEsz;
+            ok = ok && sb >= 0 && sb < a.src_num_blocks;
+            e = ((int64_t(plane) * a.src_num_blocks + sb) * a.src_block_size +
+                 int64_t(t - q * uint32_t(a.src_block_size))) * a.hs + h;
         }
-        p += sub * (kLaneElems * kSrcEsz);
+        p = base + (it.src_base + e * a.head_dim) * kSrcEsz + sub * (kLaneElems * kSrcEsz);
+    }
+
+    uint4 v[kVecs];
+    float sc = 0.0f;
+    if constexpr (kEarly) {
+        // lanes without a row read the buffer's first vector (valid, cached)
+        const char* pl = ok ? p : base;
+#pragma unroll
+        for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(pl)[k];
+        if constexpr (MODE == kUnpack && kScales)
+            sc = *(ok ? sp : reinterpret_cast<const float*>(base));
+        // keep the loads here: the compiler would otherwise sink them below
+        // the destination-page check, behind the scalar lookups
+        __asm__ volatile("" ::: "memory");
+        if constexpr (kFp8)
+#pragma unroll
+            for (int k = 0; k < kVecs; ++k)  // rows without data take part in the maximum as zeros
+                if (!ok) v[k] = make_uint4(0u, 0u, 0u, 0u);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kVecs; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
         if (ok) {
 #pragma unroll
             for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+            if constexpr (MODE == kUnpack && kScales)
+                if (sub == 0) sc = *sp;
         }
+        if constexpr (MODE != kPack) b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
     }
 
     char* dbase;
@@ -333,7 +382,6 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         if constexpr (kScales)
             sbase = reinterpret_cast<float*>(static_cast<char*>(a.dst) + it.wire_scale) + row0;
     } else {
-        const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
         if (part == 0 && sg == 0 && threadIdx.x == 0) warm_translation(a, unit);
         if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
         const int64_t page_rows = int64_t(b) * a.block_size * a.hd;

@@ -431,6 +431,16 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
         a.src_block_size = d.src_block_size;
         a.src_num_blocks = d.src_num_blocks;
         a.div_sbs = kvx::make_fastdiv(uint32_t(d.src_block_size));
+        // A part of a segment of n heads covers rows [part*rpp, (part+1)*rpp),
+        // i.e. tokens from part*rpp/n on.  When n divides rpp, a part holds
+        // rpp/n whole tokens starting at a multiple of rpp/n; when rpp/n also
+        // divides both page sizes, those tokens never straddle a source page.
+        const int rpp = kvx::kThreads >> p->lg_lpr;
+        bool uniform = true;
+        for (const kvx::Segment& g : p->segs)
+            if (rpp % g.n || d.src_block_size % (rpp / g.n) || d.block_size % (rpp / g.n))
+                uniform = false;
+        a.sbt_uniform = uniform;
     }
     return KVX_OK;
 }
