@@ -92,6 +92,8 @@ class Problem(ctypes.Structure):
         ("num_requests", ctypes.c_int32), ("seq_lens", ctypes.POINTER(ctypes.c_int32)),
         ("src_block_size", ctypes.c_int32), ("src_num_blocks", ctypes.c_int64),
         ("src_block_table", ctypes.POINTER(ctypes.c_int32)), ("src_bt_stride", ctypes.c_int32),
+        ("src_layer_offset", ctypes.c_int32), ("src_layers", ctypes.c_int32),
+        ("dst_layer_offset", ctypes.c_int32), ("dst_layers", ctypes.c_int32),
     ]
 
 
@@ -101,7 +103,8 @@ class OracleProblem:
 
     def __init__(self, layers, heads, head_dim, src_tp, dst_tp, dst_rank, src_fmt, dst_fmt,
                  src_order, block_size, num_blocks, seq_lens, src_block_size=0,
-                 src_num_blocks=0, src_block_table=None, src_bt_stride=0):
+                 src_num_blocks=0, src_block_table=None, src_bt_stride=0, src_layer_offset=0,
+                 src_layers=0, dst_layer_offset=0, dst_layers=0):
         self.seq_lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32))
         self.src_block_table = None
         sbt = ctypes.POINTER(ctypes.c_int32)()
@@ -111,7 +114,8 @@ class OracleProblem:
         self.c = Problem(layers, heads, head_dim, src_tp, dst_tp, dst_rank, src_fmt, dst_fmt,
                          src_order, block_size, num_blocks, len(self.seq_lens),
                          self.seq_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                         src_block_size, src_num_blocks, sbt, src_bt_stride)
+                         src_block_size, src_num_blocks, sbt, src_bt_stride, src_layer_offset,
+                         src_layers, dst_layer_offset, dst_layers)
 
     def __getattr__(self, name):
         return getattr(self.__dict__["c"], name)
@@ -123,6 +127,10 @@ class OracleProblem:
     @property
     def hd(self):
         return self.c.heads // self.c.dst_tp
+
+    @property
+    def dst_layers_held(self):
+        return self.c.dst_layers or self.c.layers
 
     @property
     def dst_size(self):
@@ -214,11 +222,11 @@ def wire_layout(p: OracleProblem):
 
 
 def cache_bytes(p: OracleProblem) -> int:
-    return p.layers * 2 * p.num_blocks * p.block_size * p.hd * p.head_dim * p.dst_size
+    return p.dst_layers_held * 2 * p.num_blocks * p.block_size * p.hd * p.head_dim * p.dst_size
 
 
 def scale_count(p: OracleProblem) -> int:
-    return p.layers * 2 * p.num_blocks * p.block_size * p.hd
+    return p.dst_layers_held * 2 * p.num_blocks * p.block_size * p.hd
 
 
 # ---- the operations ------------------------------------------------------------

@@ -222,10 +222,19 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
 /* index maps                                                          */
 /* ------------------------------------------------------------------ */
 
+int32_t orc_src_layers(const orc_problem *p) { return p->src_layers ? p->src_layers : p->layers; }
+int32_t orc_dst_layers(const orc_problem *p) { return p->dst_layers ? p->dst_layers : p->layers; }
+
 int orc_validate(const orc_problem *p)
 {
     if (!p) return -1;
     if (p->layers <= 0 || p->heads <= 0 || p->head_dim <= 0) return -1;
+    /* the converted layers must lie inside both sides' layer ranges */
+    if (p->src_layers < 0 || p->dst_layers < 0 || p->src_layer_offset < 0 ||
+        p->dst_layer_offset < 0)
+        return -1;
+    if ((int64_t)p->src_layer_offset + p->layers > orc_src_layers(p)) return -1;
+    if ((int64_t)p->dst_layer_offset + p->layers > orc_dst_layers(p)) return -1;
     if (p->src_tp <= 0 || p->dst_tp <= 0) return -1;
     if (p->heads % p->src_tp != 0 || p->heads % p->dst_tp != 0) return -1;
     if (p->dst_rank < 0 || p->dst_rank >= p->dst_tp) return -1;
@@ -270,7 +279,7 @@ int64_t orc_src_request_base(const orc_problem *p, int r)
     int64_t base = 0;
     if (p->src_order == ORC_PAGED) return 0; /* pages, not back-to-back requests */
     for (int q = 0; q < r; ++q)
-        base += (int64_t)p->layers * 2 * p->seq_lens[q] * Hs * p->head_dim;
+        base += (int64_t)orc_src_layers(p) * 2 * p->seq_lens[q] * Hs * p->head_dim;
     return base;
 }
 
@@ -285,7 +294,7 @@ static int64_t src_index_from(const orc_problem *p, int64_t base, int r, int l, 
     int64_t Hs = p->heads / p->src_tp;
     int64_t T = p->seq_lens[r];
     int64_t D = p->head_dim;
-    int64_t plane = (int64_t)l * 2 + kv;
+    int64_t plane = ((int64_t)p->src_layer_offset + l) * 2 + kv; /* in the source's layers */
     if (p->src_order == ORC_PAGED) {
         /* the prefill side's paged cache: token t sits in page
          * src_block_table[r][t / src_block_size], slot t % src_block_size */
@@ -308,7 +317,7 @@ int64_t orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, 
 int64_t orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d)
 {
     int64_t Hd = p->heads / p->dst_tp;
-    int64_t plane = (int64_t)l * 2 + kv;
+    int64_t plane = ((int64_t)p->dst_layer_offset + l) * 2 + kv; /* in the cache's layers */
     return (((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i) * p->head_dim + d;
 }
 
@@ -316,7 +325,7 @@ int64_t orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int 
 int64_t orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i)
 {
     int64_t Hd = p->heads / p->dst_tp;
-    int64_t plane = (int64_t)l * 2 + kv;
+    int64_t plane = ((int64_t)p->dst_layer_offset + l) * 2 + kv;
     return ((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i;
 }
 

@@ -54,6 +54,12 @@ typedef struct {
     int64_t src_num_blocks;
     const int32_t *src_block_table; /* [num_requests][src_bt_stride] */
     int32_t src_bt_stride;
+    /* Pipeline stages (layer ranges): the source buffers hold src_layers
+     * layers and converted layer l is their layer src_layer_offset + l; the
+     * cache holds dst_layers layers and layer l goes to its layer
+     * dst_layer_offset + l.  0 layers means `layers` (offsets then 0). */
+    int32_t src_layer_offset, src_layers;
+    int32_t dst_layer_offset, dst_layers;
 } orc_problem;
 
 /* ---- casts (precision alignment) ---- */
@@ -76,8 +82,11 @@ int64_t  orc_src_request_base(const orc_problem *p, int r);  /* elements; 0 for 
 /* element index in shard *shard, or -1 when the token's source page id lies
  * outside [0, src_num_blocks) (ORC_PAGED): such a row is never written */
 int64_t  orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, int d, int *shard);
+/* l is a converted layer (0..layers-1); the cache holds it at dst_layer_offset + l */
 int64_t  orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d);
 int64_t  orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i);
+int32_t  orc_src_layers(const orc_problem *p);   /* layers held by the source buffers */
+int32_t  orc_dst_layers(const orc_problem *p);   /* layers held by the cache */
 /* wire ("one-dimensional tensor") segments: byte offsets per request */
 int64_t  orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off);
 int      orc_fmt_size(int fmt);
