@@ -97,9 +97,13 @@ def main():
     bt, stride = W.block_table(w, lens)
     log(f"{w.name}: {len(lens)} requests, {int(lens.sum())} tokens; generating inputs")
     t0 = time.time()
-    shards = W.source_shards(w, lens)
+    # prefill pipeline stages: each holds a layer range in its own buffers and
+    # gets its own plan; all of them fill the one decode cache
+    stages = W.src_stages(w)
+    stage_shards = [W.source_shards(w, lens, l0, n) for l0, n in stages]
     log(f"inputs generated in {time.time() - t0:.1f}s; uploading")
-    dshards = [None if s is None else torch.from_numpy(s.view(np.int16)).cuda() for s in shards]
+    stage_dshards = [[None if s is None else torch.from_numpy(s.view(np.int16)).cuda() for s in sh]
+                     for sh in stage_shards]
     bt_d = torch.from_numpy(bt).cuda()
     F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
     order = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order]
@@ -110,20 +114,21 @@ def main():
         sbt, sstride = W.src_block_table(w, lens)
         sbt_d = torch.from_numpy(sbt).cuda()
 
-    def desc(seq):
-        return K.make_desc(w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
+    def desc(seq, stage):
+        l0, n = stage
+        return K.make_desc(n, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
                            F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks, seq,
-                           w.src_block_size, w.src_num_blocks)
+                           w.src_block_size, w.src_num_blocks, 0, n, l0, w.layers)
 
-    plan = K.kvx_plan(desc(list(lens)))
-    info = K.kvx_plan_info_get(plan)
+    plans = [K.kvx_plan(desc(list(lens), st)) for st in stages]
+    infos = [K.kvx_plan_info_get(p) for p in plans]
     esz = 1 if w.dst_dtype == "e4m3fn" else 2
     n_rows = w.layers * 2 * w.num_blocks * w.block_size * w.hd
     cache = torch.empty(n_rows * w.head_dim * esz, dtype=torch.uint8, device="cuda")
     scales = torch.empty(n_rows, dtype=torch.float32, device="cuda") if esz == 1 else None
     log(f"pool {cache.numel() / 2**30:.1f} GiB allocated")
     stream = torch.cuda.current_stream()
-    rep_bytes = info.read_bytes_repack + info.write_bytes_repack
+    rep_bytes = sum(i.read_bytes_repack + i.write_bytes_repack for i in infos)
 
     def timed(fn, steps, warmup):
         for _ in range(warmup):
@@ -143,10 +148,11 @@ def main():
         return wall * 1e3, statistics.mean(kern), min(kern), statistics.median(kern)
 
     def repack():
-        if paged:
-            K.kvx_repack_paged(plan, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream)
-        else:
-            K.kvx_repack(plan, dshards, cache, scales, bt_d, stride, stream)
+        for plan, dsh in zip(plans, stage_dshards):
+            if paged:
+                K.kvx_repack_paged(plan, dsh, sbt_d, sstride, cache, scales, bt_d, stride, stream)
+            else:
+                K.kvx_repack(plan, dsh, cache, scales, bt_d, stride, stream)
 
     log(f"repack: {args.warmup} warm-up + {args.steps} timed steps")
     ms_step, k_mean, k_min, k_med = timed(repack, args.steps, args.warmup)
@@ -165,6 +171,8 @@ def main():
                    "src_dtype": w.src_dtype, "dst_dtype": w.dst_dtype,
                    "src_order": w.src_order, "block_size": w.block_size,
                    "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes},
+        **({"prefill_stages": [list(st) for st in stages], "launches_per_step": len(stages)}
+           if len(stages) > 1 else {}),
         **({"src_pages": {"block_size": w.src_block_size, "pool_blocks": w.src_num_blocks}}
            if paged else {}),
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
@@ -181,43 +189,49 @@ def main():
                        "algorithmic_bytes_per_launch": rep_bytes}
 
     if not args.no_extras:
-        wire = torch.empty(int(info.wire_bytes), dtype=torch.uint8, device="cuda")
+        wires = [torch.empty(int(i.wire_bytes), dtype=torch.uint8, device="cuda") for i in infos]
 
         def pack():
-            if paged:
-                K.kvx_pack_paged(plan, dshards, sbt_d, sstride, wire, stream)
-            else:
-                K.kvx_pack(plan, dshards, wire, stream)
+            for plan, dsh, wire in zip(plans, stage_dshards, wires):
+                if paged:
+                    K.kvx_pack_paged(plan, dsh, sbt_d, sstride, wire, stream)
+                else:
+                    K.kvx_pack(plan, dsh, wire, stream)
 
         def unpack():
-            K.kvx_unpack(plan, wire, cache, scales, bt_d, stride, stream)
+            for plan, wire in zip(plans, wires):
+                K.kvx_unpack(plan, wire, cache, scales, bt_d, stride, stream)
 
-        for name, fn, nbytes in (("pack", pack, info.read_bytes_pack + info.write_bytes_pack),
-                                 ("unpack", unpack,
-                                  info.read_bytes_unpack + info.write_bytes_unpack)):
+        pack_bytes = sum(i.read_bytes_pack + i.write_bytes_pack for i in infos)
+        unpack_bytes = sum(i.read_bytes_unpack + i.write_bytes_unpack for i in infos)
+        for name, fn, nbytes in (("pack", pack, pack_bytes), ("unpack", unpack, unpack_bytes)):
             ms, km, _, _ = timed(fn, max(5, args.steps // 2), 2)
             out[name] = {"ms_per_step": round(ms, 4), "kernel_ms": round(km, 4),
                          "GB/s": round(nbytes / (km * 1e-3) / 1e9, 1)}
             log(f"{name}: kernel {km:.3f} ms")
-        del wire
+        del wires
 
-        # per-request latency: a single-request plan per request, host call to completion
+        # per-request latency: single-request plans (one per prefill stage) per
+        # request, host call to completion
         lat = []
         src_off = 0
         for r, T in enumerate(lens.tolist()):
-            p1 = K.kvx_plan(desc([T]))
+            p1s = [K.kvx_plan(desc([T], st)) for st in stages]
             row = bt_d[r:r + 1]
             if paged:   # the same pools, this request's row of the source block table
                 srow = sbt_d[r:r + 1]
 
                 def one():
-                    K.kvx_repack_paged(p1, dshards, srow, sstride, cache, scales, row, stride,
-                                       stream)
+                    for p1, dsh in zip(p1s, stage_dshards):
+                        K.kvx_repack_paged(p1, dsh, srow, sstride, cache, scales, row, stride,
+                                           stream)
             else:
-                sh = [None if s is None else s[src_off:] for s in dshards]
+                shs = [[None if s is None else s[src_off * n // w.layers:] for s in dsh]
+                       for (_, n), dsh in zip(stages, stage_dshards)]
 
                 def one():
-                    K.kvx_repack(p1, sh, cache, scales, row, stride, stream)
+                    for p1, sh in zip(p1s, shs):
+                        K.kvx_repack(p1, sh, cache, scales, row, stride, stream)
             src_off += w.layers * 2 * T * w.hs * w.head_dim
             ev = torch.cuda.Event()
             one()   # warm
@@ -239,7 +253,8 @@ def main():
         log(f"latency p50 {out['latency_ms_per_request']['p50']} ms")
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, lens, shards, args.cpu_seconds, value, sbt)
+        out["cpu_baseline"] = cpu_baseline(w, lens, stage_shards[0], args.cpu_seconds, value, sbt,
+                                           stages[0])
     print(json.dumps(out), flush=True)
 
 
@@ -313,11 +328,12 @@ def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
     print(json.dumps(rec))
 
 
-def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None):
+def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
     """The oracle as it stands (single thread), on whole requests of the same
     workload until about budget_s seconds of CPU work; decode pages renumbered
     into a compact host pool (same rows, same bytes).  A paged source is read
-    in place through the request's row of the source block table."""
+    in place through the request's row of the source block table.  With
+    prefill stages, the sample is the first stage's layers."""
     import numpy as np
 
     import oracle as O
@@ -325,6 +341,7 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None):
     f = {"fp16": O.FP16, "bf16": O.BF16, "e4m3fn": O.E4M3FN}
     order = {"thd": O.TOKEN_MAJOR, "htd": O.HEAD_MAJOR, "paged": O.PAGED}[w.src_order]
     esz = 1 if w.dst_dtype == "e4m3fn" else 2
+    L = stage[1] if stage else w.layers
     done_bytes = 0
     spent = 0.0
     off = 0
@@ -338,10 +355,10 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None):
         if sbt is not None:
             extra = dict(src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
                          src_block_table=sbt[r:r + 1], src_bt_stride=sbt.shape[1])
-        p = O.OracleProblem(w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
+        p = O.OracleProblem(L, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
                             f[w.src_dtype], f[w.dst_dtype], order, w.block_size, max(nb, 1), [T],
                             **extra)
-        cnt = w.layers * 2 * T * w.hs * w.head_dim
+        cnt = L * 2 * T * w.hs * w.head_dim
         if sbt is not None:
             part = shards
         else:
@@ -353,7 +370,7 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None):
         t = time.perf_counter()
         O.repack(p, part, cache, sc, bt, max(nb, 1))
         spent += time.perf_counter() - t
-        rows = w.layers * 2 * T * w.hd
+        rows = L * 2 * T * w.hd
         done_bytes += rows * w.head_dim * (2 + esz) + (rows * 4 if esz == 1 else 0)
         n += 1
         tokens += T

@@ -25,7 +25,8 @@
  *   source shard j (j = 0..src_tp-1) holds global heads [j*Hs, (j+1)*Hs),
  *     Hs = num_kv_heads / src_tp; requests are stored back to back, request r
  *     as [layer][k/v][token][Hs][dim] (KVX_THD) or [layer][k/v][Hs][token][dim]
- *     (KVX_HTD), T_r tokens; or (KVX_PAGED) the shard is the prefill side's
+ *     (KVX_HTD), T_r tokens, over the source's src_layers layers; or
+ *     (KVX_PAGED) the shard is the prefill side's
  *     own paged cache [layer][k/v][src_num_blocks][src_block_size][Hs][dim]:
  *     token t of request r sits in page
  *     src_block_table[r*src_bt_stride + t/src_block_size], slot
@@ -33,10 +34,10 @@
  *     of Sec. III-B-2 use paged attention, each with its own page size);
  *   decode rank dst_rank holds global heads [dst_rank*Hd, (dst_rank+1)*Hd),
  *     Hd = num_kv_heads / dst_tp;
- *   cache:  [layer][k/v][num_blocks][block_size][Hd][dim] in dst_dtype; token
+ *   cache:  [dst layer][k/v][num_blocks][block_size][Hd][dim] in dst_dtype; token
  *     t of request r goes to page block_table[r*bt_stride + t/block_size],
  *     slot t % block_size;
- *   scales (e4m3fn only): [layer][k/v][num_blocks][block_size][Hd] fp32;
+ *   scales (e4m3fn only): [dst layer][k/v][num_blocks][block_size][Hd] fp32;
  *   transfer tensor: per request, starting on a 256-byte boundary,
  *     [layer][k/v][token][Hd][dim] in dst_dtype, then (e4m3fn only) on the
  *     next 256-byte boundary [layer][k/v][token][Hd] fp32 scales.
@@ -71,7 +72,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 2
+#define KVX_ABI_VERSION 3
 
 typedef enum {
     KVX_OK = 0,
@@ -112,6 +113,16 @@ typedef struct {
     /* KVX_PAGED sources only (ignored otherwise): */
     int32_t src_block_size; /* tokens per prefill-side page, >= 1 */
     int64_t src_num_blocks; /* pages per (layer, k/v) plane of each shard's pool, >= 1 */
+    /* Pipeline stages: the source buffers hold src_layers layers and converted
+     * layer l (0 <= l < num_layers) is their layer src_layer_offset + l; the
+     * cache (and scales) hold dst_layers layers and receive layer l at
+     * dst_layer_offset + l.  The transfer tensor carries the num_layers
+     * converted layers only.  src_layers / dst_layers = 0 mean num_layers
+     * (with offset 0).  All zero: both sides hold exactly the converted layers. */
+    int32_t src_layer_offset;
+    int32_t src_layers;
+    int32_t dst_layer_offset;
+    int32_t dst_layers;
 } kvx_desc;
 
 typedef struct {
@@ -133,6 +144,8 @@ typedef struct {
  * H % dst_tp != 0; dst_rank outside [0, dst_tp); block_size <= 0;
  * num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
  * an unknown order; for KVX_PAGED, src_block_size <= 0 or src_num_blocks <= 0;
+ * a negative layer offset or count, or converted layers outside either side's
+ * src_layers / dst_layers;
  * head_dim * element size not a multiple of 16 bytes on either side.
  * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
  * fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row (head_dim * dst

@@ -46,6 +46,8 @@ class kvx_desc(ctypes.Structure):
         ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int64),
         ("num_requests", ctypes.c_int32), ("seq_lens", ctypes.POINTER(ctypes.c_int32)),
         ("src_block_size", ctypes.c_int32), ("src_num_blocks", ctypes.c_int64),
+        ("src_layer_offset", ctypes.c_int32), ("src_layers", ctypes.c_int32),
+        ("dst_layer_offset", ctypes.c_int32), ("dst_layers", ctypes.c_int32),
     ]
 
 
@@ -137,14 +139,16 @@ class Plan:
 
 
 def make_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype, dst_dtype,
-              src_order, block_size, num_blocks, seq_lens, src_block_size=0, src_num_blocks=0):
-    """kvx_desc plus the int32 array its seq_lens points into (the last two
-    fields matter only for a PAGED source)."""
+              src_order, block_size, num_blocks, seq_lens, src_block_size=0, src_num_blocks=0,
+              src_layer_offset=0, src_layers=0, dst_layer_offset=0, dst_layers=0):
+    """kvx_desc plus the int32 array its seq_lens points into (src_block_size
+    and src_num_blocks matter only for a PAGED source; the layer fields
+    describe pipeline stages, 0 = the converted layers)."""
     lens = (ctypes.c_int32 * max(len(seq_lens), 1))(*[int(t) for t in seq_lens])
     d = kvx_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype,
                  dst_dtype, src_order, block_size, num_blocks, len(seq_lens),
                  ctypes.cast(lens, ctypes.POINTER(ctypes.c_int32)), src_block_size,
-                 src_num_blocks)
+                 src_num_blocks, src_layer_offset, src_layers, dst_layer_offset, dst_layers)
     d._lens = lens
     return d
 

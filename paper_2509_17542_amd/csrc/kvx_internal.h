@@ -74,7 +74,9 @@ struct KArgs {
     uint32_t units;                   // work units: planes x pages x segments x parts
     uint32_t units_per_xcd;           // grid / kXcds
     uint32_t num_items;               // logical pages per plane
-    uint32_t planes;                  // 2 x layers
+    uint32_t planes;                  // 2 x converted layers
+    uint32_t src_plane0;              // 2 x source layer offset (pipeline stages)
+    uint32_t dst_plane0;              // 2 x cache layer offset
     uint32_t num_segs;
     uint32_t parts;                   // workgroup passes per (page, segment)
     FastDiv div_parts, div_segs, div_items, div_bs;

@@ -234,8 +234,8 @@ __device__ __forceinline__ void warm_translation(const KArgs& a, uint32_t unit)
     const uint32_t fu = unit + uint32_t(kPrefetchPages) * a.parts * a.num_segs;
     if (fu >= a.units) return;
     const uint32_t page_unit = fdiv(fdiv(fu, a.div_parts), a.div_segs);
-    const uint32_t plane = fdiv(page_unit, a.div_items);
-    const Item it = a.items[page_unit - plane * a.num_items];
+    const uint32_t plane = fdiv(page_unit, a.div_items) + a.dst_plane0;  // cache plane
+    const Item it = a.items[page_unit - (plane - a.dst_plane0) * a.num_items];
     const int32_t b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
     if (b < 0 || b >= a.num_blocks) return;
     const volatile uint32_t* q = reinterpret_cast<const volatile uint32_t*>(
@@ -256,11 +256,13 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     // any lane-dependent branch and every lane issues its row load
     // unconditionally (lanes without a row read the buffer's first vector), so
     // the lookups, the row loads and the paged source's page lookup overlap
-    // instead of following one another.  Measured faster for paged sources
-    // (+11%) and 16-bit token-major rows (+2%); the head-major and e4m3fn
-    // paths measure 2-4% faster with the row load inside the branch.
+    // instead of following one another.  Measured faster for repacks from
+    // paged sources (+16%) and 16-bit token-major rows (+2%); the head-major
+    // and e4m3fn paths and the pack from paged sources measure 2-4% faster
+    // with the row load inside the branch.
     constexpr bool kEarly =
-        ORDER == KVX_PAGED || (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16));
+        (ORDER == KVX_PAGED && MODE != kPack) ||
+        (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16));
 
     // XCD-contiguous unit of this workgroup -> (plane, page, segment, part)
     const uint32_t unit = (blockIdx.x % kXcds) * a.units_per_xcd + blockIdx.x / kXcds;
@@ -327,9 +329,9 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         const int h = seg.h0 + ii;                           // head within the shard
         int64_t e = 0;
         if constexpr (ORDER == KVX_THD) {
-            e = (int64_t(plane) * T + t0 + s) * a.hs + h;
+            e = (int64_t(plane + a.src_plane0) * T + t0 + s) * a.hs + h;
         } else if constexpr (ORDER == KVX_HTD) {
-            e = (int64_t(plane) * a.hs + h) * T + t0 + s;
+            e = (int64_t(plane + a.src_plane0) * a.hs + h) * T + t0 + s;
         } else {
             // the prefill side's own page of this token; a row whose page id
             // lies outside the source pool is neither read nor written
@@ -341,7 +343,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
                 sb = a.sbt[int64_t(it.req) * a.sbt_stride + q];
             }
             ok = ok && sb >= 0 && sb < a.src_num_blocks;
-            e = ((int64_t(plane) * a.src_num_blocks + sb) * a.src_block_size +
+            e = ((int64_t(plane + a.src_plane0) * a.src_num_blocks + sb) * a.src_block_size +
                  int64_t(t - q * uint32_t(a.src_block_size))) * a.hs + h;
         }
         p = base + (it.src_base + e * a.head_dim) * kSrcEsz + sub * (kLaneElems * kSrcEsz);
@@ -385,8 +387,9 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         if (part == 0 && sg == 0 && threadIdx.x == 0) warm_translation(a, unit);
         if (b < 0 || b >= a.num_blocks) return;  // not a page of the pool: nothing written
         const int64_t page_rows = int64_t(b) * a.block_size * a.hd;
-        dbase = static_cast<char*>(a.dst) + plane * a.plane_bytes + page_rows * a.row_dst_bytes;
-        if constexpr (kScales) sbase = a.dscale + plane * a.plane_scales + page_rows;
+        const uint32_t cplane = plane + a.dst_plane0;  // the cache's own layer
+        dbase = static_cast<char*>(a.dst) + cplane * a.plane_bytes + page_rows * a.row_dst_bytes;
+        if constexpr (kScales) sbase = a.dscale + cplane * a.plane_scales + page_rows;
     }
 
     uint4 out;

@@ -68,6 +68,9 @@ int pick_conv(int s, int d)
     return -1;
 }
 
+int32_t src_layers_of(const kvx_desc& d) { return d.src_layers ? d.src_layers : d.num_layers; }
+int32_t dst_layers_of(const kvx_desc& d) { return d.dst_layers ? d.dst_layers : d.num_layers; }
+
 kvx_status validate(const kvx_desc* d)
 {
     if (d->num_layers <= 0 || d->num_kv_heads <= 0 || d->head_dim <= 0)
@@ -106,8 +109,17 @@ kvx_status validate(const kvx_desc* d)
         return fail(KVX_EUNSUPPORTED, "more than %d heads per decode rank", kvx::kMaxHeadsPerRank);
     if (d->num_kv_heads / d->src_tp > 65535)
         return fail(KVX_EUNSUPPORTED, "more than 65535 heads per source shard");
-    if (int64_t(d->num_layers) * 2 > 65535)
-        return fail(KVX_EUNSUPPORTED, "2 * num_layers above 65535");
+    if (d->src_layer_offset < 0 || d->src_layers < 0 || d->dst_layer_offset < 0 ||
+        d->dst_layers < 0)
+        return fail(KVX_EINVAL, "negative layer offset or count");
+    if (int64_t(d->src_layer_offset) + d->num_layers > src_layers_of(*d))
+        return fail(KVX_EINVAL, "layers [%d, %d) outside the %d source layers", d->src_layer_offset,
+                    d->src_layer_offset + d->num_layers, src_layers_of(*d));
+    if (int64_t(d->dst_layer_offset) + d->num_layers > dst_layers_of(*d))
+        return fail(KVX_EINVAL, "layers [%d, %d) outside the %d cache layers", d->dst_layer_offset,
+                    d->dst_layer_offset + d->num_layers, dst_layers_of(*d));
+    if (int64_t(src_layers_of(*d)) * 2 > 65535 || int64_t(dst_layers_of(*d)) * 2 > 65535)
+        return fail(KVX_EUNSUPPORTED, "2 * layers above 65535");
     return KVX_OK;
 }
 
@@ -170,7 +182,7 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         const int64_t T = p->lens[r];
         const int64_t rows = L2 * T * p->hd;
         src_base[r] = paged ? 0 : src_off;  // a paged source is addressed through its pages
-        src_off += L2 * T * p->hs * d.head_dim;
+        src_off += 2 * int64_t(src_layers_of(d)) * T * p->hs * d.head_dim;
         if (paged)
             p->max_src_blocks = int32_t(std::max<int64_t>(
                 p->max_src_blocks, (T + d.src_block_size - 1) / d.src_block_size));
@@ -398,6 +410,8 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     a.bt = bt;
     a.num_items = uint32_t(p->items.size());
     a.planes = uint32_t(2 * d.num_layers);
+    a.src_plane0 = uint32_t(2 * d.src_layer_offset);
+    a.dst_plane0 = uint32_t(2 * d.dst_layer_offset);
     if (mode == kvx::kUnpack) {  // transfer-tensor rows are already in decode order
         a.num_segs = 1;
         a.parts = uint32_t(p->parts_unpack);

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 2
+    assert K.kvx_abi_version() == 3
 
 
 def desc_for(w, lens, **over):
@@ -234,3 +234,24 @@ def test_workload_source_block_tables_are_valid():
         plan = K.kvx_plan(desc_for(w, lens))
         K.kvx_check_src_block_table(plan, sbt, sstride)
         K.kvx_check_block_table(plan, bt, stride)
+
+
+@pytest.mark.parametrize("over", [dict(src_layer_offset=1), dict(src_layers=1),
+                                  dict(dst_layer_offset=3, dst_layers=4),
+                                  dict(src_layer_offset=-1, src_layers=4), dict(dst_layers=-1)])
+def test_plan_rejects_layer_ranges(over):
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_plan(K.make_desc(**dict(BASE, **over)))
+    assert e.value.status == K.EINVAL and "layer" in K.kvx_last_error()
+
+
+def test_plan_accepts_a_layer_range():
+    """Layers 3..4 of a prefill stage holding 5 layers, into a decode stage
+    holding 8 layers at 6..7: the byte counts and the transfer tensor cover
+    the 2 converted layers only."""
+    stage = K.kvx_plan(K.make_desc(**dict(BASE, src_layer_offset=3, src_layers=5,
+                                          dst_layer_offset=6, dst_layers=8)))
+    whole = K.kvx_plan(K.make_desc(**BASE))
+    a, b = K.kvx_plan_info_get(stage), K.kvx_plan_info_get(whole)
+    assert (a.read_bytes_repack, a.write_bytes_repack, a.wire_bytes) == \
+        (b.read_bytes_repack, b.write_bytes_repack, b.wire_bytes)

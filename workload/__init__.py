@@ -96,6 +96,7 @@ class Workload:
     lens_override: tuple | None = None   # explicit tokens per request (edge cases)
     src_block_size: int = 0  # "paged" sources: tokens per prefill-side page
     src_num_blocks: int = 0  # "paged" sources: pages per (layer, k/v) plane of each shard's pool
+    src_pp: int = 1          # prefill pipeline stages: equal layer ranges, one buffer set each
 
     @property
     def hs(self):
@@ -164,6 +165,11 @@ WORKLOADS = {
         Workload("llama3_70b_paged16_tp4to2_bf16_bs32", 80, 80, 8, 128, 4, 2, 0, "bf16", "bf16",
                  "paged", 32, 16384, 8, 1024, 8192, seed=17548, src_block_size=16,
                  src_num_blocks=4096),
+        # the Llama-3-8B workload (same seed, same values) from a prefill side
+        # in 2 pipeline stages of 16 layers, each with its own buffers, into
+        # one decode cache: one plan per stage
+        Workload("llama3_8b_pp2to1_bf16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "bf16", "thd",
+                 16, 65536, 16, 512, 4096, seed=17543, src_pp=2),
     ]
 }
 
@@ -199,6 +205,18 @@ def block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
         bt[r, :n] = perm[pos:pos + n]
         pos += n
     return bt, stride
+
+
+def src_stages(w: Workload) -> list[tuple[int, int]]:
+    """(first layer, layer count) of each prefill pipeline stage: w.layers
+    split into w.src_pp ranges as equal as possible, earlier stages larger."""
+    q, rem = divmod(w.layers, w.src_pp)
+    out, l0 = [], 0
+    for k in range(w.src_pp):
+        n = q + (1 if k < rem else 0)
+        out.append((l0, n))
+        l0 += n
+    return out
 
 
 def src_block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
