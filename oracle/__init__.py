@@ -55,6 +55,11 @@ def lib():
         L.orc_row_scale.restype = ctypes.c_float
         L.orc_row_scale.argtypes = [vp, ctypes.c_int]
         L.orc_fp16_to_bf16_n.argtypes = [vp, vp, ctypes.c_int64]
+        L.orc_bf16_to_fp16_n.argtypes = [vp, vp, ctypes.c_int64]
+        L.orc_src_heads.restype = ctypes.c_int32
+        L.orc_src_heads.argtypes = [P(Problem)]
+        L.orc_dst_heads.restype = ctypes.c_int32
+        L.orc_dst_heads.argtypes = [P(Problem)]
         L.orc_f32_to_e4m3fn_n.argtypes = [vp, vp, ctypes.c_int64]
         L.orc_decode_n.argtypes = [ctypes.c_int, vp, vp, ctypes.c_int64]
         L.orc_convert_row.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, vp, vp]
@@ -122,11 +127,11 @@ class OracleProblem:
 
     @property
     def hs(self):
-        return self.c.heads // self.c.src_tp
+        return lib().orc_src_heads(self.ref())
 
     @property
     def hd(self):
-        return self.c.heads // self.c.dst_tp
+        return lib().orc_dst_heads(self.ref())
 
     @property
     def dst_layers_held(self):
@@ -166,6 +171,13 @@ def fp16_to_bf16(bits: np.ndarray) -> np.ndarray:
     bits = np.ascontiguousarray(bits, dtype=np.uint16)
     out = np.empty_like(bits)
     lib().orc_fp16_to_bf16_n(_ptr(bits), _ptr(out), bits.size)
+    return out
+
+
+def bf16_to_fp16(bits: np.ndarray) -> np.ndarray:
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty_like(bits)
+    lib().orc_bf16_to_fp16_n(_ptr(bits), _ptr(out), bits.size)
     return out
 
 

@@ -120,6 +120,26 @@ static uint32_t encode(int fmt, uint32_t sign, double mag)
     return s | ((uint32_t)(E + f.bias) << f.man_bits) | (uint32_t)frac;
 }
 
+/* bf16 -> fp16.  Finite values: round the exact value to the fp16 grid (11
+ * significand bits, emin = -14), ties to even; a rounded magnitude above the
+ * largest finite fp16 (65504) overflows to infinity, as IEEE rounding to
+ * nearest does.  Infinities stay infinite.  NaN (reading taken, as for fp16 ->
+ * bf16): keep the sign, set the quiet bit, put the 7 bf16 fraction bits at
+ * the top of the fp16 fraction. */
+uint16_t orc_bf16_to_fp16(uint16_t b)
+{
+    uint32_t sign = (b >> 15) & 1u;
+    double x = orc_decode(ORC_BF16, b);
+    if (isnan(x))
+        return (uint16_t)((sign << 15) | 0x7C00u | 0x0200u | ((b & 0x7Fu) << 3));
+    if (isinf(x))
+        return (uint16_t)((sign << 15) | 0x7C00u);
+    double m = rne_to_grid(fabs(x), 11, -14);
+    if (m > 65504.0)
+        return (uint16_t)((sign << 15) | 0x7C00u);
+    return (uint16_t)encode(ORC_FP16, sign, m);
+}
+
 /* fp16 -> bf16.  Finite values and infinities: round the exact value to the
  * bf16 grid (8 significand bits, emin = -126), ties to even; no fp16 value
  * can overflow bf16.  NaN (paper silent; reading taken): keep the sign, set
@@ -163,6 +183,11 @@ float orc_row_scale(const float *x, int n)
     return amax / 448.0f;
 }
 
+void orc_bf16_to_fp16_n(const uint16_t *in, uint16_t *out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) out[k] = orc_bf16_to_fp16(in[k]);
+}
+
 void orc_fp16_to_bf16_n(const uint16_t *in, uint16_t *out, int64_t n)
 {
     for (int64_t k = 0; k < n; ++k) out[k] = orc_fp16_to_bf16(in[k]);
@@ -192,6 +217,11 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
     if (src_fmt == ORC_FP16 && dst_fmt == ORC_BF16) {
         uint16_t *o = (uint16_t *)dst_row;
         for (int d = 0; d < D; ++d) o[d] = orc_fp16_to_bf16(s[d]);
+        return;
+    }
+    if (src_fmt == ORC_BF16 && dst_fmt == ORC_FP16) {
+        uint16_t *o = (uint16_t *)dst_row;
+        for (int d = 0; d < D; ++d) o[d] = orc_bf16_to_fp16(s[d]);
         return;
     }
     /* 16-bit float -> e4m3fn with a per-row fp32 scale */
@@ -236,7 +266,9 @@ int orc_validate(const orc_problem *p)
     if ((int64_t)p->src_layer_offset + p->layers > orc_src_layers(p)) return -1;
     if ((int64_t)p->dst_layer_offset + p->layers > orc_dst_layers(p)) return -1;
     if (p->src_tp <= 0 || p->dst_tp <= 0) return -1;
-    if (p->heads % p->src_tp != 0 || p->heads % p->dst_tp != 0) return -1;
+    /* each rank holds H / tp heads, or (tp a multiple of H) one replicated head */
+    if (p->heads % p->src_tp != 0 && p->src_tp % p->heads != 0) return -1;
+    if (p->heads % p->dst_tp != 0 && p->dst_tp % p->heads != 0) return -1;
     if (p->dst_rank < 0 || p->dst_rank >= p->dst_tp) return -1;
     if (p->block_size <= 0 || p->num_blocks <= 0) return -1;
     if (p->num_requests < 0 || (p->num_requests > 0 && !p->seq_lens)) return -1;
@@ -256,26 +288,46 @@ int orc_validate(const orc_problem *p)
     if (sf != ORC_FP16 && sf != ORC_BF16) return -2;
     if (sf == df) return 0;
     if (sf == ORC_FP16 && df == ORC_BF16) return 0;
+    if (sf == ORC_BF16 && df == ORC_FP16) return 0;
     if (df == ORC_E4M3FN) return 0;
     return -2;
 }
 
-/* Decode-side head i of rank dst_rank is global head g = dst_rank*Hd + i; the
- * prefill shard holding it is g / Hs, at local position g % Hs. */
+/* Heads per rank.  With tp <= H a rank holds H / tp consecutive heads; with
+ * tp a multiple of H every head is replicated on tp / H consecutive ranks and
+ * a rank holds one head. */
+int32_t orc_src_heads(const orc_problem *p)
+{
+    return p->src_tp <= p->heads ? p->heads / p->src_tp : 1;
+}
+int32_t orc_dst_heads(const orc_problem *p)
+{
+    return p->dst_tp <= p->heads ? p->heads / p->dst_tp : 1;
+}
+
+/* Decode-side head i of rank dst_rank is global head g = dst_rank*Hd + i (or,
+ * replicated, g = dst_rank / (dst_tp / H)).  The prefill shard holding it is
+ * g / Hs at local position g % Hs; replicated, the first of its replicas,
+ * shard g * (src_tp / H), local position 0. */
 void orc_head_source(const orc_problem *p, int i, int *shard, int *head)
 {
-    int Hs = p->heads / p->src_tp;
-    int Hd = p->heads / p->dst_tp;
-    int g = p->dst_rank * Hd + i;
-    *shard = g / Hs;
-    *head = g % Hs;
+    int H = p->heads;
+    int g = p->dst_tp <= H ? p->dst_rank * (H / p->dst_tp) + i : p->dst_rank / (p->dst_tp / H);
+    if (p->src_tp <= H) {
+        int Hs = H / p->src_tp;
+        *shard = g / Hs;
+        *head = g % Hs;
+    } else {
+        *shard = g * (p->src_tp / H);
+        *head = 0;
+    }
 }
 
 /* Requests are stored back to back in every shard buffer, each one as
  * [layer][k/v][...Hs heads x T tokens...][dim]. */
 int64_t orc_src_request_base(const orc_problem *p, int r)
 {
-    int64_t Hs = p->heads / p->src_tp;
+    int64_t Hs = orc_src_heads(p);
     int64_t base = 0;
     if (p->src_order == ORC_PAGED) return 0; /* pages, not back-to-back requests */
     for (int q = 0; q < r; ++q)
@@ -291,7 +343,7 @@ static int64_t src_index_from(const orc_problem *p, int64_t base, int r, int l, 
     int j, h;
     orc_head_source(p, i, &j, &h);
     *shard = j;
-    int64_t Hs = p->heads / p->src_tp;
+    int64_t Hs = orc_src_heads(p);
     int64_t T = p->seq_lens[r];
     int64_t D = p->head_dim;
     int64_t plane = ((int64_t)p->src_layer_offset + l) * 2 + kv; /* in the source's layers */
@@ -316,7 +368,7 @@ int64_t orc_src_index(const orc_problem *p, int r, int l, int kv, int t, int i, 
 /* decode-side paged cache: [layer][k/v][block][slot][Hd][dim] */
 int64_t orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i, int d)
 {
-    int64_t Hd = p->heads / p->dst_tp;
+    int64_t Hd = orc_dst_heads(p);
     int64_t plane = ((int64_t)p->dst_layer_offset + l) * 2 + kv; /* in the cache's layers */
     return (((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i) * p->head_dim + d;
 }
@@ -324,7 +376,7 @@ int64_t orc_cache_index(const orc_problem *p, int64_t block, int l, int kv, int 
 /* decode-side scales: [layer][k/v][block][slot][Hd] */
 int64_t orc_cache_scale_index(const orc_problem *p, int64_t block, int l, int kv, int slot, int i)
 {
-    int64_t Hd = p->heads / p->dst_tp;
+    int64_t Hd = orc_dst_heads(p);
     int64_t plane = ((int64_t)p->dst_layer_offset + l) * 2 + kv;
     return ((plane * p->num_blocks + block) * p->block_size + slot) * Hd + i;
 }
@@ -337,7 +389,7 @@ static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
  * boundary.  Returns the total size in bytes. */
 int64_t orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off)
 {
-    int64_t Hd = p->heads / p->dst_tp;
+    int64_t Hd = orc_dst_heads(p);
     int64_t esz = orc_fmt_size(p->dst_fmt);
     int64_t off = 0;
     for (int r = 0; r < p->num_requests; ++r) {
@@ -377,7 +429,7 @@ int orc_pack(const orc_problem *p, const void *const *shards, void *wire)
 {
     int rc = orc_validate(p);
     if (rc) return rc;
-    int Hd = p->heads / p->dst_tp, D = p->head_dim;
+    int Hd = orc_dst_heads(p), D = p->head_dim;
     int64_t esz = orc_fmt_size(p->dst_fmt);
     int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
     int64_t *soff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
@@ -408,7 +460,7 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
 {
     int rc = orc_validate(p);
     if (rc) return rc;
-    int Hd = p->heads / p->dst_tp, D = p->head_dim, bs = p->block_size;
+    int Hd = orc_dst_heads(p), D = p->head_dim, bs = p->block_size;
     int64_t esz = orc_fmt_size(p->dst_fmt);
     int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
     int64_t *soff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
@@ -442,7 +494,7 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
 {
     int rc = orc_validate(p);
     if (rc) return rc;
-    int Hd = p->heads / p->dst_tp, D = p->head_dim, bs = p->block_size;
+    int Hd = orc_dst_heads(p), D = p->head_dim, bs = p->block_size;
     int64_t esz = orc_fmt_size(p->dst_fmt);
     uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
     uint8_t *c = (uint8_t *)cache;
@@ -476,7 +528,7 @@ int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, in
     if (rc) return rc;
     if (r < 0 || r >= p->num_requests || l < 0 || l >= p->layers || kv < 0 || kv > 1) return -1;
     if (t0 < 0 || nt < 0 || t0 + nt > p->seq_lens[r]) return -1;
-    int Hd = p->heads / p->dst_tp, D = p->head_dim;
+    int Hd = orc_dst_heads(p), D = p->head_dim;
     int64_t esz = orc_fmt_size(p->dst_fmt);
     uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
     uint8_t *o = (uint8_t *)out_rows;

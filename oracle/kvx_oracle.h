@@ -65,6 +65,8 @@ typedef struct {
 /* ---- casts (precision alignment) ---- */
 double   orc_decode(int fmt, uint32_t bits);             /* exact value; NaN/Inf as such */
 uint16_t orc_fp16_to_bf16(uint16_t h);                   /* IEEE round-to-nearest-even */
+uint16_t orc_bf16_to_fp16(uint16_t b);                   /* RNE; overflow to +-Inf */
+void     orc_bf16_to_fp16_n(const uint16_t *in, uint16_t *out, int64_t n);
 uint8_t  orc_f32_to_e4m3fn(float v);                     /* RNE, saturating to +-448 */
 float    orc_row_scale(const float *x, int n);           /* max|x| / 448, fp32 divide */
 void     orc_fp16_to_bf16_n(const uint16_t *in, uint16_t *out, int64_t n);
@@ -78,6 +80,8 @@ void     orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row,
 /* ---- index maps (parallel-strategy and VRAM-management alignment) ---- */
 int      orc_validate(const orc_problem *p);             /* 0 ok, -1 invalid, -2 unsupported */
 void     orc_head_source(const orc_problem *p, int i, int *shard, int *head);
+int32_t  orc_src_heads(const orc_problem *p);   /* heads per prefill shard (1 if replicated) */
+int32_t  orc_dst_heads(const orc_problem *p);   /* heads per decode rank (1 if replicated) */
 int64_t  orc_src_request_base(const orc_problem *p, int r);  /* elements; 0 for ORC_PAGED */
 /* element index in shard *shard, or -1 when the token's source page id lies
  * outside [0, src_num_blocks) (ORC_PAGED): such a row is never written */

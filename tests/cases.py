@@ -50,6 +50,29 @@ SMALL = {
                                         layers=1, total_layers=1, num_requests=4,
                                         lens_override=(37, 0, 16, 1), block_size=16,
                                         num_blocks=16, seed=99),
+    # GQA with more ranks than KV heads: 4 heads, decode TP8 rank 5 holds the
+    # replicated head 2
+    "gqa_rep_tp1to8_r5": QWEN.replace(name="gqa_rep_tp1to8_r5", layers=2, total_layers=2,
+                                      src_order="thd", dst_tp=8, dst_rank=5, num_requests=2,
+                                      len_lo=9, len_hi=70, block_size=16, num_blocks=16),
+    # replicated prefill shards: 4 heads over prefill TP8 (shard j holds head
+    # j // 2) -> decode TP2 rank 1 (heads 2, 3), bf16 -> e4m3fn
+    "gqa_src_rep_tp8to2_r1": FP8.replace(name="gqa_src_rep_tp8to2_r1", heads=4, layers=2,
+                                         total_layers=2, src_tp=8, dst_tp=2, dst_rank=1,
+                                         num_requests=2, len_lo=5, len_hi=40, num_blocks=16),
+    # both sides replicated: 2 heads, prefill TP4 -> decode TP8 rank 7, head-major
+    "gqa_both_rep_tp4to8_r7": QWEN.replace(name="gqa_both_rep_tp4to8_r7", heads=2, layers=1,
+                                          total_layers=1, src_tp=4, dst_tp=8, dst_rank=7,
+                                          num_requests=2, len_lo=3, len_hi=50, block_size=16,
+                                          num_blocks=16),
+    # bf16 -> fp16 with values up to about 4 sigma = 160000: many overflow to
+    # infinity, the rest round to nearest even (subnormals from the tail)
+    "bf16_fp16_overflow": L8B.replace(name="bf16_fp16_overflow", dst_dtype="fp16", layers=2,
+                                      total_layers=2, num_requests=2, len_lo=20, len_hi=60,
+                                      num_blocks=16, sigma=40000.0),
+    "bf16_fp16_small_values": L8B.replace(name="bf16_fp16_small_values", dst_dtype="fp16",
+                                          layers=1, total_layers=1, num_requests=1,
+                                          len_lo=40, len_hi=40, num_blocks=8, sigma=1e-6),
 }
 
 # Paged sources (the prefill side's own paged cache), same shapes as the two
@@ -103,10 +126,27 @@ def oracle_problem(O, w, lens, layers=None, sbt=None):
                            w.num_blocks, lens, **extra)
 
 
+def rank_heads(w):
+    """Global heads [g0, g1) of the produced decode rank: [rank*Hd,
+    (rank+1)*Hd), or the one head rank // (dst_tp / H) when dst_tp is a
+    multiple of H (tensor parallelism replicates KV heads then)."""
+    if w.dst_tp <= w.heads:
+        return w.dst_rank * w.hd, (w.dst_rank + 1) * w.hd
+    g = w.dst_rank // (w.dst_tp // w.heads)
+    return g, g + 1
+
+
+def read_shards(w):
+    """Prefill shards that store a head of the produced decode rank (with
+    replicated heads, every replica): the ones the test inputs need."""
+    lo, hi = rank_heads(w)
+    return [j for j in range(w.src_tp) if w.shard_heads(j)[0] < hi and w.shard_heads(j)[1] > lo]
+
+
 def inputs(w, layer0=0, nlayers=None):
     lens = W.seq_lens(w)
     bt, stride = W.block_table(w, lens)
-    shards = W.source_shards(w, lens, layer0, nlayers)
+    shards = W.source_shards(w, lens, layer0, nlayers, read_shards(w))
     return lens, bt, stride, shards
 
 
@@ -120,17 +160,18 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     logical values and torch library conversions:
     returns (rows uint8 [L][2][T][Hd][D*esize], scales float32 [L][2][T][Hd] or None).
 
-    Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd).
-    Casts: same type = bits; fp16->bf16 = torch .to(bfloat16);
+    Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd), or the
+    one head rank // (dst_tp / H) when dst_tp is a multiple of H.
+    Casts: same type = bits; fp16->bf16 and bf16->fp16 = torch .to();
     e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn)."""
-    heads = (w.dst_rank * w.hd, (w.dst_rank + 1) * w.hd)
+    heads = rank_heads(w)
     x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers, heads))
     x = x.to(_TDT[w.src_dtype])                                     # [L][2][Hd][T][D]
     x = x.permute(0, 1, 3, 2, 4).contiguous()                      # [L][2][T][Hd][D]
     if w.dst_dtype == w.src_dtype:
         return x.view(torch.uint8).numpy().reshape(*x.shape[:4], -1), None
-    if w.dst_dtype == "bf16":
-        y = x.to(torch.bfloat16)
+    if w.dst_dtype in ("bf16", "fp16"):
+        y = x.to(_TDT[w.dst_dtype])
         return y.view(torch.uint8).numpy().reshape(*y.shape[:4], -1), None
     xf = x.float()
     s = xf.abs().amax(dim=-1) / torch.tensor(448.0)

@@ -8,7 +8,7 @@ import torch
 
 import oracle as O
 import workload as W
-from cases import dst_size, oracle_problem
+from cases import dst_size, oracle_problem, read_shards
 
 import paper_2509_17542_amd as K
 
@@ -53,7 +53,7 @@ def check_shapes(w, lens, bt, stride, dshards, layers, sbt=None):
         assert len(lens) == 0 or (sbt.shape[0] == len(lens) and sbt.shape[1] >= snb)
     else:
         need = sum(layers * 2 * int(t) * Hs * D for t in lens)
-    for j in w.read_shards():
+    for j in read_shards(w):
         assert dshards[j] is not None and dshards[j].numel() >= need, (j, need)
     assert len(lens) == 0 or (bt.shape[0] == len(lens) and bt.shape[1] >= stride)
     # page ids outside [0, num_blocks) or [0, src_num_blocks) are allowed:

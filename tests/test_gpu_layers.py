@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from cases import FULL, SMALL, SMALL_PAGED, dst_size, oracle_problem
+from cases import FULL, SMALL, SMALL_PAGED, dst_size, oracle_problem, read_shards
 from gpu_util import DEV, check_sampled, check_unused_pages, desc_for, dev_u16, log
 
 import oracle as O
@@ -55,7 +55,7 @@ def _run_stage(w, lens, bt_d, stride, dshards, sbt_d, sstride, desc, cache, scal
         need = desc.src_layers * 2 * w.src_num_blocks * w.src_block_size * Hs * D
     else:
         need = sum(desc.src_layers * 2 * int(t) * Hs * D for t in lens)
-    for j in w.read_shards():
+    for j in read_shards(w):
         assert dshards[j].numel() >= need
     rows = desc.dst_layers * 2 * w.num_blocks * w.block_size * w.hd
     assert cache.numel() == rows * D * dst_size(w)

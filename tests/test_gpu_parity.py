@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 import torch
 
-from cases import FULL, SMALL, inputs, oracle_problem
+from cases import FULL, SMALL, inputs, oracle_problem, read_shards
 from gpu_util import (DEV, check_sampled, check_unused_pages, gpu_run, log, oracle_pool)
 
 import oracle as O
@@ -204,7 +204,7 @@ def _full_case(name, layer0=0, nlayers=None, extra_planes=2, n_req=4):
     log(f"full {name}: generating layers {layer0}..{layer0 + nlayers - 1}")
     lens = W.seq_lens(w)
     bt, stride = W.block_table(w, lens)
-    shards = W.source_shards(w, lens, layer0, nlayers)
+    shards = W.source_shards(w, lens, layer0, nlayers, read_shards(w))
     log(f"full {name}: repack on GPU ({int(lens.sum())} tokens)")
     cache, scales, _ = gpu_run("repack", w, lens, bt, stride, shards, nlayers)
     # every request in the first and the last plane; a few requests in random planes

@@ -76,6 +76,39 @@ def _parse_float(tok):
     return float.fromhex(tok) if "0x" in tok.lower() else float(tok)
 
 
+def test_bf16_to_fp16_golden():
+    rows = golden_lines("bf16_to_fp16.txt")
+    assert len(rows) == 21
+    for ln in rows:
+        b, want = (int(x, 16) for x in ln.split()[:2])
+        got = int(O.bf16_to_fp16(np.array([b], dtype=np.uint16))[0])
+        assert got == want, (ln, hex(got))
+
+
+def test_bf16_to_fp16_exhaustive_vs_torch():
+    """Every non-NaN bf16 pattern against torch's conversion (round to
+    nearest even through float32, overflow to infinity)."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got = O.bf16_to_fp16(bits)
+    t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16)
+    want = t.to(torch.float16).view(torch.int16).numpy().view(np.uint16)
+    nan = torch.isnan(t).numpy()
+    assert nan.sum() == 2 * 127
+    assert np.array_equal(got[~nan], want[~nan])
+
+
+def test_bf16_to_fp16_nan_reading():
+    """NaN: sign kept, quiet bit set, the 7 bf16 fraction bits at the top of
+    the fp16 fraction."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    nan = ((bits & 0x7F80) == 0x7F80) & ((bits & 0x7F) != 0)
+    got = O.bf16_to_fp16(bits[nan]).astype(np.uint32)
+    b = bits[nan].astype(np.uint32)
+    assert np.array_equal(got >> 15, b >> 15)
+    assert np.all((got & 0x7C00) == 0x7C00) and np.all(got & 0x0200)
+    assert np.array_equal((got >> 3) & 0x3F, b & 0x3F)
+
+
 def test_e4m3_golden_values():
     rows = golden_lines("e4m3_values.txt")
     assert len(rows) >= 19

@@ -51,6 +51,29 @@ def test_head_map_partitions_heads(H, ts, td):
     assert seen == list(range(H))
 
 
+@pytest.mark.parametrize("H,ts,td", [(4, 1, 8), (4, 8, 2), (2, 4, 8), (8, 16, 16), (4, 4, 8),
+                                     (4, 8, 1), (1, 2, 4)])
+def test_head_map_with_replicated_heads(H, ts, td):
+    """More ranks than KV heads: decode rank rho holds head rho // (td / H)
+    (td / H consecutive ranks per head), and the source chosen for every head
+    is a prefill shard that stores it (per the generator's prefill storage),
+    at that head's position in the shard."""
+    w = L8B.replace(heads=H, src_tp=ts, dst_tp=td)
+    seen = []
+    for rho in range(td):
+        p = O.OracleProblem(1, H, 16, ts, td, rho, O.BF16, O.BF16, O.TOKEN_MAJOR, 16, 4, [1])
+        assert O.validate(p) == 0
+        hd = p.hd
+        for i in range(hd):
+            g = rho * hd + i if td <= H else rho // (td // H)
+            j, h = O.head_source(p, i)
+            g0, g1 = w.replace(dst_rank=rho).shard_heads(j)
+            assert g0 <= g < g1 and h == g - g0, (rho, i, j, h)
+            seen.append(g)
+    assert sorted(set(seen)) == list(range(H))
+    assert all(seen.count(g) == max(1, td // H) for g in range(H))
+
+
 # ---- the decode side reads what the prefill side wrote ------------------------
 
 @pytest.mark.parametrize("name", list(SMALL))
@@ -231,7 +254,8 @@ def test_expected_rows_match_full_repack():
 @pytest.mark.parametrize("kw,code", [
     (dict(heads=6, src_tp=4), -1), (dict(dst_tp=3), -1), (dict(dst_rank=2), -1),
     (dict(dst_rank=-1), -1), (dict(layers=0), -1), (dict(block_size=0), -1),
-    (dict(src_fmt=O.E4M3FN, dst_fmt=O.E4M3FN), -2), (dict(src_fmt=O.BF16, dst_fmt=O.FP16), -2),
+    (dict(src_fmt=O.E4M3FN, dst_fmt=O.E4M3FN), -2), (dict(src_fmt=O.BF16, dst_fmt=99), -2),
+    (dict(heads=4, dst_tp=6), -1), (dict(heads=4, src_tp=6), -1), (dict(heads=6, dst_tp=4), -1),
 ])
 def test_validate_rejects(kw, code):
     base = dict(layers=2, heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_rank=0, src_fmt=O.FP16,
@@ -239,6 +263,21 @@ def test_validate_rejects(kw, code):
                 seq_lens=[10])
     base.update(kw)
     assert O.validate(O.OracleProblem(**base)) == code
+
+
+def test_bf16_to_fp16_case_overflows_and_keeps_the_rest():
+    """The bf16 -> fp16 overflow case holds infinities where |x| rounds above
+    65504 and finite values elsewhere (the casts are pinned exhaustively in
+    test_oracle_casts; this checks the case exercises both)."""
+    w = SMALL["bf16_fp16_overflow"]
+    lens, bt, stride, shards = inputs(w)
+    p = oracle_problem(O, w, lens)
+    cache, _ = _pool(p)
+    O.repack(p, shards, cache, None, bt, stride)
+    got = np.concatenate([gather_pages(cache, w, lens, bt, r, w.layers)[0].reshape(-1)
+                          for r in range(len(lens))]).view(np.uint16)
+    inf = (got & 0x7FFF) == 0x7C00
+    assert 0.05 < inf.mean() < 0.5
 
 
 def test_validate_rejects_negative_length():

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 from cases import (L8B, SMALL_PAGED, consumer_rows, dst_size, gather_pages, inputs,
-                   oracle_problem, written_mask)
+                   oracle_problem, read_shards, written_mask)
 
 import oracle as O
 import workload as W
@@ -37,7 +37,7 @@ def test_paged_source_generator_places_every_token_once(name):
             b = sbt[r, t // w.src_block_size]
             assert not used[b, t % w.src_block_size]
             used[b, t % w.src_block_size] = True
-    for j in w.read_shards():
+    for j in read_shards(w):
         pool = shards[j].reshape(w.layers, 2, w.src_num_blocks, w.src_block_size, -1)
         sentinel = (pool == W.SENTINEL * 0x0101).all(-1)
         assert np.array_equal(sentinel, np.broadcast_to(~used, sentinel.shape)), j

@@ -1,8 +1,10 @@
 """Seeded synthetic KV-cache workloads, shared by the tests and the benchmark.
 
 This module draws random numbers and arranges them in the prefill side's
-storage order; it holds none of the conversion's arithmetic (no head map to
-the decode side, no paging, no casts of the method).  Values are keyed by
+storage order (which heads each prefill shard stores, token- or head-major
+buffers, or the prefill side's own pages); it holds none of the conversion's
+arithmetic (no head map to the decode side, no decode paging, no casts of the
+method).  Values are keyed by
 logical coordinates (request, layer, k/v, global head, token, dim), so a
 different shard split or storage order of the same workload holds the same
 values.
@@ -100,11 +102,22 @@ class Workload:
 
     @property
     def hs(self):
-        return self.heads // self.src_tp
+        """heads per prefill shard: H / src_tp, or 1 when src_tp is a multiple
+        of H (each head then lives on src_tp / H consecutive shards)"""
+        return self.heads // self.src_tp if self.src_tp <= self.heads else 1
 
     @property
     def hd(self):
-        return self.heads // self.dst_tp
+        """heads per decode rank, likewise (sizes the decode pool)"""
+        return self.heads // self.dst_tp if self.dst_tp <= self.heads else 1
+
+    def shard_heads(self, j: int) -> tuple[int, int]:
+        """Global heads [g0, g1) that prefill shard j stores."""
+        if self.src_tp <= self.heads:
+            return j * self.hs, (j + 1) * self.hs
+        g = j // (self.src_tp // self.heads)
+        return g, g + 1
+
 
     @property
     def layer_groups(self):
@@ -114,11 +127,6 @@ class Workload:
         """(first global layer, layer count) of layer group g."""
         l0 = g * self.layers
         return l0, min(self.layers, self.total_layers - l0)
-
-    def read_shards(self) -> list[int]:
-        """Prefill shards whose head range overlaps the produced decode rank."""
-        lo, hi = self.dst_rank * self.hd, (self.dst_rank + 1) * self.hd
-        return [j for j in range(self.src_tp) if j * self.hs < hi and (j + 1) * self.hs > lo]
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -309,12 +317,13 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
     token t of request r sits in page src_block_table(w, lens)[r][t //
     src_block_size], slot t % src_block_size; slots holding no token keep the
     sentinel bytes.  Values are rounded from float32 to the storage type by
-    torch (round to nearest even).  Shards not listed are None."""
+    torch (round to nearest even).  Shards not listed in `shards` (default:
+    all of them) are None."""
     import torch
     if nlayers is None:
         nlayers = w.layers
     if shards is None:
-        shards = w.read_shards()
+        shards = list(range(w.src_tp))
     Hs, D = w.hs, w.head_dim
     if w.src_order == "paged":
         return _paged_source_shards(w, lens, layer0, nlayers, shards)
@@ -332,7 +341,7 @@ def source_shards(w: Workload, lens: np.ndarray, layer0: int = 0, nlayers: int |
             continue
         for j in shards:
             vals = torch.from_numpy(
-                logical_values(w, lens, r, layer0, nlayers, (j * Hs, (j + 1) * Hs), scratch))
+                logical_values(w, lens, r, layer0, nlayers, w.shard_heads(j), scratch))
             dst = torch.from_numpy(out[j][off:off + n].view(np.int16)).view(tdt)
             if w.src_order == "thd":
                 dst.view(nlayers, 2, T, Hs, D).copy_(vals.permute(0, 1, 3, 2, 4))
@@ -360,7 +369,7 @@ def _paged_source_shards(w: Workload, lens: np.ndarray, layer0: int, nlayers: in
         full = T // sbs
         for j in shards:
             vals = torch.from_numpy(
-                logical_values(w, lens, r, layer0, nlayers, (j * Hs, (j + 1) * Hs), scratch))
+                logical_values(w, lens, r, layer0, nlayers, w.shard_heads(j), scratch))
             x = vals.permute(0, 1, 3, 2, 4).to(tdt).view(torch.int16).numpy()  # [l][kv][t][h][d]
             pool = out[j].view(np.int16).reshape(nlayers, 2, nbs, sbs, Hs, D)
             ids = sbt[r, :nb]
