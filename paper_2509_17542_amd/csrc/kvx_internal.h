@@ -10,7 +10,7 @@ namespace kvx {
 
 constexpr int kThreads = 256;           // threads per workgroup (4 wave64)
 constexpr int kMaxHeadsPerRank = 1024;  // Hd limit
-constexpr int kMaxReadShards = 64;      // source shards one decode rank may read
+constexpr int kMaxReadShards = 64;      // head segments (and so source shards) of a decode rank
 constexpr int kMaxRowChunks = 64;       // 16-byte destination chunks per row (one wave)
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
 constexpr int kPrefetchPages = 32;      // pages ahead whose address translation a workgroup warms
@@ -46,11 +46,12 @@ enum Conv : int {
     kF16Bf16 = 1,   // fp16 -> bf16, round to nearest even
     kBf16E4m3 = 2,  // bf16 -> e4m3fn with per-row scale
     kF16E4m3 = 3,   // fp16 -> e4m3fn with per-row scale
-    kCopy8 = 4      // 8-bit bits unchanged (+ scale copy), unpack of e4m3fn
+    kCopy8 = 4,     // 8-bit bits unchanged (+ scale copy), unpack of e4m3fn
+    kBf16F16 = 5    // bf16 -> fp16, round to nearest even, overflow to infinity
 };
 
 // A run of the decode rank's heads that comes from one source shard: decode
-// heads [i0, i0 + n) are heads [h0, h0 + n) of shard slot `slot`.
+// heads [i0, i0 + n) are heads [h0, h0 + n) of the shard at src[slot].
 struct Segment {
     int32_t slot;
     int32_t h0;
@@ -61,8 +62,8 @@ struct Segment {
 
 // Kernel arguments (passed by value through the kernel-argument segment).
 struct KArgs {
-    const void* src[kMaxReadShards];  // shard first_shard + k at src[k]
-    Segment seg[kMaxReadShards];      // pack/repack: one per shard read; unpack: one, all heads
+    const void* src[kMaxReadShards];  // the k-th shard the decode rank reads at src[k]
+    Segment seg[kMaxReadShards];      // pack/repack: the head segments; unpack: one, all heads
     const void* wire_in;              // unpack source
     void* dst;                        // pack: transfer tensor; else cache
     float* dscale;                    // cache scales (unpack/repack, e4m3fn)

@@ -218,6 +218,43 @@ __device__ __forceinline__ uint4 to_bf16x8(const uint4& v)
     return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// 8 bf16 -> 8 fp16.  Without NaN: exact widening to fp32 and the hardware
+// fp32 -> fp16 conversion (round to nearest even, overflow to infinity, fp16
+// subnormals kept).  A NaN anywhere in the 8 sends them element by element
+// through the NaN rule: sign kept, quiet bit set, the 7 bf16 fraction bits at
+// the top of the fp16 fraction; other elements take the same conversion.
+__device__ __forceinline__ uint32_t bf16_to_f16(uint32_t b)
+{
+    if ((b & 0x7FFFu) > 0x7F80u) return (b & 0x8000u) | 0x7E00u | ((b & 0x7Fu) << 3);
+    const _Float16 h = static_cast<_Float16>(__uint_as_float(b << 16));
+    return __builtin_bit_cast(unsigned short, h);
+}
+
+__device__ __forceinline__ uint4 to_f16x8(const uint4& v)
+{
+    typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    us2 mm = {0, 0};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
+    uint32_t o[4];
+    if (max(uint32_t(mm.x), uint32_t(mm.y)) <= 0x7F80u) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const f2 f = {__uint_as_float(w[k] << 16), __uint_as_float(w[k] & 0xFFFF0000u)};
+            o[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, h2));
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            o[k] = bf16_to_f16(w[k] & 0xFFFFu) | (bf16_to_f16(w[k] >> 16) << 16);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // ---- the row kernel ----------------------------------------------------------
 
 __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f)
@@ -262,7 +299,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     // with the row load inside the branch.
     constexpr bool kEarly =
         (ORDER == KVX_PAGED && MODE != kPack) ||
-        (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16));
+        (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16 || CONV == kBf16F16));
 
     // XCD-contiguous unit of this workgroup -> (plane, page, segment, part)
     const uint32_t unit = (blockIdx.x % kXcds) * a.units_per_xcd + blockIdx.x / kXcds;
@@ -397,6 +434,8 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         out = to_e4m3<CONV>(v, lg, sc);  // every lane takes part in the row reduction
     else if constexpr (CONV == kF16Bf16)
         out = to_bf16x8(v[0]);
+    else if constexpr (CONV == kBf16F16)
+        out = to_f16x8(v[0]);
     else
         out = v[0];
     if (ok) {
@@ -450,6 +489,7 @@ int go_conv(int conv, const KArgs& a, void* stream)
     switch (conv) {
     case kCopy16: return go<MODE, kCopy16, ORDER>(a, stream);
     case kF16Bf16: return go<MODE, kF16Bf16, ORDER>(a, stream);
+    case kBf16F16: return go<MODE, kBf16F16, ORDER>(a, stream);
     case kBf16E4m3: return go<MODE, kBf16E4m3, ORDER>(a, stream);
     case kF16E4m3: return go<MODE, kF16E4m3, ORDER>(a, stream);
     default: return int(hipErrorInvalidValue);

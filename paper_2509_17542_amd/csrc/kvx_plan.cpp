@@ -22,7 +22,7 @@ struct kvx_plan_s {
     std::vector<int64_t> wire_data, wire_scale;  // per request, transfer-tensor offsets
     std::vector<Item> items;
     int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
-    int first_shard = 0, num_read_shards = 0;
+    std::vector<int> read_shards;  // prefill shards the decode rank reads, in slot order
     int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
     std::vector<kvx::Segment> segs;  // head runs of the decode rank, one per shard read
     int32_t max_blocks = 0;
@@ -63,10 +63,15 @@ int pick_conv(int s, int d)
     if (s != KVX_FP16 && s != KVX_BF16) return -1;
     if (s == d) return kvx::kCopy16;
     if (s == KVX_FP16 && d == KVX_BF16) return kvx::kF16Bf16;
+    if (s == KVX_BF16 && d == KVX_FP16) return kvx::kBf16F16;
     if (s == KVX_BF16 && d == KVX_FP8_E4M3FN) return kvx::kBf16E4m3;
     if (s == KVX_FP16 && d == KVX_FP8_E4M3FN) return kvx::kF16E4m3;
     return -1;
 }
+
+// Heads per rank: H / tp, or 1 when tp is a multiple of H (each KV head is
+// then replicated on tp / H consecutive ranks).
+int heads_per_rank(int H, int tp) { return tp <= H ? H / tp : 1; }
 
 int32_t src_layers_of(const kvx_desc& d) { return d.src_layers ? d.src_layers : d.num_layers; }
 int32_t dst_layers_of(const kvx_desc& d) { return d.dst_layers ? d.dst_layers : d.num_layers; }
@@ -77,8 +82,10 @@ kvx_status validate(const kvx_desc* d)
         return fail(KVX_EINVAL, "num_layers, num_kv_heads and head_dim must be >= 1");
     if (d->src_tp <= 0 || d->dst_tp <= 0)
         return fail(KVX_EINVAL, "src_tp and dst_tp must be >= 1");
-    if (d->num_kv_heads % d->src_tp || d->num_kv_heads % d->dst_tp)
-        return fail(KVX_EINVAL, "num_kv_heads (%d) must be divisible by src_tp (%d) and dst_tp (%d)",
+    if ((d->num_kv_heads % d->src_tp && d->src_tp % d->num_kv_heads) ||
+        (d->num_kv_heads % d->dst_tp && d->dst_tp % d->num_kv_heads))
+        return fail(KVX_EINVAL,
+                    "num_kv_heads (%d) and each TP degree (src %d, dst %d) must divide one another",
                     d->num_kv_heads, d->src_tp, d->dst_tp);
     if (d->dst_rank < 0 || d->dst_rank >= d->dst_tp)
         return fail(KVX_EINVAL, "dst_rank %d outside [0, %d)", d->dst_rank, d->dst_tp);
@@ -144,27 +151,36 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     p->d = d;
     p->lens.assign(d.seq_lens, d.seq_lens + d.num_requests);
     p->d.seq_lens = p->lens.data();
-    p->hs = d.num_kv_heads / d.src_tp;
-    p->hd = d.num_kv_heads / d.dst_tp;
+    p->hs = heads_per_rank(d.num_kv_heads, d.src_tp);
+    p->hd = heads_per_rank(d.num_kv_heads, d.dst_tp);
     p->esz_src = dtype_size(d.src_dtype);
     p->esz_dst = dtype_size(d.dst_dtype);
     p->conv = pick_conv(d.src_dtype, d.dst_dtype);
 
-    // parallel-strategy alignment: decode head i -> global g -> (shard, head)
-    const int g0 = d.dst_rank * p->hd;
-    p->first_shard = g0 / p->hs;
-    const int last_shard = (g0 + p->hd - 1) / p->hs;
-    p->num_read_shards = last_shard - p->first_shard + 1;
-    if (p->num_read_shards > kvx::kMaxReadShards) {
-        delete p;
-        return fail(KVX_EUNSUPPORTED, "decode rank reads more than %d shards", kvx::kMaxReadShards);
+    // parallel-strategy alignment: decode head i -> global head g -> (shard j,
+    // head h within it); runs of decode heads with the same shard and
+    // consecutive h form one head segment
+    const int H = d.num_kv_heads;
+    for (int i = 0; i < p->hd; ++i) {
+        const int g = d.dst_tp <= H ? d.dst_rank * p->hd + i : d.dst_rank / (d.dst_tp / H);
+        const int j = d.src_tp <= H ? g / p->hs : g * (d.src_tp / H);  // first replica
+        const int h = d.src_tp <= H ? g % p->hs : 0;
+        int slot = 0;
+        while (slot < int(p->read_shards.size()) && p->read_shards[slot] != j) ++slot;
+        if (slot == int(p->read_shards.size())) p->read_shards.push_back(j);
+        kvx::Segment* last = p->segs.empty() ? nullptr : &p->segs.back();
+        if (last && last->slot == slot && last->h0 + last->n == h && last->i0 + last->n == i) {
+            ++last->n;
+        } else {
+            if (int(p->segs.size()) == kvx::kMaxReadShards) {
+                delete p;
+                return fail(KVX_EUNSUPPORTED, "decode rank needs more than %d head segments",
+                            kvx::kMaxReadShards);
+            }
+            p->segs.push_back(kvx::Segment{slot, h, i, 1, {0, 0}});
+        }
     }
-    for (int k = 0; k < p->num_read_shards; ++k) {
-        const int j = p->first_shard + k;
-        const int lo = std::max(g0, j * p->hs), hi = std::min(g0 + p->hd, (j + 1) * p->hs);
-        p->segs.push_back(kvx::Segment{k, lo - j * p->hs, lo - g0, hi - lo, {0, 0}});
-        p->segs.back().div_n = kvx::make_fastdiv(uint32_t(hi - lo));
-    }
+    for (kvx::Segment& g : p->segs) g.div_n = kvx::make_fastdiv(uint32_t(g.n));
 
     // lanes per row: the smallest power of two covering the row's 16-byte chunks
     p->cpr = d.head_dim * p->esz_dst / 16;
@@ -208,7 +224,7 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
     p->parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
     p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp - 1) / rpp);
-    if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * p->num_read_shards,
+    if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * int64_t(p->segs.size()),
                                         p->parts_unpack) > kvx::kMaxUnits) {
         delete p;
         return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers x parts)",
@@ -374,11 +390,11 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     }
     if (mode != kvx::kUnpack) {
         if (!shards) return fail(KVX_EINVAL, "NULL src_shards array");
-        for (int k = 0; k < p->num_read_shards; ++k) {
-            const void* s = shards[p->first_shard + k];
-            if (!s) return fail(KVX_EINVAL, "src_shards[%d] is NULL", p->first_shard + k);
-            if (!aligned16(s))
-                return fail(KVX_EINVAL, "src_shards[%d] is not 16-byte aligned", p->first_shard + k);
+        for (size_t k = 0; k < p->read_shards.size(); ++k) {
+            const int j = p->read_shards[k];
+            const void* s = shards[j];
+            if (!s) return fail(KVX_EINVAL, "src_shards[%d] is NULL", j);
+            if (!aligned16(s)) return fail(KVX_EINVAL, "src_shards[%d] is not 16-byte aligned", j);
             a.src[k] = s;
         }
     } else {

@@ -81,6 +81,7 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
 @pytest.mark.parametrize("over,status", [
     (dict(num_layers=0), K.EINVAL), (dict(num_kv_heads=0), K.EINVAL), (dict(head_dim=-64), K.EINVAL),
     (dict(src_tp=3), K.EINVAL), (dict(dst_tp=3), K.EINVAL), (dict(dst_rank=2), K.EINVAL),
+    (dict(src_tp=16, dst_tp=16, dst_rank=16), K.EINVAL),
     (dict(dst_rank=-1), K.EINVAL), (dict(block_size=0), K.EINVAL), (dict(num_blocks=0), K.EINVAL),
     (dict(seq_lens=[4, -1]), K.EINVAL), (dict(src_order=3), K.EINVAL),
     (dict(src_order=2), K.EINVAL),                      # paged without a page size
@@ -88,7 +89,8 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(src_order=2, src_block_size=0, src_num_blocks=8), K.EINVAL),
     (dict(head_dim=4), K.EINVAL),                       # 8-byte rows
     (dict(head_dim=8, dst_dtype=3), K.EINVAL),          # 8-byte e4m3 rows
-    (dict(src_dtype=3), K.EUNSUPPORTED), (dict(src_dtype=2, dst_dtype=1), K.EUNSUPPORTED),
+    (dict(src_dtype=3), K.EUNSUPPORTED), (dict(src_dtype=3, dst_dtype=1), K.EUNSUPPORTED),
+    (dict(num_kv_heads=4, dst_tp=6), K.EINVAL), (dict(num_kv_heads=4, src_tp=6), K.EINVAL),
     (dict(dst_dtype=9), K.EINVAL), (dict(head_dim=1024), K.EUNSUPPORTED),
     (dict(num_kv_heads=4096, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
 ])

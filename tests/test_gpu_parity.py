@@ -140,6 +140,15 @@ def test_fp16_to_bf16_every_pattern():
     assert _eq(cache.cpu().numpy(), want)
 
 
+def test_bf16_to_fp16_every_pattern():
+    rows = np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(512, 128)
+    w, lens, bt, shards = _sweep_case("bf16", "fp16", rows)
+    log("bf16->fp16 all 65536 patterns")
+    cache, _, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
+    want, _ = oracle_pool(w, lens, bt, bt.shape[1], shards)
+    assert _eq(cache.cpu().numpy(), want)
+
+
 def _e4m3_rows(fmt, amaxes, rng):
     """Rows [amax, x_1..x_127] covering every finite pattern x with |x| <= amax
     (both signs) for each amax, plus NaN/Inf/zero rows."""
@@ -231,6 +240,14 @@ def test_full_qwen7b_htd():
 
 def test_full_tiny():
     _full_case("tiny_tp1to2_fp16_bf16")
+
+
+def test_full_qwen7b_gqa_replicated_tp8():
+    _full_case("qwen7b_gqa_tp1to8_r5_fp16_bf16_bs64")
+
+
+def test_full_llama3_8b_bf16_to_fp16():
+    _full_case("llama3_8b_bf16_fp16_bs16")
 
 
 @pytest.mark.parametrize("group", [0, 15])

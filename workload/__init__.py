@@ -178,6 +178,15 @@ WORKLOADS = {
         # one decode cache: one plan per stage
         Workload("llama3_8b_pp2to1_bf16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "bf16", "thd",
                  16, 65536, 16, 512, 4096, seed=17543, src_pp=2),
+        # the Qwen-7B-style GQA workload (4 KV heads, same seed and values) into
+        # a decode side with tensor parallelism 8: rank 5 holds a replica of
+        # KV head 2; 16 KiB pages of one head
+        Workload("qwen7b_gqa_tp1to8_r5_fp16_bf16_bs64", 28, 28, 4, 128, 1, 8, 5, "fp16", "bf16",
+                 "htd", 64, 8192, 32, 128, 2048, seed=17545, sigma=2.0, outlier_frac=0.001,
+                 outlier_value=60000.0),
+        # the Llama-3-8B workload (same seed and values) cast bf16 -> fp16
+        Workload("llama3_8b_bf16_fp16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "fp16", "thd",
+                 16, 65536, 16, 512, 4096, seed=17543),
     ]
 }
 
