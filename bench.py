@@ -63,6 +63,9 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="time the repack only (no pack/unpack/latency legs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--stream-chunk", type=int, default=4,
+                    help="layers per chunk of the layer-streamed transfer leg (0 = skip it)")
+    ap.add_argument("--stream-slots", type=int, default=3)
     ap.add_argument("--calib-gib", type=float, default=2.0,
                     help="bytes read (= bytes written) by the plain copies timed as ceilings "
                          "and as the reference of the rocprofv3 byte counters; 0 = skip")
@@ -252,10 +255,62 @@ def main():
             "note": "single-request plan, host call to event completion, median of 5"}
         log(f"latency p50 {out['latency_ms_per_request']['p50']} ms")
 
+    if not args.no_extras and args.stream_chunk > 0 and len(stages) == 1:
+        out["layer_stream"] = stream_leg(K, torch, plans[0], infos[0], stage_dshards[0], sbt_d,
+                                         sstride, cache, scales, bt_d, stride, stream,
+                                         min(args.stream_chunk, w.layers), args.stream_slots,
+                                         timed)
+
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lens, stage_shards[0], args.cpu_seconds, value, sbt,
                                            stages[0])
     print(json.dumps(out), flush=True)
+
+
+def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream,
+               chunk, slots, timed):
+    """The layer-streamed transfer through pinned host memory (kvx_pipe_run),
+    against the same bytes moved serially (pack everything, copy it to pinned
+    host memory, copy it back, unpack everything) and against plain copies of
+    the transfer tensor in each direction.  Rates are transfer-tensor bytes
+    per direction per second: this leg is bound by the host link, not HBM."""
+    pipe = K.kvx_pipe_create(plan, chunk, slots)
+    pinfo = K.kvx_pipe_info_get(pipe)
+    nbytes = int(pinfo.bus_bytes)
+
+    def piped():
+        K.kvx_pipe_run(pipe, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream)
+
+    wire = torch.empty(int(info.wire_bytes), dtype=torch.uint8, device="cuda")
+    back = torch.empty_like(wire)
+    host = torch.empty(int(info.wire_bytes), dtype=torch.uint8, pin_memory=True)
+
+    def pack():
+        if sbt_d is not None:
+            K.kvx_pack_paged(plan, dshards, sbt_d, sstride, wire, stream)
+        else:
+            K.kvx_pack(plan, dshards, wire, stream)
+
+    def serial():
+        pack()
+        host.copy_(wire, non_blocking=True)
+        back.copy_(host, non_blocking=True)
+        K.kvx_unpack(plan, back, cache, scales, bt_d, stride, stream)
+
+    res = {"chunk_layers": chunk, "slots": slots, "chunks": int(pinfo.num_chunks),
+           "bytes_each_way": nbytes, "pinned_host_bytes": int(pinfo.host_bytes)}
+    for name, fn, steps in (("pipe", piped, 5), ("serial", serial, 3),
+                            ("d2h_copy", lambda: host.copy_(wire, non_blocking=True), 3),
+                            ("h2d_copy", lambda: back.copy_(host, non_blocking=True), 3)):
+        ms, _, _, _ = timed(fn, steps, 1)
+        res[name + "_ms"] = round(ms, 3)
+        log(f"layer stream leg: {name} {ms:.2f} ms ({nbytes / (ms * 1e-3) / 1e9:.1f} GB/s each way)")
+    res["pipe_GB/s_each_way"] = round(nbytes / (res["pipe_ms"] * 1e-3) / 1e9, 2)
+    res["serial_over_pipe"] = round(res["serial_ms"] / res["pipe_ms"], 3)
+    res["note"] = ("layer chunks packed, copied to pinned host memory and back, unpacked; "
+                   "host-link bound, not an HBM figure")
+    del pipe, wire, back, host
+    return res
 
 
 CALIB_TOKENS_PER_GIB = 1 << 18   # 1 layer, 8 heads, dim 128, bf16: 2 x 8 x 256 B per token

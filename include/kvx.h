@@ -72,7 +72,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 3
+#define KVX_ABI_VERSION 4
 
 typedef enum {
     KVX_OK = 0,
@@ -236,6 +236,55 @@ kvx_status kvx_check_block_table(const kvx_plan_t *plan, const int32_t *host_blo
  * Pages shared between requests are allowed.  KVX_EINVAL otherwise. */
 kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host_src_block_table,
                                      int32_t src_bt_stride);
+
+/* ---- layer-streamed transfer through pinned host memory ----
+ *
+ * The transfer of Sec. III-B-1 moves the KV cache through a pinned host
+ * memory pool, and the paper's conclusion names by-layer transmission as the
+ * next step.  A pipe moves a plan's layers in chunks of chunk_layers layers:
+ * each chunk is packed into a device send slot (on the caller's stream),
+ * copied to a slot of a pinned host ring (device to host), copied into a
+ * device receive slot (host to device) and unpacked into the cache (on a
+ * stream of the pipe).  With `slots` slots per stage, chunk c + 1 is packed
+ * and chunk c - 1 unpacked while chunk c crosses the bus.  The cache and
+ * scales written equal kvx_pack followed by kvx_unpack of the whole plan.
+ *
+ * kvx_pipe_create allocates the pinned host ring (slots x the largest
+ * chunk's transfer-tensor bytes, with hipHostMalloc), device send and
+ * receive slots of the same size, two copy streams, one unpack stream and
+ * their events (all default priority), on the plan's device.  The plan must
+ * outlive the pipe.  KVX_EINVAL for a NULL plan or out, chunk_layers outside
+ * [1, num_layers] or slots < 1; KVX_EDEVICE for a host-only plan;
+ * KVX_ENOMEM if an allocation fails.
+ *
+ * kvx_pipe_run enqueues the whole transfer and returns; the caller's stream
+ * then waits for the last unpack.  Arguments as kvx_repack (kvx_repack_paged
+ * for a paged plan, whose source block table is passed; otherwise it must be
+ * NULL).  Two runs of one pipe must not overlap (they share the slots);
+ * runs of different pipes may. */
+typedef struct kvx_pipe_s kvx_pipe_t; /* opaque, library-owned */
+
+typedef struct {
+    int32_t chunk_layers;      /* layers per chunk (the last chunk may hold fewer) */
+    int32_t num_chunks;
+    int32_t slots;
+    int32_t reserved;
+    uint64_t slot_bytes;       /* transfer-tensor bytes of the largest chunk */
+    uint64_t host_bytes;       /* pinned host ring: slots x slot_bytes */
+    uint64_t device_bytes;     /* send + receive slots: 2 x slots x slot_bytes */
+    uint64_t bus_bytes;        /* bytes each direction moves per run: the plan's wire bytes, by chunk */
+} kvx_pipe_info;
+
+kvx_status kvx_pipe_create(const kvx_plan_t *plan, int32_t chunk_layers, int32_t slots,
+                           kvx_pipe_t **out);
+kvx_status kvx_pipe_info_get(const kvx_pipe_t *pipe, kvx_pipe_info *info);
+kvx_status kvx_pipe_run(kvx_pipe_t *pipe, const void *const *src_shards,
+                        const int32_t *src_block_table, int32_t src_bt_stride, void *cache,
+                        float *scales, const int32_t *block_table, int32_t bt_stride,
+                        void *hip_stream);
+/* Waits for the pipe's streams, then frees everything it allocated.  NULL is
+ * accepted. */
+kvx_status kvx_pipe_destroy(kvx_pipe_t *pipe);
 
 /* Message for the calling thread's last non-OK status ("" if none). */
 const char *kvx_last_error(void);

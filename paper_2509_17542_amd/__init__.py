@@ -62,6 +62,15 @@ class kvx_plan_info(ctypes.Structure):
     ]
 
 
+class kvx_pipe_info(ctypes.Structure):
+    _fields_ = [
+        ("chunk_layers", ctypes.c_int32), ("num_chunks", ctypes.c_int32),
+        ("slots", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("slot_bytes", ctypes.c_uint64), ("host_bytes", ctypes.c_uint64),
+        ("device_bytes", ctypes.c_uint64), ("bus_bytes", ctypes.c_uint64),
+    ]
+
+
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
 _lib.kvx_plan.restype = ctypes.c_int
@@ -87,6 +96,14 @@ _lib.kvx_check_block_table.restype = ctypes.c_int
 _lib.kvx_check_block_table.argtypes = [_vp, _vp, _i32]
 _lib.kvx_check_src_block_table.restype = ctypes.c_int
 _lib.kvx_check_src_block_table.argtypes = [_vp, _vp, _i32]
+_lib.kvx_pipe_create.restype = ctypes.c_int
+_lib.kvx_pipe_create.argtypes = [_vp, _i32, _i32, ctypes.POINTER(_vp)]
+_lib.kvx_pipe_info_get.restype = ctypes.c_int
+_lib.kvx_pipe_info_get.argtypes = [_vp, ctypes.POINTER(kvx_pipe_info)]
+_lib.kvx_pipe_run.restype = ctypes.c_int
+_lib.kvx_pipe_run.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp]
+_lib.kvx_pipe_destroy.restype = ctypes.c_int
+_lib.kvx_pipe_destroy.argtypes = [_vp]
 _lib.kvx_last_error.restype = ctypes.c_char_p
 _lib.kvx_last_error.argtypes = []
 _lib.kvx_abi_version.restype = ctypes.c_int32
@@ -94,7 +111,8 @@ _lib.kvx_abi_version.argtypes = []
 
 EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_destroy", "kvx_pack",
            "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged",
-           "kvx_check_block_table", "kvx_check_src_block_table", "kvx_last_error",
+           "kvx_check_block_table", "kvx_check_src_block_table", "kvx_pipe_create",
+           "kvx_pipe_info_get", "kvx_pipe_run", "kvx_pipe_destroy", "kvx_last_error",
            "kvx_abi_version")
 
 
@@ -127,6 +145,26 @@ class Plan:
 
     def __init__(self, handle: int):
         self.handle = handle
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h:
+            self._destroy(h)
+
+    @property
+    def _as_parameter_(self):
+        return ctypes.c_void_p(self.handle)
+
+
+class Pipe:
+    """Owns a kvx_pipe_t*; destroyed with kvx_pipe_destroy.  Keeps its plan
+    alive."""
+
+    _destroy = _lib.kvx_pipe_destroy
+
+    def __init__(self, handle: int, plan: "Plan"):
+        self.handle = handle
+        self.plan = plan
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
@@ -242,3 +280,27 @@ def kvx_last_error() -> str:
 
 def kvx_abi_version() -> int:
     return int(_lib.kvx_abi_version())
+
+
+def kvx_pipe_create(plan: Plan, chunk_layers: int, slots: int) -> Pipe:
+    h = _vp()
+    _check(_lib.kvx_pipe_create(plan, chunk_layers, slots, ctypes.byref(h)))
+    return Pipe(h.value, plan)
+
+
+def kvx_pipe_info_get(pipe: Pipe) -> kvx_pipe_info:
+    info = kvx_pipe_info()
+    _check(_lib.kvx_pipe_info_get(pipe, ctypes.byref(info)))
+    return info
+
+
+def kvx_pipe_run(pipe: Pipe, src_shards, src_block_table, src_bt_stride: int, cache, scales,
+                 block_table, bt_stride: int, stream=None) -> None:
+    _check(_lib.kvx_pipe_run(pipe, _shard_array(src_shards), _addr(src_block_table),
+                             src_bt_stride, _addr(cache), _addr(scales), _addr(block_table),
+                             bt_stride, _stream(stream)))
+
+
+def kvx_pipe_destroy(pipe: Pipe) -> None:
+    h, pipe.handle = pipe.handle, None
+    _check(_lib.kvx_pipe_destroy(h))

@@ -1,0 +1,45 @@
+// Host-side internals shared by the planner (kvx_plan.cpp) and the
+// layer-streamed transfer (kvx_pipe.cpp): the plan object, the error setter
+// and a launch with shifted layer offsets.  Not part of the C ABI.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "kvx.h"
+#include "kvx_internal.h"
+
+struct kvx_plan_s {
+    kvx_desc d;                   // seq_lens points into lens
+    std::vector<int32_t> lens;
+    std::vector<int64_t> wire_data, wire_scale;  // per request, transfer-tensor offsets
+    std::vector<kvx::Item> items;
+    int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
+    std::vector<int> read_shards;  // prefill shards the decode rank reads, in slot order
+    int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
+    std::vector<kvx::Segment> segs;  // head segments of the decode rank
+    int32_t max_blocks = 0;
+    int32_t max_src_blocks = 0;   // paged sources: pages per request on the prefill side
+    uint64_t wire_bytes = 0;
+    int64_t total_tokens = 0;
+    int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
+    int device = -1;
+    void* dev_table = nullptr;    // device copy of items
+    const kvx::Item* dev_items = nullptr;
+};
+
+namespace kvx {
+
+// Sets the calling thread's last-error message; returns s.
+kvx_status fail(kvx_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+// One pack / unpack / repack launch of plan p with both sides' layer offsets
+// moved by layer_shift layers (the layers of a chunk of a larger plan); the
+// argument checks of the public calls apply.  The source is paged exactly
+// when the plan's is.
+kvx_status launch_shifted(const kvx_plan_t* p, int mode, int layer_shift,
+                          const void* const* shards, const int32_t* sbt, int32_t sbt_stride,
+                          const void* wire, void* dst, float* scales, const int32_t* bt,
+                          int32_t bt_stride, void* stream);
+
+}  // namespace kvx

@@ -1,0 +1,219 @@
+// Layer-streamed transfer through a pinned host ring: the plan's layers move
+// in chunks, each packed into a device send slot, copied to a slot of pinned
+// host memory and back into a device receive slot, and unpacked, with the
+// stages of consecutive chunks overlapped on four streams.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "kvx.h"
+#include "kvx_host.h"
+#include "kvx_internal.h"
+
+struct kvx_pipe_s {
+    const kvx_plan_t* plan = nullptr;
+    int chunk_layers = 0, num_chunks = 0, slots = 0, device = -1;
+    kvx_plan_t* full = nullptr;   // plan of chunk_layers layers
+    kvx_plan_t* tail = nullptr;   // plan of the last, shorter chunk (or none)
+    uint64_t slot_bytes = 0, bus_bytes = 0;
+    char* host = nullptr;         // pinned ring, slots x slot_bytes
+    char* send = nullptr;         // device, slots x slot_bytes
+    char* recv = nullptr;         // device, slots x slot_bytes
+    hipStream_t d2h = nullptr, h2d = nullptr, unpack = nullptr;
+    hipEvent_t start = nullptr;
+    std::vector<hipEvent_t> packed, sent, received, unpacked;  // one per slot
+};
+
+namespace {
+
+using kvx::fail;
+
+void release(kvx_pipe_s* q)
+{
+    if (!q) return;
+    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+        if (s) (void)hipStreamSynchronize(s);
+    for (auto* v : {&q->packed, &q->sent, &q->received, &q->unpacked})
+        for (hipEvent_t e : *v)
+            if (e) (void)hipEventDestroy(e);
+    if (q->start) (void)hipEventDestroy(q->start);
+    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+        if (s) (void)hipStreamDestroy(s);
+    if (q->host) (void)hipHostFree(q->host);
+    if (q->send) (void)hipFree(q->send);
+    if (q->recv) (void)hipFree(q->recv);
+    kvx_plan_destroy(q->full);
+    kvx_plan_destroy(q->tail);
+    delete q;
+}
+
+// Plan of n layers starting where the parent plan's layers start; its launches
+// are shifted to the chunk's first layer.
+kvx_status chunk_plan(const kvx_plan_t* p, int n, kvx_plan_t** out)
+{
+    kvx_desc d = p->d;
+    d.src_layers = d.src_layers ? d.src_layers : d.num_layers;
+    d.dst_layers = d.dst_layers ? d.dst_layers : d.num_layers;
+    d.num_layers = n;
+    return kvx_plan(&d, out);
+}
+
+bool ok(hipError_t e) { return e == hipSuccess; }
+
+}  // namespace
+
+extern "C" {
+
+kvx_status kvx_pipe_create(const kvx_plan_t* p, int32_t chunk_layers, int32_t slots,
+                           kvx_pipe_t** out)
+{
+    if (!p || !out) return fail(KVX_EINVAL, "NULL plan or out");
+    *out = nullptr;
+    const int L = p->d.num_layers;
+    if (chunk_layers < 1 || chunk_layers > L)
+        return fail(KVX_EINVAL, "chunk_layers %d outside [1, %d]", chunk_layers, L);
+    if (slots < 1) return fail(KVX_EINVAL, "slots must be >= 1");
+    if (p->device < 0) return fail(KVX_EDEVICE, "plan has no device tables (no HIP device)");
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != p->device)
+        return fail(KVX_EDEVICE, "current device %d is not the plan's device %d", cur, p->device);
+
+    kvx_pipe_s* q = new (std::nothrow) kvx_pipe_s();
+    if (!q) return fail(KVX_ENOMEM, "host allocation failed");
+    q->plan = p;
+    q->chunk_layers = chunk_layers;
+    q->num_chunks = (L + chunk_layers - 1) / chunk_layers;
+    q->slots = slots;
+    q->device = p->device;
+    kvx_status st = chunk_plan(p, chunk_layers, &q->full);
+    if (st == KVX_OK && L % chunk_layers) st = chunk_plan(p, L % chunk_layers, &q->tail);
+    if (st != KVX_OK) {
+        release(q);
+        return st;
+    }
+    q->slot_bytes = q->full->wire_bytes;
+    q->bus_bytes = uint64_t(L / chunk_layers) * q->full->wire_bytes +
+                   (q->tail ? q->tail->wire_bytes : 0);
+    const size_t ring = size_t(q->slot_bytes) * size_t(slots);
+    if (ring) {
+        if (!ok(hipHostMalloc(reinterpret_cast<void**>(&q->host), ring, hipHostMallocDefault)) ||
+            !ok(hipMalloc(reinterpret_cast<void**>(&q->send), ring)) ||
+            !ok(hipMalloc(reinterpret_cast<void**>(&q->recv), ring))) {
+            (void)hipGetLastError();
+            release(q);
+            return fail(KVX_ENOMEM, "pipe buffers (3 x %zu bytes) could not be allocated", ring);
+        }
+    }
+    bool good = ok(hipStreamCreateWithFlags(&q->d2h, hipStreamNonBlocking)) &&
+                ok(hipStreamCreateWithFlags(&q->h2d, hipStreamNonBlocking)) &&
+                ok(hipStreamCreateWithFlags(&q->unpack, hipStreamNonBlocking)) &&
+                ok(hipEventCreateWithFlags(&q->start, hipEventDisableTiming));
+    for (auto* v : {&q->packed, &q->sent, &q->received, &q->unpacked}) {
+        v->assign(size_t(slots), nullptr);
+        for (hipEvent_t& e : *v) good = good && ok(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    }
+    if (!good) {
+        (void)hipGetLastError();
+        release(q);
+        return fail(KVX_EDEVICE, "pipe streams or events could not be created");
+    }
+    *out = q;
+    return KVX_OK;
+}
+
+kvx_status kvx_pipe_info_get(const kvx_pipe_t* q, kvx_pipe_info* info)
+{
+    if (!q || !info) return fail(KVX_EINVAL, "NULL pipe or info");
+    std::memset(info, 0, sizeof *info);
+    info->chunk_layers = q->chunk_layers;
+    info->num_chunks = q->num_chunks;
+    info->slots = q->slots;
+    info->slot_bytes = q->slot_bytes;
+    info->host_bytes = q->slot_bytes * uint64_t(q->slots);
+    info->device_bytes = 2 * info->host_bytes;
+    info->bus_bytes = q->bus_bytes;
+    return KVX_OK;
+}
+
+kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t* sbt,
+                        int32_t sbt_stride, void* cache, float* scales, const int32_t* bt,
+                        int32_t bt_stride, void* stream)
+{
+    if (!q) return fail(KVX_EINVAL, "NULL pipe");
+    const bool paged = q->plan->d.src_order == KVX_PAGED;
+    if (!paged && sbt) return fail(KVX_EINVAL, "source block table given for a contiguous source");
+    if (q->plan->items.empty()) return KVX_OK;
+    // the checks of the unpack side up front, so that a bad argument is
+    // reported before anything is enqueued (the pack side's are the first
+    // chunk's pack, which runs first)
+    const bool fp8 = q->plan->d.dst_dtype == KVX_FP8_E4M3FN;
+    if (!cache || (reinterpret_cast<uintptr_t>(cache) & 15u))
+        return fail(KVX_EINVAL, "NULL or misaligned cache");
+    if (fp8 != (scales != nullptr) || (reinterpret_cast<uintptr_t>(scales) & 15u))
+        return fail(KVX_EINVAL, "scales must be given, 16-byte aligned, exactly for e4m3fn");
+    if (!bt || bt_stride < q->plan->max_blocks)
+        return fail(KVX_EINVAL, "NULL block table or bt_stride below %d", q->plan->max_blocks);
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != q->device)
+        return fail(KVX_EDEVICE, "current device %d is not the pipe's device %d", cur, q->device);
+    hipStream_t s0 = static_cast<hipStream_t>(stream);
+
+    // the pipe's streams start after the caller's earlier work
+    if (!ok(hipEventRecord(q->start, s0))) return fail(KVX_EDEVICE, "event record failed");
+    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+        if (!ok(hipStreamWaitEvent(s, q->start, 0))) return fail(KVX_EDEVICE, "stream wait failed");
+
+    for (int c = 0; c < q->num_chunks; ++c) {
+        const int s = c % q->slots;
+        const bool reuse = c >= q->slots;  // slot s held chunk c - slots
+        const kvx_plan_t* cp = (q->tail && c == q->num_chunks - 1) ? q->tail : q->full;
+        const int shift = c * q->chunk_layers;
+        const size_t bytes = size_t(cp->wire_bytes);
+        char* send = q->send + size_t(s) * q->slot_bytes;
+        char* host = q->host + size_t(s) * q->slot_bytes;
+        char* recv = q->recv + size_t(s) * q->slot_bytes;
+
+        // pack (caller's stream): the send slot must have left for the host
+        if (reuse && !ok(hipStreamWaitEvent(s0, q->sent[s], 0)))
+            return fail(KVX_EDEVICE, "stream wait failed");
+        kvx_status st = kvx::launch_shifted(cp, kvx::kPack, shift, shards, sbt, sbt_stride,
+                                            nullptr, send, nullptr, nullptr, 0, stream);
+        if (st != KVX_OK) return st;
+        bool good = ok(hipEventRecord(q->packed[s], s0));
+        // device -> host: the host slot must have been read back
+        good = good && ok(hipStreamWaitEvent(q->d2h, q->packed[s], 0));
+        if (reuse) good = good && ok(hipStreamWaitEvent(q->d2h, q->received[s], 0));
+        good = good && ok(hipMemcpyAsync(host, send, bytes, hipMemcpyDeviceToHost, q->d2h)) &&
+               ok(hipEventRecord(q->sent[s], q->d2h));
+        // host -> device: the receive slot must have been unpacked
+        good = good && ok(hipStreamWaitEvent(q->h2d, q->sent[s], 0));
+        if (reuse) good = good && ok(hipStreamWaitEvent(q->h2d, q->unpacked[s], 0));
+        good = good && ok(hipMemcpyAsync(recv, host, bytes, hipMemcpyHostToDevice, q->h2d)) &&
+               ok(hipEventRecord(q->received[s], q->h2d));
+        // unpack (pipe's stream)
+        good = good && ok(hipStreamWaitEvent(q->unpack, q->received[s], 0));
+        if (!good) return fail(KVX_EDEVICE, "copy or event enqueue failed: %s",
+                               hipGetErrorString(hipGetLastError()));
+        st = kvx::launch_shifted(cp, kvx::kUnpack, shift, nullptr, nullptr, 0, recv, cache,
+                                 scales, bt, bt_stride, q->unpack);
+        if (st != KVX_OK) return st;
+        if (!ok(hipEventRecord(q->unpacked[s], q->unpack)))
+            return fail(KVX_EDEVICE, "event record failed");
+    }
+    // the caller's stream continues after the last unpack (the unpack stream
+    // runs its chunks in order)
+    const int last = (q->num_chunks - 1) % q->slots;
+    if (!ok(hipStreamWaitEvent(s0, q->unpacked[last], 0))) return fail(KVX_EDEVICE, "stream wait failed");
+    return KVX_OK;
+}
+
+kvx_status kvx_pipe_destroy(kvx_pipe_t* q)
+{
+    release(q);
+    return KVX_OK;
+}
+
+}  // extern "C"

@@ -12,35 +12,17 @@
 #include <vector>
 
 #include "kvx.h"
+#include "kvx_host.h"
 #include "kvx_internal.h"
 
 using kvx::Item;
 
-struct kvx_plan_s {
-    kvx_desc d;                   // seq_lens points into lens
-    std::vector<int32_t> lens;
-    std::vector<int64_t> wire_data, wire_scale;  // per request, transfer-tensor offsets
-    std::vector<Item> items;
-    int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
-    std::vector<int> read_shards;  // prefill shards the decode rank reads, in slot order
-    int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
-    std::vector<kvx::Segment> segs;  // head runs of the decode rank, one per shard read
-    int32_t max_blocks = 0;
-    int32_t max_src_blocks = 0;   // paged sources: pages per request on the prefill side
-    uint64_t wire_bytes = 0;
-    int64_t total_tokens = 0;
-    int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
-    int device = -1;
-    void* dev_table = nullptr;    // device copy of items
-    const Item* dev_items = nullptr;
-};
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
 
-kvx_status fail(kvx_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-kvx_status fail(kvx_status s, const char* fmt, ...)
+kvx_status kvx::fail(kvx_status s, const char* fmt, ...)
 {
     char buf[512];
     va_list ap;
@@ -50,6 +32,10 @@ kvx_status fail(kvx_status s, const char* fmt, ...)
     g_last_error = buf;
     return s;
 }
+
+namespace {
+
+using kvx::fail;
 
 int dtype_size(int dt) { return dt == KVX_FP8_E4M3FN ? 1 : 2; }
 
@@ -372,7 +358,8 @@ int conv_for(const kvx_plan_t* p, int mode)
 // the plan's source order (the unpack reads no source and takes either).
 kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* const* shards,
                    const int32_t* sbt, int32_t sbt_stride, const void* wire, void* dst,
-                   float* scales, const int32_t* bt, int32_t bt_stride, kvx::KArgs& a)
+                   float* scales, const int32_t* bt, int32_t bt_stride, kvx::KArgs& a,
+                   int layer_shift = 0)
 {
     if (!p) return fail(KVX_EINVAL, "NULL plan");
     const bool fp8 = p->d.dst_dtype == KVX_FP8_E4M3FN;
@@ -426,8 +413,8 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     a.bt = bt;
     a.num_items = uint32_t(p->items.size());
     a.planes = uint32_t(2 * d.num_layers);
-    a.src_plane0 = uint32_t(2 * d.src_layer_offset);
-    a.dst_plane0 = uint32_t(2 * d.dst_layer_offset);
+    a.src_plane0 = uint32_t(2 * (d.src_layer_offset + layer_shift));
+    a.dst_plane0 = uint32_t(2 * (d.dst_layer_offset + layer_shift));
     if (mode == kvx::kUnpack) {  // transfer-tensor rows are already in decode order
         a.num_segs = 1;
         a.parts = uint32_t(p->parts_unpack);
@@ -485,6 +472,18 @@ kvx_status run(const kvx_plan_t* p, int mode, const kvx::KArgs& a, void* stream)
 }
 
 }  // namespace
+
+kvx_status kvx::launch_shifted(const kvx_plan_t* p, int mode, int layer_shift,
+                               const void* const* shards, const int32_t* sbt, int32_t sbt_stride,
+                               const void* wire, void* dst, float* scales, const int32_t* bt,
+                               int32_t bt_stride, void* stream)
+{
+    kvx::KArgs a;
+    const bool paged = p && p->d.src_order == KVX_PAGED;
+    kvx_status st = prepare(p, mode, paged, shards, sbt, sbt_stride, wire, dst, scales, bt,
+                            bt_stride, a, layer_shift);
+    return st != KVX_OK ? st : run(p, mode, a, stream);
+}
 
 extern "C" {
 

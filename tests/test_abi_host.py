@@ -26,11 +26,11 @@ def declared_entry_points():
 
 def test_every_declared_symbol_is_exported():
     names = declared_entry_points()
-    assert len(names) == 13, names
+    assert len(names) == 17, names
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 3
+    assert K.kvx_abi_version() == 4
 
 
 def desc_for(w, lens, **over):
@@ -257,3 +257,17 @@ def test_plan_accepts_a_layer_range():
     a, b = K.kvx_plan_info_get(stage), K.kvx_plan_info_get(whole)
     assert (a.read_bytes_repack, a.write_bytes_repack, a.wire_bytes) == \
         (b.read_bytes_repack, b.write_bytes_repack, b.wire_bytes)
+
+
+def test_pipe_create_errors_on_the_host():
+    """A host-only plan (no device here) cannot get a pipe; bad chunk sizes
+    and slot counts are rejected first."""
+    plan = K.kvx_plan(K.make_desc(**BASE))
+    for chunk, slots, status in ((0, 2, K.EINVAL), (3, 2, K.EINVAL), (1, 0, K.EINVAL)):
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_pipe_create(plan, chunk, slots)
+        assert e.value.status == status, K.kvx_last_error()
+    if K.kvx_plan_info_get(plan).device < 0:
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_pipe_create(plan, 1, 2)
+        assert e.value.status == K.EDEVICE

@@ -1,0 +1,90 @@
+"""GPU parity of the layer-streamed transfer (kvx_pipe_*): chunks of layers
+packed, copied through a pinned host ring and unpacked, against the oracle's
+whole-plan conversion, byte for byte (whole pools for the small cases, sampled
+pages for the full Llama-3-8B workload).  Chunk sizes that do and do not
+divide the layer count, one to three slots, two runs in a row on one pipe."""
+import numpy as np
+import pytest
+import torch
+
+from cases import FULL, SMALL, SMALL_PAGED, dst_size, inputs
+from gpu_util import (DEV, check_sampled, check_shapes, check_unused_pages, desc_for, dev_u16, log,
+                      oracle_pool, pool)
+
+import workload as W
+
+import paper_2509_17542_amd as K
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+@pytest.fixture(autouse=True)
+def _release_device_memory():
+    yield
+    import gc
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _pipe_run(w, lens, bt, stride, shards, chunk, slots, runs=1):
+    plan = K.kvx_plan(desc_for(w, lens))
+    pipe = K.kvx_pipe_create(plan, chunk, slots)
+    info = K.kvx_pipe_info_get(pipe)
+    assert info.num_chunks == -(-w.layers // chunk) and info.host_bytes == slots * info.slot_bytes
+    dsh = [dev_u16(s) for s in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    sbt = sbt_d = None
+    sstride = 0
+    if w.src_order == "paged":
+        sbt, sstride = W.src_block_table(w, lens)
+        sbt_d = torch.from_numpy(sbt).to(DEV)
+    check_shapes(w, lens, bt, stride, dsh, w.layers, sbt)
+    out = []
+    for _ in range(runs):
+        cache, scales = pool(w, w.layers)
+        K.kvx_pipe_run(pipe, dsh, sbt_d, sstride, cache, scales, bt_d, stride)
+        torch.cuda.synchronize()
+        out.append((cache, scales))
+    del pipe
+    return out
+
+
+CASES = [("llama3_8b_small", 1, 1), ("fp8_small", 1, 2), ("qwen_htd_small", 2, 3),
+         ("llama3_70b_small_r1", 1, 3), ("fp16_e4m3_htd_empty", 1, 1),
+         ("paged16_tp4to2_bs32_small", 1, 2), ("paged16_e4m3_bs24", 2, 1),
+         ("gqa_src_rep_tp8to2_r1", 2, 2), ("bf16_fp16_overflow", 1, 2)]
+
+
+@pytest.mark.parametrize("name,chunk,slots", CASES)
+def test_pipe_small(name, chunk, slots):
+    w = (SMALL | SMALL_PAGED)[name]
+    lens, bt, stride, shards = inputs(w)
+    log(f"pipe {name}: chunk {chunk} of {w.layers} layers, {slots} slots")
+    want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
+    for cache, scales in _pipe_run(w, lens, bt, stride, shards, chunk, slots, runs=2):
+        assert np.array_equal(cache.cpu().numpy(), want_c)
+        if want_s is not None:
+            assert np.array_equal(scales.cpu().numpy().view(np.uint32), want_s.view(np.uint32))
+
+
+@pytest.mark.parametrize("chunk,slots", [(1, 2), (2, 3), (3, 2), (5, 1)])
+def test_pipe_chunkings_of_five_layers(chunk, slots):
+    w = SMALL["llama3_70b_small_r0"].replace(layers=5, total_layers=5)
+    lens, bt, stride, shards = inputs(w)
+    log(f"pipe 5 layers: chunk {chunk}, {slots} slots")
+    want_c, _ = oracle_pool(w, lens, bt, stride, shards)
+    (cache, _), = _pipe_run(w, lens, bt, stride, shards, chunk, slots)
+    assert np.array_equal(cache.cpu().numpy(), want_c)
+
+
+def test_pipe_full_llama3_8b():
+    w = FULL["llama3_8b_bf16_bs16"]
+    rng = np.random.default_rng(5)
+    lens, bt, stride, shards = inputs(w)
+    log("pipe full 8B: chunks of 4 layers, 3 slots")
+    (cache, _), = _pipe_run(w, lens, bt, stride, shards, 4, 3)
+    planes = [(0, 0), (3, 1), (4, 0), (31, 1), (17, 0)]
+    n = check_sampled(w, lens, bt, shards, cache, None, w.layers, planes, range(len(lens)), rng)
+    check_unused_pages(w, lens, bt, cache, w.layers, rng)
+    log(f"pipe full 8B: {n} rows checked")
