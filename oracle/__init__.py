@@ -56,6 +56,7 @@ def lib():
         L.orc_row_scale.argtypes = [vp, ctypes.c_int]
         L.orc_fp16_to_bf16_n.argtypes = [vp, vp, ctypes.c_int64]
         L.orc_bf16_to_fp16_n.argtypes = [vp, vp, ctypes.c_int64]
+        L.orc_dequant_row.argtypes = [ctypes.c_int, ctypes.c_int, vp, ctypes.c_float, vp]
         L.orc_src_heads.restype = ctypes.c_int32
         L.orc_src_heads.argtypes = [P(Problem)]
         L.orc_dst_heads.restype = ctypes.c_int32
@@ -99,6 +100,7 @@ class Problem(ctypes.Structure):
         ("src_block_table", ctypes.POINTER(ctypes.c_int32)), ("src_bt_stride", ctypes.c_int32),
         ("src_layer_offset", ctypes.c_int32), ("src_layers", ctypes.c_int32),
         ("dst_layer_offset", ctypes.c_int32), ("dst_layers", ctypes.c_int32),
+        ("cache_fmt", ctypes.c_int32),
     ]
 
 
@@ -109,7 +111,7 @@ class OracleProblem:
     def __init__(self, layers, heads, head_dim, src_tp, dst_tp, dst_rank, src_fmt, dst_fmt,
                  src_order, block_size, num_blocks, seq_lens, src_block_size=0,
                  src_num_blocks=0, src_block_table=None, src_bt_stride=0, src_layer_offset=0,
-                 src_layers=0, dst_layer_offset=0, dst_layers=0):
+                 src_layers=0, dst_layer_offset=0, dst_layers=0, cache_fmt=0):
         self.seq_lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32))
         self.src_block_table = None
         sbt = ctypes.POINTER(ctypes.c_int32)()
@@ -120,7 +122,7 @@ class OracleProblem:
                          src_order, block_size, num_blocks, len(self.seq_lens),
                          self.seq_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                          src_block_size, src_num_blocks, sbt, src_bt_stride, src_layer_offset,
-                         src_layers, dst_layer_offset, dst_layers)
+                         src_layers, dst_layer_offset, dst_layers, cache_fmt)
 
     def __getattr__(self, name):
         return getattr(self.__dict__["c"], name)
@@ -139,7 +141,16 @@ class OracleProblem:
 
     @property
     def dst_size(self):
+        """element size of the transfer tensor"""
         return FMT_SIZE[self.c.dst_fmt]
+
+    @property
+    def cache_fmt_eff(self):
+        return self.c.cache_fmt or self.c.dst_fmt
+
+    @property
+    def cache_size(self):
+        return FMT_SIZE[self.cache_fmt_eff]
 
     def ref(self):
         return ctypes.byref(self.c)
@@ -171,6 +182,14 @@ def fp16_to_bf16(bits: np.ndarray) -> np.ndarray:
     bits = np.ascontiguousarray(bits, dtype=np.uint16)
     out = np.empty_like(bits)
     lib().orc_fp16_to_bf16_n(_ptr(bits), _ptr(out), bits.size)
+    return out
+
+
+def dequant_row(cache_fmt: int, q: np.ndarray, s) -> np.ndarray:
+    """e4m3fn codes (uint8) of one row and their fp32 scale -> 16-bit bits."""
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    out = np.empty(q.size, dtype=np.uint16)
+    lib().orc_dequant_row(cache_fmt, q.size, _ptr(q), ctypes.c_float(float(s)), _ptr(out))
     return out
 
 
@@ -234,7 +253,7 @@ def wire_layout(p: OracleProblem):
 
 
 def cache_bytes(p: OracleProblem) -> int:
-    return p.dst_layers_held * 2 * p.num_blocks * p.block_size * p.hd * p.head_dim * p.dst_size
+    return p.dst_layers_held * 2 * p.num_blocks * p.block_size * p.hd * p.head_dim * p.cache_size
 
 
 def scale_count(p: OracleProblem) -> int:
@@ -269,12 +288,12 @@ def repack(p: OracleProblem, shards, cache, scales, block_table, bt_stride):
 
 
 def expected_rows(p: OracleProblem, shards, r, l, kv, t0, nt, sentinel=0xA5):
-    """Expected destination rows (nt*Hd, D*esize bytes) and scales (or None).
-    Rows with no source (a source page outside the source pool) keep the
-    sentinel bytes, as the destination does."""
-    row_bytes = p.head_dim * p.dst_size
+    """Expected cache rows (nt*Hd, D*esize bytes, in the cache format) and
+    scales (or None).  Rows with no source (a source page outside the source
+    pool) keep the sentinel bytes, as the destination does."""
+    row_bytes = p.head_dim * p.cache_size
     out = np.full((nt * p.hd, row_bytes), sentinel, dtype=np.uint8)
     sc = np.full(nt * p.hd * 4, sentinel, dtype=np.uint8).view(np.float32)
     _check(lib().orc_expected_rows(p.ref(), _shard_ptrs(shards), r, l, kv, t0, nt, _ptr(out),
                                    _ptr(sc)))
-    return out, (sc if p.dst_fmt == E4M3FN else None)
+    return out, (sc if p.cache_fmt_eff == E4M3FN else None)

@@ -140,6 +140,37 @@ uint16_t orc_bf16_to_fp16(uint16_t b)
     return (uint16_t)encode(ORC_FP16, sign, m);
 }
 
+/* float -> fp16 / bf16, round to nearest even; magnitudes that round above
+ * the format's largest finite value become infinite. */
+static uint16_t f32_to_16(int fmt, float v, uint32_t nan_sign)
+{
+    int bf = fmt == ORC_BF16;
+    uint32_t sign = signbit(v) ? 1u : 0u;
+    if (isnan(v))
+        return (uint16_t)((nan_sign << 15) | (bf ? 0x7FC0u : 0x7E00u));
+    if (isinf(v))
+        return (uint16_t)((sign << 15) | (bf ? 0x7F80u : 0x7C00u));
+    double m = bf ? rne_to_grid(fabs((double)v), 8, -126) : rne_to_grid(fabs((double)v), 11, -14);
+    double maxf = bf ? ldexp(255.0, 120) : 65504.0;      /* (2 - 2^-7) 2^127, (2 - 2^-10) 2^15 */
+    if (m > maxf)
+        return (uint16_t)((sign << 15) | (bf ? 0x7F80u : 0x7C00u));
+    return (uint16_t)encode(fmt, sign, m);
+}
+
+/* Dequantisation (reading R25): q * s as one fp32 product (round to nearest
+ * even), then rounded to the cache format.  A NaN code, or a NaN product
+ * (0 * Inf in a row whose scale is infinite), gives the quiet NaN with the
+ * code's sign. */
+void orc_dequant_row(int cache_fmt, int D, const uint8_t *q, float s, uint16_t *out)
+{
+    for (int d = 0; d < D; ++d) {
+        uint32_t sign = (q[d] >> 7) & 1u;
+        float x = (float)orc_decode(ORC_E4M3FN, q[d]);   /* exact */
+        float v = x * s;                                   /* fp32 product */
+        out[d] = f32_to_16(cache_fmt, isnan(x) ? NAN : v, sign);
+    }
+}
+
 /* fp16 -> bf16.  Finite values and infinities: round the exact value to the
  * bf16 grid (8 significand bits, emin = -126), ties to even; no fp16 value
  * can overflow bf16.  NaN (paper silent; reading taken): keep the sign, set
@@ -253,6 +284,7 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
 /* ------------------------------------------------------------------ */
 
 int32_t orc_src_layers(const orc_problem *p) { return p->src_layers ? p->src_layers : p->layers; }
+int32_t orc_cache_fmt(const orc_problem *p) { return p->cache_fmt ? p->cache_fmt : p->dst_fmt; }
 int32_t orc_dst_layers(const orc_problem *p) { return p->dst_layers ? p->dst_layers : p->layers; }
 
 int orc_validate(const orc_problem *p)
@@ -284,8 +316,11 @@ int orc_validate(const orc_problem *p)
             if (nb > 0 && (!p->src_block_table || p->src_bt_stride < nb)) return -1;
         }
     }
-    int sf = p->src_fmt, df = p->dst_fmt;
+    int sf = p->src_fmt, df = p->dst_fmt, cf = orc_cache_fmt(p);
     if (sf != ORC_FP16 && sf != ORC_BF16) return -2;
+    /* a cache format other than the transfer format: only the dequantising
+     * unpack e4m3fn -> fp16 / bf16 */
+    if (cf != df && !(df == ORC_E4M3FN && (cf == ORC_FP16 || cf == ORC_BF16))) return -2;
     if (sf == df) return 0;
     if (sf == ORC_FP16 && df == ORC_BF16) return 0;
     if (sf == ORC_BF16 && df == ORC_FP16) return 0;
@@ -462,6 +497,8 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
     if (rc) return rc;
     int Hd = orc_dst_heads(p), D = p->head_dim, bs = p->block_size;
     int64_t esz = orc_fmt_size(p->dst_fmt);
+    int cf = orc_cache_fmt(p);
+    int64_t cesz = orc_fmt_size(cf);
     int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
     int64_t *soff = (int64_t *)malloc(sizeof(int64_t) * (size_t)(p->num_requests + 1));
     orc_wire_layout(p, doff, soff);
@@ -477,6 +514,13 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
                     if (b < 0 || b >= p->num_blocks) continue;  /* not a page of the pool */
                     for (int i = 0; i < Hd; ++i) {
                         int64_t row = (((int64_t)l * 2 + kv) * T + t) * Hd + i;
+                        if (cf != p->dst_fmt) {   /* dequantise the row */
+                            float sc;
+                            memcpy(&sc, w + soff[r] + row * 4, 4);
+                            orc_dequant_row(cf, D, w + doff[r] + row * D * esz, sc,
+                                            (uint16_t *)(c + orc_cache_index(p, b, l, kv, slot, i, 0) * cesz));
+                            continue;
+                        }
                         memcpy(c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
                                w + doff[r] + row * D * esz, (size_t)(D * esz));
                         if (p->dst_fmt == ORC_E4M3FN)
@@ -496,7 +540,9 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
     if (rc) return rc;
     int Hd = orc_dst_heads(p), D = p->head_dim, bs = p->block_size;
     int64_t esz = orc_fmt_size(p->dst_fmt);
+    int cf = orc_cache_fmt(p);
     uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
+    uint8_t *q = (uint8_t *)malloc((size_t)D);
     uint8_t *c = (uint8_t *)cache;
     for (int r = 0; r < p->num_requests; ++r) {
         int T = p->seq_lens[r];
@@ -509,6 +555,12 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
                     if (b < 0 || b >= p->num_blocks) continue;  /* not a page of the pool */
                     for (int i = 0; i < Hd; ++i) {
                         float sc = 0.0f;
+                        if (cf != p->dst_fmt) {   /* quantise, then dequantise into the cache */
+                            if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, q, &sc))
+                                orc_dequant_row(cf, D, q, sc,
+                                                (uint16_t *)(c + orc_cache_index(p, b, l, kv, slot, i, 0) * 2));
+                            continue;
+                        }
                         if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
                                                  c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
                                                  &sc) &&
@@ -518,6 +570,7 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
                 }
     }
     free(tmp);
+    free(q);
     return 0;
 }
 
@@ -530,17 +583,25 @@ int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, in
     if (t0 < 0 || nt < 0 || t0 + nt > p->seq_lens[r]) return -1;
     int Hd = orc_dst_heads(p), D = p->head_dim;
     int64_t esz = orc_fmt_size(p->dst_fmt);
+    int cf = orc_cache_fmt(p);
     uint16_t *tmp = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)D);
+    uint8_t *q = (uint8_t *)malloc((size_t)D);
     uint8_t *o = (uint8_t *)out_rows;
     int64_t base = orc_src_request_base(p, r);
     for (int t = t0; t < t0 + nt; ++t)
         for (int i = 0; i < Hd; ++i) {
             int64_t row = (int64_t)(t - t0) * Hd + i;
             float sc = 0.0f;
+            if (cf != p->dst_fmt) {
+                if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, q, &sc))
+                    orc_dequant_row(cf, D, q, sc, (uint16_t *)(o + row * D * 2));
+                continue;
+            }
             if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, o + row * D * esz, &sc) &&
                 p->dst_fmt == ORC_E4M3FN && out_scales)
                 out_scales[row] = sc;
         }
     free(tmp);
+    free(q);
     return 0;
 }

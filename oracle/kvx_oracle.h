@@ -60,12 +60,21 @@ typedef struct {
      * dst_layer_offset + l.  0 layers means `layers` (offsets then 0). */
     int32_t src_layer_offset, src_layers;
     int32_t dst_layer_offset, dst_layers;
+    /* Element format of the decode cache; 0 means dst_fmt.  A 16-bit cache
+     * under an e4m3fn dst_fmt is a dequantising unpack: the transfer tensor
+     * carries e4m3fn codes and scales, the cache their values q * s. */
+    int32_t cache_fmt;
 } orc_problem;
 
 /* ---- casts (precision alignment) ---- */
 double   orc_decode(int fmt, uint32_t bits);             /* exact value; NaN/Inf as such */
 uint16_t orc_fp16_to_bf16(uint16_t h);                   /* IEEE round-to-nearest-even */
 uint16_t orc_bf16_to_fp16(uint16_t b);                   /* RNE; overflow to +-Inf */
+/* one e4m3fn row back to a 16-bit format: each value q * s (fp32 product),
+ * rounded to nearest even; NaN codes and NaN products give the format's
+ * quiet NaN with the code's sign */
+void     orc_dequant_row(int cache_fmt, int D, const uint8_t *q, float s, uint16_t *out);
+int32_t  orc_cache_fmt(const orc_problem *p);
 void     orc_bf16_to_fp16_n(const uint16_t *in, uint16_t *out, int64_t n);
 uint8_t  orc_f32_to_e4m3fn(float v);                     /* RNE, saturating to +-448 */
 float    orc_row_scale(const float *x, int n);           /* max|x| / 448, fp32 divide */
@@ -104,9 +113,10 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
 int orc_repack(const orc_problem *p, const void *const *shards, void *cache, float *scales,
                const int32_t *block_table, int32_t bt_stride);
 
-/* expected destination rows of request r, plane (l, kv), tokens [t0, t0+nt):
- * nt*Hd rows in (token, head) order, plus nt*Hd scales for e4m3fn; rows whose
- * source page lies outside the source pool are left as the caller filled them */
+/* expected cache rows of request r, plane (l, kv), tokens [t0, t0+nt): nt*Hd
+ * rows in (token, head) order in the cache format, plus nt*Hd scales for an
+ * e4m3fn cache; rows whose source page lies outside the source pool are left
+ * as the caller filled them */
 int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, int l, int kv,
                       int t0, int nt, void *out_rows, float *out_scales);
 

@@ -75,6 +75,27 @@ SMALL = {
                                           len_lo=40, len_hi=40, num_blocks=8, sigma=1e-6),
 }
 
+# Dequantising unpack: e4m3fn codes and scales in the transfer tensor, a
+# 16-bit decode cache holding q * s.
+SMALL_DEQUANT = {
+    "dequant_bf16_e4m3_bf16": FP8.replace(name="dequant_bf16_e4m3_bf16", cache_dtype="bf16",
+                                          layers=2, total_layers=3, num_requests=3, len_lo=5,
+                                          len_hi=70, num_blocks=64),
+    "dequant_fp16_e4m3_fp16_htd": QWEN.replace(name="dequant_fp16_e4m3_fp16_htd",
+                                               dst_dtype="e4m3fn", cache_dtype="fp16", layers=2,
+                                               total_layers=2, num_requests=3, len_lo=10,
+                                               len_hi=150, num_blocks=16),
+    "dequant_paged_tp4to2_bf16": P70B.replace(name="dequant_paged_tp4to2_bf16", dst_dtype="e4m3fn",
+                                              cache_dtype="bf16", layers=2, total_layers=2,
+                                              num_requests=2, len_lo=33, len_hi=90,
+                                              num_blocks=16, src_num_blocks=24),
+    "dequant_fp16_e4m3_bf16_empty": QWEN.replace(name="dequant_fp16_e4m3_bf16_empty",
+                                                 dst_dtype="e4m3fn", cache_dtype="bf16", layers=1,
+                                                 total_layers=1, num_requests=4,
+                                                 lens_override=(37, 0, 16, 1), block_size=16,
+                                                 num_blocks=16, seed=98),
+}
+
 # Paged sources (the prefill side's own paged cache), same shapes as the two
 # full paged workloads plus page-size ratios that do not divide each other.
 SMALL_PAGED = {
@@ -107,6 +128,12 @@ def fmt_codes(mod):
 
 
 def dst_size(w):
+    """element size of the decode cache"""
+    return 1 if w.cdt == "e4m3fn" else 2
+
+
+def wire_size(w):
+    """element size of the transfer tensor"""
     return 1 if w.dst_dtype == "e4m3fn" else 2
 
 
@@ -121,6 +148,8 @@ def oracle_problem(O, w, lens, layers=None, sbt=None):
             sbt, _ = W.src_block_table(w, lens)
         extra = dict(src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
                      src_block_table=sbt, src_bt_stride=sbt.shape[1])
+    if w.cache_dtype:
+        extra["cache_fmt"] = f[w.cache_dtype]
     return O.OracleProblem(layers or w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp,
                            w.dst_rank, f[w.src_dtype], f[w.dst_dtype], order, w.block_size,
                            w.num_blocks, lens, **extra)
@@ -163,16 +192,17 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd), or the
     one head rank // (dst_tp / H) when dst_tp is a multiple of H.
     Casts: same type = bits; fp16->bf16 and bf16->fp16 = torch .to();
+    a 16-bit cache under an e4m3fn transfer = q.float() * s then .to();
     e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn)."""
     heads = rank_heads(w)
     x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers, heads))
     x = x.to(_TDT[w.src_dtype])                                     # [L][2][Hd][T][D]
     x = x.permute(0, 1, 3, 2, 4).contiguous()                      # [L][2][T][Hd][D]
     if w.dst_dtype == w.src_dtype:
-        return x.view(torch.uint8).numpy().reshape(*x.shape[:4], -1), None
+        return x.view(torch.uint8).numpy().reshape(*x.shape[:4], 2 * w.head_dim), None
     if w.dst_dtype in ("bf16", "fp16"):
         y = x.to(_TDT[w.dst_dtype])
-        return y.view(torch.uint8).numpy().reshape(*y.shape[:4], -1), None
+        return y.view(torch.uint8).numpy().reshape(*y.shape[:4], 2 * w.head_dim), None
     xf = x.float()
     s = xf.abs().amax(dim=-1) / torch.tensor(448.0)
     v = xf / s[..., None]
@@ -180,6 +210,9 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     zero_rows = (s == 0)[..., None].expand_as(q)
     signed_zero = torch.where(torch.signbit(xf), 0x80, 0).to(torch.uint8)
     q = torch.where(zero_rows, signed_zero, q)
+    if w.cdt != "e4m3fn":   # dequantising unpack: q * s in fp32, then the 16-bit cast
+        y = (q.view(torch.float8_e4m3fn).float() * s[..., None]).to(_TDT[w.cdt])
+        return y.view(torch.uint8).numpy().reshape(*y.shape[:4], 2 * w.head_dim), None
     return q.numpy(), s.numpy()
 
 

@@ -99,6 +99,12 @@ class Workload:
     src_block_size: int = 0  # "paged" sources: tokens per prefill-side page
     src_num_blocks: int = 0  # "paged" sources: pages per (layer, k/v) plane of each shard's pool
     src_pp: int = 1          # prefill pipeline stages: equal layer ranges, one buffer set each
+    cache_dtype: str = ""    # decode cache type when it differs from dst_dtype (dequantising unpack)
+
+    @property
+    def cdt(self):
+        """element type of the decode cache"""
+        return self.cache_dtype or self.dst_dtype
 
     @property
     def hs(self):
