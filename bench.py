@@ -121,11 +121,12 @@ def main():
         l0, n = stage
         return K.make_desc(n, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
                            F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks, seq,
-                           w.src_block_size, w.src_num_blocks, 0, n, l0, w.layers)
+                           w.src_block_size, w.src_num_blocks, 0, n, l0, w.layers,
+                           F[w.cache_dtype] if w.cache_dtype else 0)
 
     plans = [K.kvx_plan(desc(list(lens), st)) for st in stages]
     infos = [K.kvx_plan_info_get(p) for p in plans]
-    esz = 1 if w.dst_dtype == "e4m3fn" else 2
+    esz = 1 if w.cdt == "e4m3fn" else 2   # the cache's element size
     n_rows = w.layers * 2 * w.num_blocks * w.block_size * w.hd
     cache = torch.empty(n_rows * w.head_dim * esz, dtype=torch.uint8, device="cuda")
     scales = torch.empty(n_rows, dtype=torch.float32, device="cuda") if esz == 1 else None
@@ -166,12 +167,15 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.src_dtype if w.src_dtype == w.cdt == w.dst_dtype else
+                 "->".join(dict.fromkeys([w.src_dtype, w.dst_dtype, w.cdt])),
         "data": "synthetic",
         "config": {"workload": w.name, "layers": w.layers, "kv_heads": w.heads,
                    "head_dim": w.head_dim, "requests": len(lens), "tokens": int(lens.sum()),
                    "src_tp": w.src_tp, "dst_tp": w.dst_tp, "dst_rank": w.dst_rank,
                    "src_dtype": w.src_dtype, "dst_dtype": w.dst_dtype,
+                   **({"cache_dtype": w.cache_dtype} if w.cache_dtype else {}),
                    "src_order": w.src_order, "block_size": w.block_size,
                    "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes},
         **({"prefill_stages": [list(st) for st in stages], "launches_per_step": len(stages)}
@@ -395,7 +399,7 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
 
     f = {"fp16": O.FP16, "bf16": O.BF16, "e4m3fn": O.E4M3FN}
     order = {"thd": O.TOKEN_MAJOR, "htd": O.HEAD_MAJOR, "paged": O.PAGED}[w.src_order]
-    esz = 1 if w.dst_dtype == "e4m3fn" else 2
+    esz = 1 if w.cdt == "e4m3fn" else 2   # the cache's element size
     L = stage[1] if stage else w.layers
     done_bytes = 0
     spent = 0.0
@@ -410,6 +414,8 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
         if sbt is not None:
             extra = dict(src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
                          src_block_table=sbt[r:r + 1], src_bt_stride=sbt.shape[1])
+        if w.cache_dtype:
+            extra["cache_fmt"] = f[w.cache_dtype]
         p = O.OracleProblem(L, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
                             f[w.src_dtype], f[w.dst_dtype], order, w.block_size, max(nb, 1), [T],
                             **extra)

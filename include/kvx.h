@@ -19,7 +19,9 @@
  *     the same device;
  *   - precision alignment (Sec. I, contribution 1, named only): the decode
  *     element type.  Casts round to nearest even; the e4m3fn cast uses a
- *     per-(token, head) fp32 scale max|x| / 448 and saturates at +-448.
+ *     per-(token, head) fp32 scale max|x| / 448 and saturates at +-448; an
+ *     e4m3fn transfer tensor may be dequantised into a 16-bit cache
+ *     (cache_dtype).
  *
  * Layouts (element indices; all dimensions row-major):
  *   source shard j (j = 0..src_tp-1) holds global heads [j*Hs, (j+1)*Hs),
@@ -34,10 +36,11 @@
  *     of Sec. III-B-2 use paged attention, each with its own page size);
  *   decode rank dst_rank holds global heads [dst_rank*Hd, (dst_rank+1)*Hd),
  *     Hd = num_kv_heads / dst_tp;
- *   cache:  [dst layer][k/v][num_blocks][block_size][Hd][dim] in dst_dtype; token
+ *   cache:  [dst layer][k/v][num_blocks][block_size][Hd][dim] in the cache
+ *     dtype (cache_dtype, else dst_dtype); token
  *     t of request r goes to page block_table[r*bt_stride + t/block_size],
  *     slot t % block_size;
- *   scales (e4m3fn only): [dst layer][k/v][num_blocks][block_size][Hd] fp32;
+ *   scales (e4m3fn cache only): [dst layer][k/v][num_blocks][block_size][Hd] fp32;
  *   transfer tensor: per request, starting on a 256-byte boundary,
  *     [layer][k/v][token][Hd][dim] in dst_dtype, then (e4m3fn only) on the
  *     next 256-byte boundary [layer][k/v][token][Hd] fp32 scales.
@@ -72,7 +75,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 4
+#define KVX_ABI_VERSION 5
 
 typedef enum {
     KVX_OK = 0,
@@ -100,11 +103,11 @@ typedef struct {
     int32_t num_layers;     /* L >= 1 */
     int32_t num_kv_heads;   /* H >= 1, global KV heads */
     int32_t head_dim;       /* D >= 1 */
-    int32_t src_tp;         /* prefill TP degree, divides H */
-    int32_t dst_tp;         /* decode TP degree, divides H */
+    int32_t src_tp;         /* prefill TP degree; divides H or is a multiple of H */
+    int32_t dst_tp;         /* decode TP degree; divides H or is a multiple of H */
     int32_t dst_rank;       /* 0 <= dst_rank < dst_tp */
     int32_t src_dtype;      /* kvx_dtype: KVX_FP16 or KVX_BF16 */
-    int32_t dst_dtype;      /* kvx_dtype */
+    int32_t dst_dtype;      /* kvx_dtype of the transfer tensor */
     int32_t src_order;      /* kvx_order */
     int32_t block_size;     /* tokens per decode page, >= 1 */
     int64_t num_blocks;     /* pages per (layer, k/v) plane of the pool, >= 1 */
@@ -123,12 +126,24 @@ typedef struct {
     int32_t src_layers;
     int32_t dst_layer_offset;
     int32_t dst_layers;
+    /* The decode cache's element type; 0 means dst_dtype.  With an e4m3fn
+     * transfer tensor, KVX_BF16 or KVX_FP16 asks for a dequantising unpack
+     * (precision alignment, Sec. I, done on the receiving side): each element
+     * of the cache is the product of its e4m3fn code's exact value and the
+     * row's fp32 scale, computed in fp32 and rounded to nearest even to the
+     * 16-bit type (fp16: overflow to infinity); a NaN code, or a NaN product,
+     * gives that type's quiet NaN (bf16 0x7FC0, fp16 0x7E00) with the code's
+     * sign.  The cache then holds no scales.  The pack and the transfer tensor
+     * are those of the e4m3fn plan; the repack writes what its pack followed
+     * by this unpack would. */
+    int32_t cache_dtype;
 } kvx_desc;
 
 typedef struct {
     uint64_t wire_bytes;            /* transfer tensor size (multiple of 256) */
     int64_t total_tokens;           /* sum of T_r */
-    int64_t read_bytes_pack, write_bytes_pack;     /* algorithmic bytes per call */
+    /* algorithmic bytes per call: elements and scales read and written once */
+    int64_t read_bytes_pack, write_bytes_pack;
     int64_t read_bytes_unpack, write_bytes_unpack;
     int64_t read_bytes_repack, write_bytes_repack;
     int32_t max_blocks_per_request; /* minimum valid bt_stride */
@@ -140,16 +155,18 @@ typedef struct {
 /* Validate the problem and build a plan (host tables, plus a device table on
  * the current HIP device when one is usable; otherwise the plan is host-only
  * and the launch calls return KVX_EDEVICE).
- * Returns KVX_EINVAL for: NULL desc/out; a dimension <= 0; H % src_tp != 0 or
- * H % dst_tp != 0; dst_rank outside [0, dst_tp); block_size <= 0;
+ * Returns KVX_EINVAL for: NULL desc/out; a dimension <= 0; a TP degree that
+ * neither divides H nor is a multiple of it; dst_rank outside [0, dst_tp); block_size <= 0;
  * num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
  * an unknown order; for KVX_PAGED, src_block_size <= 0 or src_num_blocks <= 0;
  * a negative layer offset or count, or converted layers outside either side's
  * src_layers / dst_layers;
- * head_dim * element size not a multiple of 16 bytes on either side.
+ * head_dim * element size not a multiple of 16 bytes on either side; an
+ * unknown dtype.
  * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
- * fp16->bf16, fp16->e4m3fn, bf16->e4m3fn}; a destination row (head_dim * dst
- * size) above 1024 bytes; more than 1024 heads per decode rank; more than
+ * fp16->bf16, bf16->fp16, fp16->e4m3fn, bf16->e4m3fn}; a cache_dtype other
+ * than dst_dtype unless dst_dtype is e4m3fn; a cache row (head_dim * cache
+ * element size) above 1024 bytes; more than 1024 heads per decode rank; more than
  * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
  * (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if
  * the table cannot be allocated. */
@@ -180,10 +197,11 @@ kvx_status kvx_pack(const kvx_plan_t *plan, const void *const *src_shards, void 
                     void *hip_stream);
 
 /* Unpack (VRAM-management alignment, decode side): scatter the transfer
- * tensor into the paged cache (and the scales) without further casting.
- *   cache:       device [L][2][num_blocks][block_size][Hd][D] dst_dtype, 16-byte aligned.
+ * tensor into the paged cache (and the scales), with no cast unless
+ * cache_dtype asks for the dequantisation described at kvx_desc.
+ *   cache:       device [L][2][num_blocks][block_size][Hd][D] cache dtype, 16-byte aligned.
  *   scales:      device [L][2][num_blocks][block_size][Hd] fp32, 16-byte aligned;
- *                non-NULL if and only if dst_dtype is e4m3fn.
+ *                non-NULL if and only if the cache dtype is e4m3fn.
  *   block_table: device int32 [num_requests][bt_stride]; the first
  *                ceil(T_r/block_size) entries of row r are used.  Contents are a
  *                caller contract (kvx_check_block_table checks them on the
@@ -191,7 +209,7 @@ kvx_status kvx_pack(const kvx_plan_t *plan, const void *const *src_shards, void 
  *                written.  Ids shared by two requests are two writers (a race).
  *   bt_stride:   >= max_blocks_per_request.
  * Errors as kvx_pack, plus KVX_EINVAL for a scales pointer whose presence does
- * not match dst_dtype, a NULL block table with pages to write, or a short
+ * not match the cache dtype, a NULL block table with pages to write, or a short
  * bt_stride. */
 kvx_status kvx_unpack(const kvx_plan_t *plan, const void *wire, void *cache, float *scales,
                       const int32_t *block_table, int32_t bt_stride, void *hip_stream);

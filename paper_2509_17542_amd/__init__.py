@@ -24,6 +24,12 @@ if not os.path.exists(LIB_PATH):
 
 _lib = ctypes.CDLL(LIB_PATH)
 
+# the struct layouts below are those of this version of include/kvx.h
+ABI_VERSION = 5
+if _lib.kvx_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} implements kvx ABI {_lib.kvx_abi_version()}, this binding "
+                      f"ABI {ABI_VERSION}: rebuild the library")
+
 OK, EINVAL, EUNSUPPORTED, ENOMEM, EDEVICE = 0, -1, -2, -3, -4
 FP16, BF16, E4M3FN = 1, 2, 3
 THD, HTD, PAGED = 0, 1, 2
@@ -48,6 +54,7 @@ class kvx_desc(ctypes.Structure):
         ("src_block_size", ctypes.c_int32), ("src_num_blocks", ctypes.c_int64),
         ("src_layer_offset", ctypes.c_int32), ("src_layers", ctypes.c_int32),
         ("dst_layer_offset", ctypes.c_int32), ("dst_layers", ctypes.c_int32),
+        ("cache_dtype", ctypes.c_int32),
     ]
 
 
@@ -178,15 +185,19 @@ class Pipe:
 
 def make_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype, dst_dtype,
               src_order, block_size, num_blocks, seq_lens, src_block_size=0, src_num_blocks=0,
-              src_layer_offset=0, src_layers=0, dst_layer_offset=0, dst_layers=0):
+              src_layer_offset=0, src_layers=0, dst_layer_offset=0, dst_layers=0,
+              cache_dtype=0):
     """kvx_desc plus the int32 array its seq_lens points into (src_block_size
     and src_num_blocks matter only for a PAGED source; the layer fields
-    describe pipeline stages, 0 = the converted layers)."""
+    describe pipeline stages, 0 = the converted layers; cache_dtype 0 = the
+    cache holds dst_dtype, FP16 / BF16 with an E4M3FN dst_dtype = the
+    dequantising unpack)."""
     lens = (ctypes.c_int32 * max(len(seq_lens), 1))(*[int(t) for t in seq_lens])
     d = kvx_desc(num_layers, num_kv_heads, head_dim, src_tp, dst_tp, dst_rank, src_dtype,
                  dst_dtype, src_order, block_size, num_blocks, len(seq_lens),
                  ctypes.cast(lens, ctypes.POINTER(ctypes.c_int32)), src_block_size,
-                 src_num_blocks, src_layer_offset, src_layers, dst_layer_offset, dst_layers)
+                 src_num_blocks, src_layer_offset, src_layers, dst_layer_offset, dst_layers,
+                 cache_dtype)
     d._lens = lens
     return d
 

@@ -47,7 +47,15 @@ enum Conv : int {
     kBf16E4m3 = 2,  // bf16 -> e4m3fn with per-row scale
     kF16E4m3 = 3,   // fp16 -> e4m3fn with per-row scale
     kCopy8 = 4,     // 8-bit bits unchanged (+ scale copy), unpack of e4m3fn
-    kBf16F16 = 5    // bf16 -> fp16, round to nearest even, overflow to infinity
+    kBf16F16 = 5,   // bf16 -> fp16, round to nearest even, overflow to infinity
+    // dequantising unpack: e4m3fn transfer tensor (+ scales) -> 16-bit cache
+    kDq8Bf16 = 6,
+    kDq8F16 = 7,
+    // repack into a 16-bit cache through e4m3fn: quantise, then dequantise
+    kQdBf16Bf16 = 8,
+    kQdF16Bf16 = 9,
+    kQdBf16F16 = 10,
+    kQdF16F16 = 11
 };
 
 // A run of the decode rank's heads that comes from one source shard: decode
@@ -86,7 +94,8 @@ struct KArgs {
     int32_t hs;                       // heads per source shard
     int32_t hd;                       // heads per decode rank
     int32_t head_dim;
-    int32_t row_dst_bytes;            // head_dim * dst element size
+    int32_t row_dst_bytes;            // pack: transfer-tensor row bytes; else cache row bytes
+    int32_t row_wire_bytes;           // transfer-tensor row bytes (the unpack's source rows)
     int32_t cpr;                      // 16-byte destination chunks per row
     int32_t lg_lpr;                   // log2(lanes per row), lanes per row >= cpr
     // paged sources: the prefill side's pages
@@ -96,7 +105,6 @@ struct KArgs {
     int32_t src_block_size;
     FastDiv div_sbs;
     int32_t sbt_uniform;              // every part lies in one source page
-    int32_t pad_;
 };
 
 // Launch one conversion over a.units work units; returns a hipError_t value.

@@ -86,13 +86,19 @@ __device__ __forceinline__ float quotient(float a, float s, float r)
     return __builtin_fmaf(e, r, q);
 }
 
+// source format of a quantising conversion: fp16 or bf16
+constexpr bool f16_source(int conv)
+{
+    return conv == kF16E4m3 || conv == kQdF16Bf16 || conv == kQdF16F16;
+}
+
 template <int CONV>
 struct SrcFmt {
-    static constexpr uint32_t kInf = CONV == kF16E4m3 ? 0x7C00u : 0x7F80u;
+    static constexpr uint32_t kInf = f16_source(CONV) ? 0x7C00u : 0x7F80u;
     // magnitude bits (sign cleared) -> fp32
     __device__ static __forceinline__ float widen(uint32_t m)
     {
-        if constexpr (CONV == kF16E4m3)
+        if constexpr (f16_source(CONV))
             return static_cast<float>(
                 __builtin_bit_cast(_Float16, static_cast<unsigned short>(m)));
         else
@@ -100,19 +106,20 @@ struct SrcFmt {
     }
 };
 
-// General path: one lane's 16 source elements (two 16-byte vectors) -> 16
+// General path: one lane's 2*NW source elements (NW 32-bit words) -> 2*NW
 // e4m3fn bytes, every case of the definition (NaN elements, zero rows, scales
 // too small or too large for the two-step divide), element by element in
 // software.  The row maximum is reduced over the lanes-per-row group (2^lg
 // lanes, consecutive, so xor shuffles stay inside the group); every lane of the
 // wave must execute the reduction.
-template <int CONV>
-__device__ __forceinline__ uint4 to_e4m3_general(const uint32_t (&w)[8], int lg, float& scale_out)
+template <int CONV, int NW>
+__device__ __forceinline__ void e4m3_codes_general(const uint32_t (&w)[NW], int lg,
+                                                   float& scale_out, uint32_t (&out)[NW / 2])
 {
     using F = SrcFmt<CONV>;
     uint32_t m = 0;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < NW; ++k) {
         uint32_t lo = w[k] & 0x7FFFu, hi = (w[k] >> 16) & 0x7FFFu;
         lo = lo > F::kInf ? 0u : lo;  // NaN elements do not take part in the maximum
         hi = hi > F::kInf ? 0u : hi;
@@ -126,9 +133,10 @@ __device__ __forceinline__ uint4 to_e4m3_general(const uint32_t (&w)[8], int lg,
     const bool fast = s >= 0x1p-80f && s <= 0x1p100f;
     const float r0 = __builtin_amdgcn_rcpf(s);
     const float r = __builtin_fmaf(__builtin_fmaf(-s, r0, 1.0f), r0, r0);
-    uint32_t out[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
+    for (int k = 0; k < NW / 2; ++k) out[k] = 0u;
+#pragma unroll
+    for (int k = 0; k < 2 * NW; ++k) {
         const uint32_t h = (w[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
         const uint32_t mag = h & 0x7FFFu;
         uint32_t code;
@@ -144,37 +152,38 @@ __device__ __forceinline__ uint4 to_e4m3_general(const uint32_t (&w)[8], int lg,
         }
         out[k >> 2] |= (code | ((h >> 8) & 0x80u)) << ((k & 3) * 8);
     }
-    return make_uint4(out[0], out[1], out[2], out[3]);
 }
 
-// One lane's 16 source elements -> 16 e4m3fn bytes.  Fast path for rows with
+// One lane's 2*NW source elements -> 2*NW e4m3fn bytes.  Fast path for rows with
 // no NaN and a scale in [2^-80, 2^100]: the row maximum from packed 16-bit
 // maxima, the exact quotient |x| / s, the element's sign set on it, and the
 // hardware conversion v_cvt_pk_fp8_f32 (round to nearest even, OCP e4m3fn on
 // gfx950; it equals e4m3_code on every fp32 magnitude up to 448, and a
 // quotient cannot round above 448 because |x| <= amax).  Other rows take the
 // general path.  Every lane of the wave must execute this.
-template <int CONV>
-__device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& scale_out)
+template <int CONV, int NW>
+__device__ __forceinline__ void e4m3_codes(const uint32_t (&w)[NW], int lg, float& scale_out,
+                                           uint32_t (&out)[NW / 2])
 {
     using F = SrcFmt<CONV>;
     typedef unsigned short us2 __attribute__((ext_vector_type(2)));
-    const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
     us2 mm = {0, 0};
 #pragma unroll
-    for (int k = 0; k < 8; ++k)  // magnitudes, NaN included
+    for (int k = 0; k < NW; ++k)  // magnitudes, NaN included
         mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
     uint32_t m = max(uint32_t(mm.x), uint32_t(mm.y));
     for (int o = 1; o < (1 << lg); o <<= 1)
         m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
     const float s = F::widen(m) / 448.0f;  // IEEE divide; NaN if the row holds a NaN
-    if (!(s >= 0x1p-80f && s <= 0x1p100f)) return to_e4m3_general<CONV>(w, lg, scale_out);
+    if (!(s >= 0x1p-80f && s <= 0x1p100f)) {
+        e4m3_codes_general<CONV, NW>(w, lg, scale_out, out);
+        return;
+    }
     scale_out = s;
     const float r0 = __builtin_amdgcn_rcpf(s);
     const float r = __builtin_fmaf(__builtin_fmaf(-s, r0, 1.0f), r0, r0);
-    uint32_t out[4];
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {  // output dword d = elements 4d .. 4d+3 = source words 2d, 2d+1
+    for (int d = 0; d < NW / 2; ++d) {  // output dword d = elements 4d .. 4d+3 = words 2d, 2d+1
         float q[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -185,7 +194,86 @@ __device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& sca
         const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
         out[d] = uint32_t(__builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true));
     }
+}
+
+// One lane's 16 source elements (two 16-byte vectors) -> 16 e4m3fn bytes.
+template <int CONV>
+__device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& scale_out)
+{
+    const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+    uint32_t out[4];
+    e4m3_codes<CONV, 8>(w, lg, scale_out, out);
     return make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+// ---- dequantisation: e4m3fn codes and a row scale -> 16-bit values ----------
+
+// The product q * s is rounded to fp32 before its 16-bit conversion.  Left
+// alone, the compiler folds the multiply and an f32 -> f16 conversion into
+// one mixed-precision FMA (v_fma_mixlo_f16): that rounds the exact product
+// once, straight to fp16, and adds +0, which drops the sign of a zero product.
+// The empty asm makes the fp32 value opaque, so it is materialised as such.
+template <typename T>
+__device__ __forceinline__ T as_rounded(T v)
+{
+    __asm__("" : "+v"(v));
+    return v;
+}
+
+// One code -> q * s rounded to the 16-bit format: the exact value of the code
+// (3 fraction bits, bias 7, codes below 8 subnormal), one fp32 product, the
+// conversion rounding to nearest even.  NaN codes and NaN products (0 * Inf)
+// give the format's quiet NaN with the code's sign.
+template <bool kBf16>
+__device__ __forceinline__ uint32_t dequant1(uint32_t c, float s)
+{
+    const uint32_t sign = (c & 0x80u) << 8;
+    const uint32_t e = (c >> 3) & 0xFu, m = c & 7u;
+    const uint32_t qnan = kBf16 ? 0x7FC0u : 0x7E00u;
+    if ((c & 0x7Fu) == 0x7Fu) return sign | qnan;
+    const float x = e ? __builtin_ldexpf(float(8u + m), int(e) - 10) : float(m) * 0x1p-9f;
+    const float v = as_rounded((c & 0x80u ? -x : x) * s);
+    if (v != v) return sign | qnan;
+    if constexpr (kBf16)
+        return __builtin_bit_cast(unsigned short, static_cast<__bf16>(v));
+    else
+        return __builtin_bit_cast(unsigned short, static_cast<_Float16>(v));
+}
+
+// 8 codes (two dwords) -> 8 16-bit values.  Rows without NaN codes and with a
+// finite scale: the hardware decode v_cvt_pk_f32_fp8 (exact), the fp32
+// product and the packed conversion; otherwise code by code.
+template <bool kBf16>
+__device__ __forceinline__ uint4 dequant8(uint32_t c0, uint32_t c1, float s)
+{
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    // a byte b has (b & 0x7F) == 0x7F exactly when (b & 0x7F) + 1 sets bit 7
+    const uint32_t nan = (((c0 & 0x7F7F7F7Fu) + 0x01010101u) | ((c1 & 0x7F7F7F7Fu) + 0x01010101u)) &
+                         0x80808080u;
+    uint32_t o[4];
+    if (!nan && __builtin_fabsf(s) <= 0x1.fffffep127f) {
+        const f2 f[4] = {as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c0), false) * s),
+                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c0), true) * s),
+                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c1), false) * s),
+                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c1), true) * s)};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if constexpr (kBf16)
+                o[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f[k], b2));
+            else
+                o[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f[k], h2));
+        }
+    } else {
+        const uint32_t c[2] = {c0, c1};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t w = c[k >> 1] >> ((k & 1) * 16);
+            o[k] = dequant1<kBf16>(w & 0xFFu, s) | (dequant1<kBf16>((w >> 8) & 0xFFu, s) << 16);
+        }
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // 8 fp16 -> 8 bf16.  Without NaN (the usual case): exact widening and the
@@ -284,19 +372,27 @@ __device__ __forceinline__ void warm_translation(const KArgs& a, uint32_t unit)
 template <int MODE, int CONV, int ORDER>
 __device__ __forceinline__ void convert_part(const KArgs& a)
 {
-    constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;
-    constexpr bool kScales = kFp8 || CONV == kCopy8;
+    constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;     // writes e4m3fn codes
+    constexpr bool kQd = CONV == kQdBf16Bf16 || CONV == kQdF16Bf16 ||  // quantise + dequantise
+                         CONV == kQdBf16F16 || CONV == kQdF16F16;
+    constexpr bool kDq = CONV == kDq8Bf16 || CONV == kDq8F16;          // dequantising unpack
+    constexpr bool kQuant = kFp8 || kQd;                               // row maximum over lanes
+    constexpr bool kScalesIn = CONV == kCopy8 || kDq;                  // unpack reads row scales
+    constexpr bool kScales = kFp8 || CONV == kCopy8;                   // rows written with a scale
+    constexpr bool kToBf16 = CONV == kDq8Bf16 || CONV == kQdBf16Bf16 || CONV == kQdF16Bf16;
     constexpr int kVecs = kFp8 ? 2 : 1;                       // 16-byte loads per lane
     constexpr int kSrcEsz = CONV == kCopy8 ? 1 : 2;
     constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;
+    static_assert(!kDq || MODE == kUnpack, "dequantisation reads the transfer tensor");
+    static_assert(!kQd || MODE == kRepack, "quantise + dequantise is a repack");
     // Issue order.  "Early": the page lookups are scalar loads issued before
     // any lane-dependent branch and every lane issues its row load
     // unconditionally (lanes without a row read the buffer's first vector), so
     // the lookups, the row loads and the paged source's page lookup overlap
     // instead of following one another.  Measured faster for repacks from
     // paged sources (+16%) and 16-bit token-major rows (+2%); the head-major
-    // and e4m3fn paths and the pack from paged sources measure 2-4% faster
-    // with the row load inside the branch.
+    // and e4m3fn paths measure 2-4% faster with the row load inside the
+    // branch, and the pack from paged sources the same either way.
     constexpr bool kEarly =
         (ORDER == KVX_PAGED && MODE != kPack) ||
         (ORDER == KVX_THD && (CONV == kCopy16 || CONV == kF16Bf16 || CONV == kBf16F16));
@@ -358,8 +454,9 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     const float* sp = nullptr;
     if constexpr (MODE == kUnpack) {
         base = static_cast<const char*>(a.wire_in);
-        p = base + it.wire_data + (row0 + row) * a.row_dst_bytes + sub * 16;
-        if constexpr (kScales)
+        // a dequantising lane reads the 8 codes of its 16 output bytes
+        p = base + it.wire_data + (row0 + row) * a.row_wire_bytes + sub * (kDq ? 8 : 16);
+        if constexpr (kScalesIn)
             sp = reinterpret_cast<const float*>(base + it.wire_scale) + row0 + row;
     } else {
         base = static_cast<const char*>(a.src[seg.slot]);
@@ -391,14 +488,19 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     if constexpr (kEarly) {
         // lanes without a row read the buffer's first vector (valid, cached)
         const char* pl = ok ? p : base;
+        if constexpr (kDq) {
+            const uint2 c = *reinterpret_cast<const uint2*>(pl);
+            v[0] = make_uint4(c.x, c.y, 0u, 0u);
+        } else {
 #pragma unroll
-        for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(pl)[k];
-        if constexpr (MODE == kUnpack && kScales)
+            for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(pl)[k];
+        }
+        if constexpr (MODE == kUnpack && kScalesIn)
             sc = *(ok ? sp : reinterpret_cast<const float*>(base));
         // keep the loads here: the compiler would otherwise sink them below
         // the destination-page check, behind the scalar lookups
         __asm__ volatile("" ::: "memory");
-        if constexpr (kFp8)
+        if constexpr (kQuant)
 #pragma unroll
             for (int k = 0; k < kVecs; ++k)  // rows without data take part in the maximum as zeros
                 if (!ok) v[k] = make_uint4(0u, 0u, 0u, 0u);
@@ -406,10 +508,15 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
 #pragma unroll
         for (int k = 0; k < kVecs; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
         if (ok) {
+            if constexpr (kDq) {
+                const uint2 c = *reinterpret_cast<const uint2*>(p);
+                v[0] = make_uint4(c.x, c.y, 0u, 0u);
+            } else {
 #pragma unroll
-            for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
-            if constexpr (MODE == kUnpack && kScales)
-                if (sub == 0) sc = *sp;
+                for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+            }
+            if constexpr (MODE == kUnpack && kScalesIn)
+                if (kDq || sub == 0) sc = *sp;  // every dequantising lane needs the scale
         }
         if constexpr (MODE != kPack) b = a.bt[int64_t(it.req) * a.bt_stride + it.blk];
     }
@@ -430,9 +537,16 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     }
 
     uint4 out;
-    if constexpr (kFp8)
+    if constexpr (kFp8) {
         out = to_e4m3<CONV>(v, lg, sc);  // every lane takes part in the row reduction
-    else if constexpr (CONV == kF16Bf16)
+    } else if constexpr (kQd) {
+        const uint32_t w[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
+        uint32_t c[2];
+        e4m3_codes<CONV, 4>(w, lg, sc, c);  // every lane takes part in the row reduction
+        out = dequant8<kToBf16>(c[0], c[1], sc);
+    } else if constexpr (kDq) {
+        out = dequant8<kToBf16>(v[0].x, v[0].y, sc);
+    } else if constexpr (CONV == kF16Bf16)
         out = to_bf16x8(v[0]);
     else if constexpr (CONV == kBf16F16)
         out = to_f16x8(v[0]);
@@ -492,8 +606,18 @@ int go_conv(int conv, const KArgs& a, void* stream)
     case kBf16F16: return go<MODE, kBf16F16, ORDER>(a, stream);
     case kBf16E4m3: return go<MODE, kBf16E4m3, ORDER>(a, stream);
     case kF16E4m3: return go<MODE, kF16E4m3, ORDER>(a, stream);
-    default: return int(hipErrorInvalidValue);
+    default: break;
     }
+    if constexpr (MODE == kRepack) {
+        switch (conv) {
+        case kQdBf16Bf16: return go<MODE, kQdBf16Bf16, ORDER>(a, stream);
+        case kQdF16Bf16: return go<MODE, kQdF16Bf16, ORDER>(a, stream);
+        case kQdBf16F16: return go<MODE, kQdBf16F16, ORDER>(a, stream);
+        case kQdF16F16: return go<MODE, kQdF16F16, ORDER>(a, stream);
+        default: break;
+        }
+    }
+    return int(hipErrorInvalidValue);
 }
 
 }  // namespace
@@ -503,6 +627,8 @@ int launch(int mode, int conv, int order, const KArgs& a, void* stream)
     if (mode == kUnpack) {
         if (conv == kCopy16) return go<kUnpack, kCopy16, KVX_THD>(a, stream);
         if (conv == kCopy8) return go<kUnpack, kCopy8, KVX_THD>(a, stream);
+        if (conv == kDq8Bf16) return go<kUnpack, kDq8Bf16, KVX_THD>(a, stream);
+        if (conv == kDq8F16) return go<kUnpack, kDq8F16, KVX_THD>(a, stream);
         return int(hipErrorInvalidValue);
     }
     if (mode == kPack) {

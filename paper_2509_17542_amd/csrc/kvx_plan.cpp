@@ -59,6 +59,18 @@ int pick_conv(int s, int d)
 // then replicated on tp / H consecutive ranks).
 int heads_per_rank(int H, int tp) { return tp <= H ? H / tp : 1; }
 
+// The cache's element type: dst_dtype, or the 16-bit type of a dequantising
+// unpack of an e4m3fn transfer tensor.
+int cache_dtype_of(const kvx_desc& d) { return d.cache_dtype ? d.cache_dtype : d.dst_dtype; }
+
+// repack kernel variant that quantises to e4m3fn and dequantises into a
+// 16-bit cache
+int qd_conv(int s, int c)
+{
+    if (s == KVX_BF16) return c == KVX_BF16 ? kvx::kQdBf16Bf16 : kvx::kQdBf16F16;
+    return c == KVX_BF16 ? kvx::kQdF16Bf16 : kvx::kQdF16F16;
+}
+
 int32_t src_layers_of(const kvx_desc& d) { return d.src_layers ? d.src_layers : d.num_layers; }
 int32_t dst_layers_of(const kvx_desc& d) { return d.dst_layers ? d.dst_layers : d.num_layers; }
 
@@ -92,12 +104,19 @@ kvx_status validate(const kvx_desc* d)
     if (pick_conv(d->src_dtype, d->dst_dtype) < 0)
         return fail(KVX_EUNSUPPORTED, "dtype pair %d -> %d is not supported", d->src_dtype,
                     d->dst_dtype);
+    const int cdt = cache_dtype_of(*d);
+    if (cdt != KVX_FP16 && cdt != KVX_BF16 && cdt != KVX_FP8_E4M3FN)
+        return fail(KVX_EINVAL, "unknown cache_dtype %d", d->cache_dtype);
+    if (cdt != d->dst_dtype && d->dst_dtype != KVX_FP8_E4M3FN)
+        return fail(KVX_EUNSUPPORTED,
+                    "cache_dtype %d differs from a 16-bit dst_dtype %d (only an e4m3fn transfer "
+                    "tensor is dequantised)", cdt, d->dst_dtype);
     if ((int64_t(d->head_dim) * dtype_size(d->src_dtype)) % 16 ||
         (int64_t(d->head_dim) * dtype_size(d->dst_dtype)) % 16)
         return fail(KVX_EINVAL, "head_dim %d: rows must be whole 16-byte vectors on both sides",
                     d->head_dim);
-    if (int64_t(d->head_dim) * dtype_size(d->dst_dtype) > 16 * kvx::kMaxRowChunks)
-        return fail(KVX_EUNSUPPORTED, "destination rows above %d bytes", 16 * kvx::kMaxRowChunks);
+    if (int64_t(d->head_dim) * dtype_size(cdt) > 16 * kvx::kMaxRowChunks)
+        return fail(KVX_EUNSUPPORTED, "cache rows above %d bytes", 16 * kvx::kMaxRowChunks);
     if (d->num_kv_heads / d->dst_tp > kvx::kMaxHeadsPerRank)
         return fail(KVX_EUNSUPPORTED, "more than %d heads per decode rank", kvx::kMaxHeadsPerRank);
     if (d->num_kv_heads / d->src_tp > 65535)
@@ -142,6 +161,9 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     p->esz_src = dtype_size(d.src_dtype);
     p->esz_dst = dtype_size(d.dst_dtype);
     p->conv = pick_conv(d.src_dtype, d.dst_dtype);
+    p->cache_dtype = cache_dtype_of(d);
+    p->esz_cache = dtype_size(p->cache_dtype);
+    p->dequant = p->cache_dtype != d.dst_dtype;
 
     // parallel-strategy alignment: decode head i -> global head g -> (shard j,
     // head h within it); runs of decode heads with the same shard and
@@ -168,9 +190,12 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     }
     for (kvx::Segment& g : p->segs) g.div_n = kvx::make_fastdiv(uint32_t(g.n));
 
-    // lanes per row: the smallest power of two covering the row's 16-byte chunks
+    // lanes per row: the smallest power of two covering the row's 16-byte
+    // chunks (transfer-tensor rows for the pack, cache rows otherwise)
     p->cpr = d.head_dim * p->esz_dst / 16;
     while ((1 << p->lg_lpr) < p->cpr) ++p->lg_lpr;
+    p->cpr_c = d.head_dim * p->esz_cache / 16;
+    while ((1 << p->lg_c) < p->cpr_c) ++p->lg_c;
 
     // requests: source offsets, transfer-tensor segments, work items
     const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
@@ -205,13 +230,16 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         p->elems_rows += rows;
     }
     p->wire_bytes = uint64_t(align256(wire));
-    const int64_t rpp = kvx::kThreads >> p->lg_lpr;  // rows per workgroup pass
+    // rows per workgroup pass: of the transfer tensor (pack), of the cache
+    const int64_t rpp = kvx::kThreads >> p->lg_lpr, rpp_c = kvx::kThreads >> p->lg_c;
     int max_n = 0;
     for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
     p->parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
-    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp - 1) / rpp);
-    if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * int64_t(p->segs.size()),
-                                        p->parts_unpack) > kvx::kMaxUnits) {
+    p->parts_repack = int32_t((int64_t(d.block_size) * max_n + rpp_c - 1) / rpp_c);
+    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp_c - 1) / rpp_c);
+    const int64_t most = std::max<int64_t>(
+        int64_t(std::max(p->parts, p->parts_repack)) * int64_t(p->segs.size()), p->parts_unpack);
+    if (nitems * L2 * most > kvx::kMaxUnits) {
         delete p;
         return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers x parts)",
                     (long long)kvx::kMaxUnits);
@@ -256,14 +284,16 @@ kvx_status kvx_plan_info_get(const kvx_plan_t* p, kvx_plan_info* info)
     const int64_t rd = p->elems_rows * D * p->esz_src;
     const int64_t wr = p->elems_rows * D * p->esz_dst +
                        (p->d.dst_dtype == KVX_FP8_E4M3FN ? p->elems_rows * 4 : 0);
+    const int64_t cw = p->elems_rows * D * p->esz_cache +
+                       (p->cache_dtype == KVX_FP8_E4M3FN ? p->elems_rows * 4 : 0);
     info->wire_bytes = p->wire_bytes;
     info->total_tokens = p->total_tokens;
     info->read_bytes_pack = rd;
     info->write_bytes_pack = wr;
     info->read_bytes_unpack = wr;
-    info->write_bytes_unpack = wr;
+    info->write_bytes_unpack = cw;
     info->read_bytes_repack = rd;
-    info->write_bytes_repack = wr;
+    info->write_bytes_repack = cw;
     info->max_blocks_per_request = p->max_blocks;
     info->num_items = int32_t(p->items.size());
     info->device = p->device;
@@ -349,7 +379,11 @@ namespace {
 
 int conv_for(const kvx_plan_t* p, int mode)
 {
-    if (mode == kvx::kUnpack) return p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
+    if (mode == kvx::kUnpack) {
+        if (p->dequant) return p->cache_dtype == KVX_BF16 ? kvx::kDq8Bf16 : kvx::kDq8F16;
+        return p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
+    }
+    if (mode == kvx::kRepack && p->dequant) return qd_conv(p->d.src_dtype, p->cache_dtype);
     return p->conv;
 }
 
@@ -362,7 +396,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
                    int layer_shift = 0)
 {
     if (!p) return fail(KVX_EINVAL, "NULL plan");
-    const bool fp8 = p->d.dst_dtype == KVX_FP8_E4M3FN;
+    const bool fp8 = p->cache_dtype == KVX_FP8_E4M3FN;  // the cache holds scales
     const bool paged = p->d.src_order == KVX_PAGED;
     std::memset(&a, 0, sizeof a);
     if (mode != kvx::kUnpack && paged != paged_call)
@@ -393,8 +427,8 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     if (!aligned16(dst)) return fail(KVX_EINVAL, "destination not 16-byte aligned");
     if (mode != kvx::kPack) {
         if (fp8 != (scales != nullptr))
-            return fail(KVX_EINVAL, fp8 ? "e4m3fn destination needs a scales buffer"
-                                        : "scales given for a 16-bit destination");
+            return fail(KVX_EINVAL, fp8 ? "e4m3fn cache needs a scales buffer"
+                                        : "scales given for a 16-bit cache");
         if (scales && !aligned16(scales)) return fail(KVX_EINVAL, "scales not 16-byte aligned");
         if (!p->items.empty() && !bt) return fail(KVX_EINVAL, "NULL block table");
         if (bt_stride < p->max_blocks)
@@ -421,7 +455,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
         a.seg[0] = kvx::Segment{0, 0, 0, p->hd, kvx::make_fastdiv(uint32_t(p->hd))};
     } else {
         a.num_segs = uint32_t(p->segs.size());
-        a.parts = uint32_t(p->parts);
+        a.parts = uint32_t(mode == kvx::kPack ? p->parts : p->parts_repack);
         for (size_t k = 0; k < p->segs.size(); ++k) a.seg[k] = p->segs[k];
     }
     const int64_t units = int64_t(p->items.size()) * a.planes * a.num_segs * a.parts;
@@ -432,16 +466,20 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     a.div_items = kvx::make_fastdiv(a.num_items);
     a.div_bs = kvx::make_fastdiv(uint32_t(d.block_size));
     a.num_blocks = d.num_blocks;
-    a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_dst;
+    a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_cache;
     a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
     a.bt_stride = bt_stride;
     a.block_size = d.block_size;
     a.hs = p->hs;
     a.hd = p->hd;
     a.head_dim = d.head_dim;
-    a.row_dst_bytes = d.head_dim * p->esz_dst;
-    a.cpr = p->cpr;
-    a.lg_lpr = p->lg_lpr;
+    // lanes follow the rows written: transfer-tensor rows for the pack,
+    // cache rows otherwise
+    const bool to_wire = mode == kvx::kPack;
+    a.row_wire_bytes = d.head_dim * p->esz_dst;
+    a.row_dst_bytes = to_wire ? a.row_wire_bytes : d.head_dim * p->esz_cache;
+    a.cpr = to_wire ? p->cpr : p->cpr_c;
+    a.lg_lpr = to_wire ? p->lg_lpr : p->lg_c;
     if (mode != kvx::kUnpack && paged) {
         a.sbt = sbt;
         a.sbt_stride = sbt_stride;
@@ -452,7 +490,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
         // i.e. tokens from part*rpp/n on.  When n divides rpp, a part holds
         // rpp/n whole tokens starting at a multiple of rpp/n; when rpp/n also
         // divides both page sizes, those tokens never straddle a source page.
-        const int rpp = kvx::kThreads >> p->lg_lpr;
+        const int rpp = kvx::kThreads >> a.lg_lpr;
         bool uniform = true;
         for (const kvx::Segment& g : p->segs)
             if (rpp % g.n || d.src_block_size % (rpp / g.n) || d.block_size % (rpp / g.n))

@@ -241,3 +241,81 @@ def written_mask(w, lens, bt, nlayers):
             n = min(w.block_size, int(T) - k * w.block_size)
             m[:, :, bt[r, k], :n] = True
     return m
+
+
+def double_rounding_scales(bits):
+    """fp32 scales s for which some e4m3fn value q makes the fp32 product q * s
+    land exactly on a midpoint of a format with `bits` significand bits (11:
+    fp16, 8: bf16) while the exact product does not: rounding q * s to fp32
+    first, then to that format, differs from rounding the exact product
+    once.  One scale per (q, midpoint) pair tried."""
+    def rne(x, p):
+        e = np.floor(np.log2(abs(x)))
+        step = 2.0 ** (p - 1 - e)
+        return np.rint(x * step) / step
+
+    out = []
+    for q in (1.875, 1.625, 1.375, 1.125, 1.75, 1.25):
+        for mid in (1 + 2.0 ** -bits, 1 + 3 * 2.0 ** -bits, 1.5 + 2.0 ** -bits):
+            s0 = np.float32(mid / q)
+            for k in range(1, 41):
+                s = s0
+                for _ in range(k // 2):
+                    s = np.nextafter(s, np.float32(np.inf if k % 2 else -np.inf))
+                p = q * float(s)                    # exact in float64
+                if rne(float(np.float32(p)), bits) != rne(p, bits):
+                    out.append(float(s))
+                    break
+    return out
+
+
+# ---- cast sweeps: rows of chosen bit patterns in a one-request workload ----
+
+def sweep_case(src, dst, rows_bits):
+    """One request whose 2*T rows (layer 0, k then v) are the given rows
+    (uint16 [2T, 128]); TP1, one head, 16-token pages in order."""
+    n = rows_bits.shape[0]
+    assert n % 32 == 0
+    T = n // 2
+    w = W.Workload("sweep", 1, 1, 1, 128, 1, 1, 0, src, dst, "thd", 16, T // 16, 1, T, T, seed=1)
+    lens = np.array([T], dtype=np.int32)
+    bt = np.arange(T // 16, dtype=np.int32)[None, :]
+    return w, lens, bt, [np.ascontiguousarray(rows_bits.reshape(-1))]
+
+
+def pad_rows(rows):
+    n = -(-rows.shape[0] // 32) * 32
+    out = np.zeros((n, 128), dtype=np.uint16)
+    out[:rows.shape[0]] = rows
+    return out
+
+
+def e4m3_sweep_rows(fmt, amaxes, rng):
+    """Rows [amax, x_1..x_127] covering every finite pattern x with |x| <= amax
+    (both signs) for each amax, plus NaN/Inf/zero rows."""
+    allp = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    inf = 0x7C00 if fmt == "fp16" else 0x7F80
+    mag = allp & 0x7FFF
+    finite = allp[mag < inf]
+    out = []
+    for a in amaxes:
+        xs = finite[(finite & 0x7FFF) <= a]
+        xs = rng.permutation(xs)
+        k = -(-xs.size // 127)
+        xs = np.concatenate([xs, np.zeros(k * 127 - xs.size, np.uint16)]).reshape(k, 127)
+        pos = rng.integers(0, 128, k)
+        rows = np.empty((k, 128), np.uint16)
+        for j in range(k):
+            rows[j] = np.insert(xs[j], pos[j], a | (rng.integers(0, 2) << 15))
+        out.append(rows)
+    special = np.zeros((6, 128), np.uint16)
+    special[1, :] = 0x8000                         # all -0
+    special[2, 5] = inf | 0x1                      # a NaN in a zero row
+    special[3, :] = 0x3C00 if fmt == "fp16" else 0x3F80
+    special[3, 7] = inf                            # +Inf sets the row maximum
+    special[4, :64] = (inf | 0x40) | 0x8000        # half NaN, rest zero
+    special[5, :] = rng.integers(0, 0x7800, 128)
+    special[5, 9] = inf | 0x20                     # one NaN among finite values
+    special[5, 11] = inf | 0x8000                  # and -Inf: the row maximum is Inf
+    out.append(special)
+    return np.concatenate(out)

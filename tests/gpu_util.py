@@ -26,7 +26,8 @@ _ORDER = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}
 def desc_for(w, lens, layers=None):
     return K.make_desc(layers or w.layers, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
                        _F[w.src_dtype], _F[w.dst_dtype], _ORDER[w.src_order], w.block_size,
-                       w.num_blocks, list(lens), w.src_block_size, w.src_num_blocks)
+                       w.num_blocks, list(lens), w.src_block_size, w.src_num_blocks,
+                       cache_dtype=_F[w.cache_dtype] if w.cache_dtype else 0)
 
 
 def dev_u16(a):
@@ -38,7 +39,7 @@ def pool(w, layers, fill=W.SENTINEL):
     n = layers * 2 * w.num_blocks * w.block_size * w.hd
     cache = torch.full((n * row,), fill, dtype=torch.uint8, device=DEV)
     scales = None
-    if w.dst_dtype == "e4m3fn":
+    if w.cdt == "e4m3fn":
         scales = torch.full((n * 4,), fill, dtype=torch.uint8, device=DEV).view(torch.float32)
     return cache, scales
 
@@ -107,7 +108,7 @@ def oracle_pool(w, lens, bt, stride, shards, layers=None, op="repack", wire=None
     p = oracle_problem(O, w, lens, layers, sbt=sbt)
     cache = np.full(O.cache_bytes(p), W.SENTINEL, dtype=np.uint8)
     scales = None
-    if w.dst_dtype == "e4m3fn":
+    if w.cdt == "e4m3fn":
         scales = np.full(4 * O.scale_count(p), W.SENTINEL, dtype=np.uint8).view(np.float32)
     if op == "repack":
         O.repack(p, shards, cache, scales, bt, stride)

@@ -8,7 +8,7 @@ import re
 import numpy as np
 import pytest
 
-from cases import SMALL, SMALL_PAGED, FULL, oracle_problem
+from cases import FULL, SMALL, SMALL_DEQUANT, SMALL_PAGED, oracle_problem
 from conftest import ROOT
 
 import oracle as O
@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 4
+    assert K.kvx_abi_version() == 5
 
 
 def desc_for(w, lens, **over):
@@ -40,24 +40,28 @@ def desc_for(w, lens, **over):
               dst_dtype=f[w.dst_dtype],
               src_order={"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order],
               block_size=w.block_size, num_blocks=w.num_blocks, seq_lens=list(lens),
-              src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks)
+              src_block_size=w.src_block_size, src_num_blocks=w.src_num_blocks,
+              cache_dtype=f[w.cache_dtype] if w.cache_dtype else 0)
     kw.update(over)
     return K.make_desc(**kw)
 
 
-@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_PAGED) + list(FULL))
+@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_PAGED) + list(SMALL_DEQUANT) +
+                         list(FULL))
 def test_plan_bytes_and_segments(name):
-    w = (SMALL | SMALL_PAGED | FULL)[name]
+    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | FULL)[name]
     lens = W.seq_lens(w)
     plan = K.kvx_plan(desc_for(w, lens))
     info = K.kvx_plan_info_get(plan)
-    esz_s, esz_d = 2, (1 if w.dst_dtype == "e4m3fn" else 2)
     rows = w.layers * 2 * int(lens.sum()) * w.hd
-    rd = rows * w.head_dim * esz_s
-    wr = rows * w.head_dim * esz_d + (rows * 4 if w.dst_dtype == "e4m3fn" else 0)
-    assert (info.read_bytes_repack, info.write_bytes_repack) == (rd, wr)
+
+    def row_bytes(dt):  # a row of head_dim elements, plus its scale for e4m3fn
+        return w.head_dim + 4 if dt == "e4m3fn" else 2 * w.head_dim
+
+    rd, wr, cw = rows * 2 * w.head_dim, rows * row_bytes(w.dst_dtype), rows * row_bytes(w.cdt)
+    assert (info.read_bytes_repack, info.write_bytes_repack) == (rd, cw)
     assert (info.read_bytes_pack, info.write_bytes_pack) == (rd, wr)
-    assert (info.read_bytes_unpack, info.write_bytes_unpack) == (wr, wr)
+    assert (info.read_bytes_unpack, info.write_bytes_unpack) == (wr, cw)
     nb = [(int(t) + w.block_size - 1) // w.block_size for t in lens]
     assert info.max_blocks_per_request == max(nb + [0])
     assert info.num_items == sum(nb)
@@ -93,6 +97,9 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(num_kv_heads=4, dst_tp=6), K.EINVAL), (dict(num_kv_heads=4, src_tp=6), K.EINVAL),
     (dict(dst_dtype=9), K.EINVAL), (dict(head_dim=1024), K.EUNSUPPORTED),
     (dict(num_kv_heads=4096, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
+    (dict(cache_dtype=1), K.EUNSUPPORTED),               # a 16-bit transfer tensor is not dequantised
+    (dict(dst_dtype=3, cache_dtype=9), K.EINVAL),
+    (dict(dst_dtype=3, cache_dtype=2, head_dim=1024), K.EUNSUPPORTED),   # 2048-byte cache rows
 ])
 def test_plan_rejects(over, status):
     kw = dict(BASE)
@@ -151,6 +158,16 @@ def test_launch_argument_errors_before_device():
     with pytest.raises(K.KvxError) as e:
         K.kvx_repack(fp8, [good], good, None, good, 3)                      # fp8 needs scales
     assert e.value.status == K.EINVAL
+    # a dequantising plan's cache holds no scales, whatever the transfer tensor carries
+    dq = K.kvx_plan(K.make_desc(**dict(BASE, dst_dtype=3, cache_dtype=2)))
+    for call in (lambda: K.kvx_repack(dq, [good], good, good, good, 3),
+                 lambda: K.kvx_unpack(dq, good, good, good, good, 3)):
+        with pytest.raises(K.KvxError) as e:
+            call()
+        assert e.value.status == K.EINVAL and "scales" in K.kvx_last_error()
+    # the same cache dtype named explicitly is the plain plan
+    same = K.kvx_plan(K.make_desc(**dict(BASE, dst_dtype=3, cache_dtype=3)))
+    assert K.kvx_plan_info_get(same).write_bytes_unpack == K.kvx_plan_info_get(fp8).write_bytes_unpack
 
 
 def test_merge_needs_every_overlapping_shard():

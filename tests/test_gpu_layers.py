@@ -90,7 +90,7 @@ def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
     whole = oracle_problem(O, w, lens, L)
     want_c = np.full(O.cache_bytes(whole), W.SENTINEL, dtype=np.uint8)
     want_s = None
-    if w.dst_dtype == "e4m3fn":
+    if w.cdt == "e4m3fn":
         want_s = np.full(4 * O.scale_count(whole), W.SENTINEL, dtype=np.uint8).view(np.float32)
     O.repack(whole, W.source_shards(w, lens, 0, L), want_c, want_s, bt, stride)
 
@@ -107,7 +107,7 @@ def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
         cache = torch.full((rows * w.head_dim * dst_size(w),), W.SENTINEL, dtype=torch.uint8,
                            device=DEV)
         scales = None
-        if w.dst_dtype == "e4m3fn":
+        if w.cdt == "e4m3fn":
             scales = torch.full((rows * 4,), W.SENTINEL, dtype=torch.uint8,
                                 device=DEV).view(torch.float32)
         for (s0, sn), dsh in zip(src_st, src_bufs):

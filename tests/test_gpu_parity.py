@@ -11,7 +11,8 @@ import numpy as np
 import pytest
 import torch
 
-from cases import FULL, SMALL, inputs, oracle_problem, read_shards
+from cases import (FULL, SMALL, e4m3_sweep_rows, inputs, oracle_problem, pad_rows,
+                   read_shards, sweep_case)
 from gpu_util import (DEV, check_sampled, check_unused_pages, gpu_run, log, oracle_pool)
 
 import oracle as O
@@ -112,28 +113,9 @@ def test_empty_batch_is_a_no_op():
 
 # ---- cast sweeps --------------------------------------------------------------------
 
-def _sweep_case(src, dst, rows_bits):
-    """One request whose 2*T rows (layer 0, k then v) are the given rows
-    (uint16 [2T, 128]); TP1, one head, 16-token pages in order."""
-    n = rows_bits.shape[0]
-    assert n % 32 == 0
-    T = n // 2
-    w = W.Workload("sweep", 1, 1, 1, 128, 1, 1, 0, src, dst, "thd", 16, T // 16, 1, T, T, seed=1)
-    lens = np.array([T], dtype=np.int32)
-    bt = np.arange(T // 16, dtype=np.int32)[None, :]
-    return w, lens, bt, [np.ascontiguousarray(rows_bits.reshape(-1))]
-
-
-def _pad_rows(rows):
-    n = -(-rows.shape[0] // 32) * 32
-    out = np.zeros((n, 128), dtype=np.uint16)
-    out[:rows.shape[0]] = rows
-    return out
-
-
 def test_fp16_to_bf16_every_pattern():
     rows = np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(512, 128)
-    w, lens, bt, shards = _sweep_case("fp16", "bf16", rows)
+    w, lens, bt, shards = sweep_case("fp16", "bf16", rows)
     log("fp16->bf16 all 65536 patterns")
     cache, _, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
     want, _ = oracle_pool(w, lens, bt, bt.shape[1], shards)
@@ -142,42 +124,11 @@ def test_fp16_to_bf16_every_pattern():
 
 def test_bf16_to_fp16_every_pattern():
     rows = np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(512, 128)
-    w, lens, bt, shards = _sweep_case("bf16", "fp16", rows)
+    w, lens, bt, shards = sweep_case("bf16", "fp16", rows)
     log("bf16->fp16 all 65536 patterns")
     cache, _, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
     want, _ = oracle_pool(w, lens, bt, bt.shape[1], shards)
     assert _eq(cache.cpu().numpy(), want)
-
-
-def _e4m3_rows(fmt, amaxes, rng):
-    """Rows [amax, x_1..x_127] covering every finite pattern x with |x| <= amax
-    (both signs) for each amax, plus NaN/Inf/zero rows."""
-    allp = np.arange(65536, dtype=np.uint32).astype(np.uint16)
-    inf = 0x7C00 if fmt == "fp16" else 0x7F80
-    mag = allp & 0x7FFF
-    finite = allp[mag < inf]
-    out = []
-    for a in amaxes:
-        xs = finite[(finite & 0x7FFF) <= a]
-        xs = rng.permutation(xs)
-        k = -(-xs.size // 127)
-        xs = np.concatenate([xs, np.zeros(k * 127 - xs.size, np.uint16)]).reshape(k, 127)
-        pos = rng.integers(0, 128, k)
-        rows = np.empty((k, 128), np.uint16)
-        for j in range(k):
-            rows[j] = np.insert(xs[j], pos[j], a | (rng.integers(0, 2) << 15))
-        out.append(rows)
-    special = np.zeros((6, 128), np.uint16)
-    special[1, :] = 0x8000                         # all -0
-    special[2, 5] = inf | 0x1                      # a NaN in a zero row
-    special[3, :] = 0x3C00 if fmt == "fp16" else 0x3F80
-    special[3, 7] = inf                            # +Inf sets the row maximum
-    special[4, :64] = (inf | 0x40) | 0x8000        # half NaN, rest zero
-    special[5, :] = rng.integers(0, 0x7800, 128)
-    special[5, 9] = inf | 0x20                     # one NaN among finite values
-    special[5, 11] = inf | 0x8000                  # and -Inf: the row maximum is Inf
-    out.append(special)
-    return np.concatenate(out)
 
 
 @pytest.mark.parametrize("fmt", ["bf16", "fp16"])
@@ -193,8 +144,8 @@ def test_e4m3_sweep(fmt):
     else:
         amaxes = sorted(set([0x0001, 0x0200, 0x03FF, 0x0400, 0x3C00, 0x5F00, 0x5EFF, 0x7BFF,
                              0x1000, 0x2000]) | set(rng.integers(1, 0x7C00, 24).tolist()))
-    rows = _pad_rows(_e4m3_rows(fmt, amaxes, rng))
-    w, lens, bt, shards = _sweep_case(fmt, "e4m3fn", rows)
+    rows = pad_rows(e4m3_sweep_rows(fmt, amaxes, rng))
+    w, lens, bt, shards = sweep_case(fmt, "e4m3fn", rows)
     log(f"{fmt}->e4m3fn sweep: {rows.shape[0]} rows, {len(amaxes)} row maxima")
     cache, scales, _ = gpu_run("repack", w, lens, bt, bt.shape[1], shards)
     want_c, want_s = oracle_pool(w, lens, bt, bt.shape[1], shards)

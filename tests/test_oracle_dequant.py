@@ -8,7 +8,8 @@ import numpy as np
 import pytest
 import torch
 
-from cases import SMALL_DEQUANT, consumer_rows, dst_size, gather_pages, inputs, oracle_problem
+from cases import (SMALL_DEQUANT, consumer_rows, double_rounding_scales, dst_size, gather_pages,
+                   inputs, oracle_problem)
 
 import oracle as O
 import workload as W
@@ -19,10 +20,14 @@ _TDT = {O.BF16: torch.bfloat16, O.FP16: torch.float16}
 @pytest.mark.parametrize("fmt", [O.BF16, O.FP16])
 def test_dequant_every_code_vs_torch(fmt):
     """All 256 codes under 200 scales (2^-40 .. 2^30, random mantissas, plus
-    exact powers of two): bits equal torch's q.float() * s then .to(); NaN
-    codes give the quiet NaN with the code's sign."""
+    exact powers of two) and the scales whose products round differently
+    through fp32 than at once: bits equal torch's q.float() * s then .to()
+    (an fp32 product, then the 16-bit cast); NaN codes give the quiet NaN
+    with the code's sign."""
     rng = np.random.default_rng(7)
-    scales = np.concatenate([2.0 ** rng.uniform(-40, 30, 190), 2.0 ** np.arange(-10, 0)])
+    dr = double_rounding_scales(11 if fmt == O.FP16 else 8)
+    assert len(dr) >= 8
+    scales = np.concatenate([2.0 ** rng.uniform(-40, 30, 190), 2.0 ** np.arange(-10, 0), dr])
     codes = np.arange(256, dtype=np.uint8)
     nan = (codes & 0x7F) == 0x7F
     canon = 0x7FC0 if fmt == O.BF16 else 0x7E00

@@ -193,6 +193,10 @@ WORKLOADS = {
         # the Llama-3-8B workload (same seed and values) cast bf16 -> fp16
         Workload("llama3_8b_bf16_fp16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "fp16", "thd",
                  16, 65536, 16, 512, 4096, seed=17543),
+        # the Llama-3-8B workload (same seed and values) moved as e4m3fn codes
+        # with per-(token, head) scales and dequantised into a bf16 cache
+        Workload("llama3_8b_bf16_e4m3_bf16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "e4m3fn",
+                 "thd", 16, 65536, 16, 512, 4096, seed=17543, cache_dtype="bf16"),
     ]
 }
 
