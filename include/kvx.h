@@ -165,8 +165,8 @@ typedef struct {
  * unknown dtype.
  * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
  * fp16->bf16, bf16->fp16, fp16->e4m3fn, bf16->e4m3fn}; a cache_dtype other
- * than dst_dtype unless dst_dtype is e4m3fn; a cache row (head_dim * cache
- * element size) above 1024 bytes; more than 1024 heads per decode rank; more than
+ * than dst_dtype unless dst_dtype is e4m3fn; a transfer-tensor row (head_dim
+ * * dst element size) above 1024 bytes; more than 1024 heads per decode rank; more than
  * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
  * (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if
  * the table cannot be allocated. */

@@ -18,9 +18,9 @@ struct kvx_plan_s {
     int cache_dtype = 0, esz_cache = 0;  // the cache's element type (dst_dtype unless dequantising)
     bool dequant = false;                // e4m3fn transfer tensor, 16-bit cache
     std::vector<int> read_shards;  // prefill shards the decode rank reads, in slot order
-    // lanes per row for transfer-tensor rows (pack) and cache rows (unpack,
-    // repack), and workgroup passes per (page, segment) of each operation
-    int cpr = 0, lg_lpr = 0, cpr_c = 0, lg_c = 0, parts = 0, parts_repack = 0, parts_unpack = 0;
+    // lanes per row (from the transfer-tensor row; a dequantising lane covers
+    // two 16-byte cache chunks) and workgroup passes per (page, segment)
+    int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
     std::vector<kvx::Segment> segs;  // head segments of the decode rank
     int32_t max_blocks = 0;
     int32_t max_src_blocks = 0;   // paged sources: pages per request on the prefill side

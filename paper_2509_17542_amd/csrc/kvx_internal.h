@@ -96,7 +96,7 @@ struct KArgs {
     int32_t head_dim;
     int32_t row_dst_bytes;            // pack: transfer-tensor row bytes; else cache row bytes
     int32_t row_wire_bytes;           // transfer-tensor row bytes (the unpack's source rows)
-    int32_t cpr;                      // 16-byte destination chunks per row
+    int32_t cpr;                      // 16-byte transfer-tensor chunks per row
     int32_t lg_lpr;                   // log2(lanes per row), lanes per row >= cpr
     // paged sources: the prefill side's pages
     const int32_t* sbt;               // source block table [requests][sbt_stride]

@@ -380,9 +380,15 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     constexpr bool kScalesIn = CONV == kCopy8 || kDq;                  // unpack reads row scales
     constexpr bool kScales = kFp8 || CONV == kCopy8;                   // rows written with a scale
     constexpr bool kToBf16 = CONV == kDq8Bf16 || CONV == kQdBf16Bf16 || CONV == kQdF16Bf16;
-    constexpr int kVecs = kFp8 ? 2 : 1;                       // 16-byte loads per lane
+    // Lanes follow the transfer-tensor row: lane `sub` of a row owns its 16-byte
+    // chunk sub.  A dequantising lane owns the 16 codes of chunk sub and writes
+    // them as the two 16-byte cache chunks sub and sub + cpr (and reads, for
+    // the repack, the source chunks at the same places), so each load and
+    // each store instruction covers one contiguous half row.
+    constexpr bool kHalves = kDq || kQd;
+    constexpr int kVecs = (kFp8 || kQd) ? 2 : 1;              // 16-byte loads per lane
     constexpr int kSrcEsz = CONV == kCopy8 ? 1 : 2;
-    constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;
+    constexpr int kLaneElems = (kFp8 || CONV == kCopy8) ? 16 : 8;  // at the lane's first load
     static_assert(!kDq || MODE == kUnpack, "dequantisation reads the transfer tensor");
     static_assert(!kQd || MODE == kRepack, "quantise + dequantise is a repack");
     // Issue order.  "Early": the page lookups are scalar loads issued before
@@ -454,7 +460,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     const float* sp = nullptr;
     if constexpr (MODE == kUnpack) {
         base = static_cast<const char*>(a.wire_in);
-        // a dequantising lane reads the 8 codes of its 16 output bytes
+        // a dequantising lane reads 8 codes at sub * 8 and 8 at (sub + cpr) * 8
         p = base + it.wire_data + (row0 + row) * a.row_wire_bytes + sub * (kDq ? 8 : 16);
         if constexpr (kScalesIn)
             sp = reinterpret_cast<const float*>(base + it.wire_scale) + row0 + row;
@@ -483,17 +489,21 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         p = base + (it.src_base + e * a.head_dim) * kSrcEsz + sub * (kLaneElems * kSrcEsz);
     }
 
+    // byte distance from a lane's first load to its second
+    const int second = kHalves ? a.cpr * (kDq ? 8 : 16) : 16;
     uint4 v[kVecs];
     float sc = 0.0f;
     if constexpr (kEarly) {
         // lanes without a row read the buffer's first vector (valid, cached)
         const char* pl = ok ? p : base;
         if constexpr (kDq) {
-            const uint2 c = *reinterpret_cast<const uint2*>(pl);
-            v[0] = make_uint4(c.x, c.y, 0u, 0u);
+            const uint2 c0 = *reinterpret_cast<const uint2*>(pl);
+            const uint2 c1 = *reinterpret_cast<const uint2*>(pl + (ok ? second : 0));
+            v[0] = make_uint4(c0.x, c0.y, c1.x, c1.y);
         } else {
 #pragma unroll
-            for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(pl)[k];
+            for (int k = 0; k < kVecs; ++k)
+                v[k] = *reinterpret_cast<const uint4*>(pl + (ok ? k * second : 0));
         }
         if constexpr (MODE == kUnpack && kScalesIn)
             sc = *(ok ? sp : reinterpret_cast<const float*>(base));
@@ -509,11 +519,13 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         for (int k = 0; k < kVecs; ++k) v[k] = make_uint4(0u, 0u, 0u, 0u);
         if (ok) {
             if constexpr (kDq) {
-                const uint2 c = *reinterpret_cast<const uint2*>(p);
-                v[0] = make_uint4(c.x, c.y, 0u, 0u);
+                const uint2 c0 = *reinterpret_cast<const uint2*>(p);
+                const uint2 c1 = *reinterpret_cast<const uint2*>(p + second);
+                v[0] = make_uint4(c0.x, c0.y, c1.x, c1.y);
             } else {
 #pragma unroll
-                for (int k = 0; k < kVecs; ++k) v[k] = reinterpret_cast<const uint4*>(p)[k];
+                for (int k = 0; k < kVecs; ++k)
+                    v[k] = *reinterpret_cast<const uint4*>(p + k * second);
             }
             if constexpr (MODE == kUnpack && kScalesIn)
                 if (kDq || sub == 0) sc = *sp;  // every dequantising lane needs the scale
@@ -536,16 +548,18 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         if constexpr (kScales) sbase = a.dscale + cplane * a.plane_scales + page_rows;
     }
 
-    uint4 out;
+    uint4 out, out2;  // out2: a dequantising lane's second cache chunk
     if constexpr (kFp8) {
         out = to_e4m3<CONV>(v, lg, sc);  // every lane takes part in the row reduction
     } else if constexpr (kQd) {
-        const uint32_t w[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
-        uint32_t c[2];
-        e4m3_codes<CONV, 4>(w, lg, sc, c);  // every lane takes part in the row reduction
+        const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+        uint32_t c[4];
+        e4m3_codes<CONV, 8>(w, lg, sc, c);  // every lane takes part in the row reduction
         out = dequant8<kToBf16>(c[0], c[1], sc);
+        out2 = dequant8<kToBf16>(c[2], c[3], sc);
     } else if constexpr (kDq) {
         out = dequant8<kToBf16>(v[0].x, v[0].y, sc);
+        out2 = dequant8<kToBf16>(v[0].z, v[0].w, sc);
     } else if constexpr (CONV == kF16Bf16)
         out = to_bf16x8(v[0]);
     else if constexpr (CONV == kBf16F16)
@@ -554,9 +568,12 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         out = v[0];
     if (ok) {
         typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+        char* drow = dbase + int64_t(row) * a.row_dst_bytes;
         __builtin_nontemporal_store(__builtin_bit_cast(v4u, out),
-                                    reinterpret_cast<v4u*>(dbase + int64_t(row) * a.row_dst_bytes +
-                                                           sub * 16));
+                                    reinterpret_cast<v4u*>(drow + sub * 16));
+        if constexpr (kHalves)
+            __builtin_nontemporal_store(__builtin_bit_cast(v4u, out2),
+                                        reinterpret_cast<v4u*>(drow + (sub + a.cpr) * 16));
         if constexpr (kScales)
             if (sub == 0) __builtin_nontemporal_store(sc, sbase + row);
     }

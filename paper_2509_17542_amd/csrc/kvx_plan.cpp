@@ -115,8 +115,9 @@ kvx_status validate(const kvx_desc* d)
         (int64_t(d->head_dim) * dtype_size(d->dst_dtype)) % 16)
         return fail(KVX_EINVAL, "head_dim %d: rows must be whole 16-byte vectors on both sides",
                     d->head_dim);
-    if (int64_t(d->head_dim) * dtype_size(cdt) > 16 * kvx::kMaxRowChunks)
-        return fail(KVX_EUNSUPPORTED, "cache rows above %d bytes", 16 * kvx::kMaxRowChunks);
+    if (int64_t(d->head_dim) * dtype_size(d->dst_dtype) > 16 * kvx::kMaxRowChunks)
+        return fail(KVX_EUNSUPPORTED, "transfer-tensor rows above %d bytes",
+                    16 * kvx::kMaxRowChunks);
     if (d->num_kv_heads / d->dst_tp > kvx::kMaxHeadsPerRank)
         return fail(KVX_EUNSUPPORTED, "more than %d heads per decode rank", kvx::kMaxHeadsPerRank);
     if (d->num_kv_heads / d->src_tp > 65535)
@@ -190,12 +191,10 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     }
     for (kvx::Segment& g : p->segs) g.div_n = kvx::make_fastdiv(uint32_t(g.n));
 
-    // lanes per row: the smallest power of two covering the row's 16-byte
-    // chunks (transfer-tensor rows for the pack, cache rows otherwise)
+    // lanes per row: the smallest power of two covering the transfer-tensor
+    // row's 16-byte chunks (a dequantising lane writes two cache chunks)
     p->cpr = d.head_dim * p->esz_dst / 16;
     while ((1 << p->lg_lpr) < p->cpr) ++p->lg_lpr;
-    p->cpr_c = d.head_dim * p->esz_cache / 16;
-    while ((1 << p->lg_c) < p->cpr_c) ++p->lg_c;
 
     // requests: source offsets, transfer-tensor segments, work items
     const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
@@ -230,16 +229,13 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         p->elems_rows += rows;
     }
     p->wire_bytes = uint64_t(align256(wire));
-    // rows per workgroup pass: of the transfer tensor (pack), of the cache
-    const int64_t rpp = kvx::kThreads >> p->lg_lpr, rpp_c = kvx::kThreads >> p->lg_c;
+    const int64_t rpp = kvx::kThreads >> p->lg_lpr;  // rows per workgroup pass
     int max_n = 0;
     for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
     p->parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
-    p->parts_repack = int32_t((int64_t(d.block_size) * max_n + rpp_c - 1) / rpp_c);
-    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp_c - 1) / rpp_c);
-    const int64_t most = std::max<int64_t>(
-        int64_t(std::max(p->parts, p->parts_repack)) * int64_t(p->segs.size()), p->parts_unpack);
-    if (nitems * L2 * most > kvx::kMaxUnits) {
+    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp - 1) / rpp);
+    if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * int64_t(p->segs.size()),
+                                        p->parts_unpack) > kvx::kMaxUnits) {
         delete p;
         return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers x parts)",
                     (long long)kvx::kMaxUnits);
@@ -455,7 +451,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
         a.seg[0] = kvx::Segment{0, 0, 0, p->hd, kvx::make_fastdiv(uint32_t(p->hd))};
     } else {
         a.num_segs = uint32_t(p->segs.size());
-        a.parts = uint32_t(mode == kvx::kPack ? p->parts : p->parts_repack);
+        a.parts = uint32_t(p->parts);
         for (size_t k = 0; k < p->segs.size(); ++k) a.seg[k] = p->segs[k];
     }
     const int64_t units = int64_t(p->items.size()) * a.planes * a.num_segs * a.parts;
@@ -473,13 +469,10 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     a.hs = p->hs;
     a.hd = p->hd;
     a.head_dim = d.head_dim;
-    // lanes follow the rows written: transfer-tensor rows for the pack,
-    // cache rows otherwise
-    const bool to_wire = mode == kvx::kPack;
     a.row_wire_bytes = d.head_dim * p->esz_dst;
-    a.row_dst_bytes = to_wire ? a.row_wire_bytes : d.head_dim * p->esz_cache;
-    a.cpr = to_wire ? p->cpr : p->cpr_c;
-    a.lg_lpr = to_wire ? p->lg_lpr : p->lg_c;
+    a.row_dst_bytes = mode == kvx::kPack ? a.row_wire_bytes : d.head_dim * p->esz_cache;
+    a.cpr = p->cpr;
+    a.lg_lpr = p->lg_lpr;
     if (mode != kvx::kUnpack && paged) {
         a.sbt = sbt;
         a.sbt_stride = sbt_stride;

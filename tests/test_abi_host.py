@@ -99,7 +99,7 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(num_kv_heads=4096, dst_tp=2), K.EUNSUPPORTED), (dict(num_layers=40000), K.EUNSUPPORTED),
     (dict(cache_dtype=1), K.EUNSUPPORTED),               # a 16-bit transfer tensor is not dequantised
     (dict(dst_dtype=3, cache_dtype=9), K.EINVAL),
-    (dict(dst_dtype=3, cache_dtype=2, head_dim=1024), K.EUNSUPPORTED),   # 2048-byte cache rows
+    (dict(dst_dtype=3, cache_dtype=2, head_dim=2048), K.EUNSUPPORTED),  # 2048-byte e4m3fn rows
 ])
 def test_plan_rejects(over, status):
     kw = dict(BASE)
