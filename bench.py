@@ -108,7 +108,7 @@ def main():
     stage_dshards = [[None if s is None else torch.from_numpy(s.view(np.int16)).cuda() for s in sh]
                      for sh in stage_shards]
     bt_d = torch.from_numpy(bt).cuda()
-    F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
+    F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN, "e5m2": K.E5M2}
     order = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order]
     paged = w.src_order == "paged"
     sbt = sbt_d = None
@@ -126,7 +126,7 @@ def main():
 
     plans = [K.kvx_plan(desc(list(lens), st)) for st in stages]
     infos = [K.kvx_plan_info_get(p) for p in plans]
-    esz = 1 if w.cdt == "e4m3fn" else 2   # the cache's element size
+    esz = 1 if w.cdt in ("e4m3fn", "e5m2") else 2   # the cache's element size
     n_rows = w.layers * 2 * w.num_blocks * w.block_size * w.hd
     cache = torch.empty(n_rows * w.head_dim * esz, dtype=torch.uint8, device="cuda")
     scales = torch.empty(n_rows, dtype=torch.float32, device="cuda") if esz == 1 else None
@@ -397,9 +397,9 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
 
     import oracle as O
 
-    f = {"fp16": O.FP16, "bf16": O.BF16, "e4m3fn": O.E4M3FN}
+    f = {"fp16": O.FP16, "bf16": O.BF16, "e4m3fn": O.E4M3FN, "e5m2": O.E5M2}
     order = {"thd": O.TOKEN_MAJOR, "htd": O.HEAD_MAJOR, "paged": O.PAGED}[w.src_order]
-    esz = 1 if w.cdt == "e4m3fn" else 2   # the cache's element size
+    esz = 1 if w.cdt in ("e4m3fn", "e5m2") else 2   # the cache's element size
     L = stage[1] if stage else w.layers
     done_bytes = 0
     spent = 0.0

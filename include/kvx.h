@@ -18,9 +18,10 @@
  *     (kvx_unpack); kvx_repack does both in one pass when both sides are on
  *     the same device;
  *   - precision alignment (Sec. I, contribution 1, named only): the decode
- *     element type.  Casts round to nearest even; the e4m3fn cast uses a
- *     per-(token, head) fp32 scale max|x| / 448 and saturates at +-448; an
- *     e4m3fn transfer tensor may be dequantised into a 16-bit cache
+ *     element type.  Casts round to nearest even; the 8-bit casts use a
+ *     per-(token, head) fp32 scale max|x| / fmax and saturate at +-fmax
+ *     (e4m3fn: fmax 448, NaN S.1111.111; e5m2: fmax 57344, NaN S.11111.11);
+ *     an 8-bit transfer tensor may be dequantised into a 16-bit cache
  *     (cache_dtype).
  *
  * Layouts (element indices; all dimensions row-major):
@@ -40,9 +41,9 @@
  *     dtype (cache_dtype, else dst_dtype); token
  *     t of request r goes to page block_table[r*bt_stride + t/block_size],
  *     slot t % block_size;
- *   scales (e4m3fn cache only): [dst layer][k/v][num_blocks][block_size][Hd] fp32;
+ *   scales (8-bit cache only): [dst layer][k/v][num_blocks][block_size][Hd] fp32;
  *   transfer tensor: per request, starting on a 256-byte boundary,
- *     [layer][k/v][token][Hd][dim] in dst_dtype, then (e4m3fn only) on the
+ *     [layer][k/v][token][Hd][dim] in dst_dtype, then (8-bit only) on the
  *     next 256-byte boundary [layer][k/v][token][Hd] fp32 scales.
  * Bytes outside these positions (slots past the end of a request's last page,
  * pages not in a block-table row, transfer-tensor padding) are never written.
@@ -75,7 +76,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 5
+#define KVX_ABI_VERSION 6
 
 typedef enum {
     KVX_OK = 0,
@@ -85,7 +86,7 @@ typedef enum {
     KVX_EDEVICE = -4       /* no usable device for the plan, or a HIP error */
 } kvx_status;
 
-typedef enum { KVX_FP16 = 1, KVX_BF16 = 2, KVX_FP8_E4M3FN = 3 } kvx_dtype;
+typedef enum { KVX_FP16 = 1, KVX_BF16 = 2, KVX_FP8_E4M3FN = 3, KVX_FP8_E5M2 = 4 } kvx_dtype;
 
 typedef enum {
     KVX_THD = 0,  /* [token][head][dim] within one (layer, k/v) plane of a request */
@@ -126,16 +127,17 @@ typedef struct {
     int32_t src_layers;
     int32_t dst_layer_offset;
     int32_t dst_layers;
-    /* The decode cache's element type; 0 means dst_dtype.  With an e4m3fn
+    /* The decode cache's element type; 0 means dst_dtype.  With an 8-bit
      * transfer tensor, KVX_BF16 or KVX_FP16 asks for a dequantising unpack
      * (precision alignment, Sec. I, done on the receiving side): each element
-     * of the cache is the product of its e4m3fn code's exact value and the
+     * of the cache is the product of its code's exact value and the
      * row's fp32 scale, computed in fp32 and rounded to nearest even to the
-     * 16-bit type (fp16: overflow to infinity); a NaN code, or a NaN product,
-     * gives that type's quiet NaN (bf16 0x7FC0, fp16 0x7E00) with the code's
-     * sign.  The cache then holds no scales.  The pack and the transfer tensor
-     * are those of the e4m3fn plan; the repack writes what its pack followed
-     * by this unpack would. */
+     * 16-bit type (fp16: overflow to infinity; an e5m2 infinity code gives
+     * an infinite product); a NaN code, or a NaN product, gives that type's
+     * quiet NaN (bf16 0x7FC0, fp16 0x7E00) with the code's sign.  The cache
+     * then holds no scales.  The pack and the transfer tensor are those of
+     * the plain 8-bit plan; the repack writes what its pack followed by this
+     * unpack would. */
     int32_t cache_dtype;
 } kvx_desc;
 
@@ -164,8 +166,9 @@ typedef struct {
  * head_dim * element size not a multiple of 16 bytes on either side; an
  * unknown dtype.
  * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
- * fp16->bf16, bf16->fp16, fp16->e4m3fn, bf16->e4m3fn}; a cache_dtype other
- * than dst_dtype unless dst_dtype is e4m3fn; a transfer-tensor row (head_dim
+ * fp16->bf16, bf16->fp16, fp16/bf16->e4m3fn, fp16/bf16->e5m2}; a cache_dtype
+ * other than dst_dtype unless dst_dtype is 8-bit and cache_dtype 16-bit; a
+ * transfer-tensor row (head_dim
  * * dst element size) above 1024 bytes; more than 1024 heads per decode rank; more than
  * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
  * (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if
@@ -175,7 +178,7 @@ kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);
 kvx_status kvx_plan_info_get(const kvx_plan_t *plan, kvx_plan_info *info);
 
 /* Byte offsets of request r's data and scale regions in the transfer tensor
- * (scale_off = -1 unless dst is e4m3fn).  KVX_EINVAL for r out of range. */
+ * (scale_off = -1 unless dst is 8-bit).  KVX_EINVAL for r out of range. */
 kvx_status kvx_plan_segment(const kvx_plan_t *plan, int32_t r, int64_t *data_off,
                             int64_t *scale_off);
 
@@ -201,7 +204,7 @@ kvx_status kvx_pack(const kvx_plan_t *plan, const void *const *src_shards, void 
  * cache_dtype asks for the dequantisation described at kvx_desc.
  *   cache:       device [L][2][num_blocks][block_size][Hd][D] cache dtype, 16-byte aligned.
  *   scales:      device [L][2][num_blocks][block_size][Hd] fp32, 16-byte aligned;
- *                non-NULL if and only if the cache dtype is e4m3fn.
+ *                non-NULL if and only if the cache dtype is 8-bit.
  *   block_table: device int32 [num_requests][bt_stride]; the first
  *                ceil(T_r/block_size) entries of row r are used.  Contents are a
  *                caller contract (kvx_check_block_table checks them on the

@@ -21,9 +21,10 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "kvx_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
-FP16, BF16, E4M3FN = 1, 2, 3
+FP16, BF16, E4M3FN, E5M2 = 1, 2, 3, 4
 TOKEN_MAJOR, HEAD_MAJOR, PAGED = 0, 1, 2
-FMT_SIZE = {FP16: 2, BF16: 2, E4M3FN: 1}
+FMT_SIZE = {FP16: 2, BF16: 2, E4M3FN: 1, E5M2: 1}
+FP8 = (E4M3FN, E5M2)
 
 GCC_CMD = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-fPIC", "-shared",
            "-ffp-contract=off", "-fno-fast-math", "-o", _LIB_PATH, _SRC, "-lm"]
@@ -56,7 +57,11 @@ def lib():
         L.orc_row_scale.argtypes = [vp, ctypes.c_int]
         L.orc_fp16_to_bf16_n.argtypes = [vp, vp, ctypes.c_int64]
         L.orc_bf16_to_fp16_n.argtypes = [vp, vp, ctypes.c_int64]
-        L.orc_dequant_row.argtypes = [ctypes.c_int, ctypes.c_int, vp, ctypes.c_float, vp]
+        L.orc_dequant_row.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, vp,
+                                      ctypes.c_float, vp]
+        L.orc_f32_to_e5m2_n.argtypes = [vp, vp, ctypes.c_int64]
+        L.orc_row_scale_to.restype = ctypes.c_float
+        L.orc_row_scale_to.argtypes = [vp, ctypes.c_int, ctypes.c_float]
         L.orc_src_heads.restype = ctypes.c_int32
         L.orc_src_heads.argtypes = [P(Problem)]
         L.orc_dst_heads.restype = ctypes.c_int32
@@ -172,7 +177,7 @@ def _shard_ptrs(shards):
 # ---- casts -----------------------------------------------------------------
 
 def decode(fmt: int, bits: np.ndarray) -> np.ndarray:
-    bits = np.ascontiguousarray(bits, dtype=np.uint8 if fmt == E4M3FN else np.uint16)
+    bits = np.ascontiguousarray(bits, dtype=np.uint8 if fmt in FP8 else np.uint16)
     out = np.empty(bits.shape, dtype=np.float64)
     lib().orc_decode_n(fmt, _ptr(bits), _ptr(out), bits.size)
     return out
@@ -185,11 +190,13 @@ def fp16_to_bf16(bits: np.ndarray) -> np.ndarray:
     return out
 
 
-def dequant_row(cache_fmt: int, q: np.ndarray, s) -> np.ndarray:
-    """e4m3fn codes (uint8) of one row and their fp32 scale -> 16-bit bits."""
+def dequant_row(cache_fmt: int, q: np.ndarray, s, code_fmt: int = E4M3FN) -> np.ndarray:
+    """8-bit codes (uint8, e4m3fn or e5m2) of one row and their fp32 scale ->
+    16-bit bits."""
     q = np.ascontiguousarray(q, dtype=np.uint8)
     out = np.empty(q.size, dtype=np.uint16)
-    lib().orc_dequant_row(cache_fmt, q.size, _ptr(q), ctypes.c_float(float(s)), _ptr(out))
+    lib().orc_dequant_row(code_fmt, cache_fmt, q.size, _ptr(q), ctypes.c_float(float(s)),
+                          _ptr(out))
     return out
 
 
@@ -207,9 +214,16 @@ def f32_to_e4m3fn(v: np.ndarray) -> np.ndarray:
     return out
 
 
-def row_scale(x: np.ndarray) -> np.float32:
+def f32_to_e5m2(v: np.ndarray) -> np.ndarray:
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    out = np.empty(v.shape, dtype=np.uint8)
+    lib().orc_f32_to_e5m2_n(_ptr(v), _ptr(out), v.size)
+    return out
+
+
+def row_scale(x: np.ndarray, fmax: float = 448.0) -> np.float32:
     x = np.ascontiguousarray(x, dtype=np.float32)
-    return np.float32(lib().orc_row_scale(_ptr(x), x.size))
+    return np.float32(lib().orc_row_scale_to(_ptr(x), x.size, ctypes.c_float(fmax)))
 
 
 def convert_row(src_fmt: int, dst_fmt: int, row_bits: np.ndarray):
@@ -219,7 +233,7 @@ def convert_row(src_fmt: int, dst_fmt: int, row_bits: np.ndarray):
     out = np.empty(D * FMT_SIZE[dst_fmt], dtype=np.uint8)
     sc = np.zeros(1, dtype=np.float32)
     lib().orc_convert_row(src_fmt, dst_fmt, D, _ptr(row_bits), _ptr(out), _ptr(sc))
-    return out, (sc[0] if dst_fmt == E4M3FN else None)
+    return out, (sc[0] if dst_fmt in FP8 else None)
 
 
 # ---- index maps --------------------------------------------------------------
@@ -296,4 +310,4 @@ def expected_rows(p: OracleProblem, shards, r, l, kv, t0, nt, sentinel=0xA5):
     sc = np.full(nt * p.hd * 4, sentinel, dtype=np.uint8).view(np.float32)
     _check(lib().orc_expected_rows(p.ref(), _shard_ptrs(shards), r, l, kv, t0, nt, _ptr(out),
                                    _ptr(sc)))
-    return out, (sc if p.cache_fmt_eff == E4M3FN else None)
+    return out, (sc if p.cache_fmt_eff in FP8 else None)

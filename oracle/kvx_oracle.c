@@ -16,9 +16,9 @@
  *     size and layout;
  *   - precision alignment (named among the module's components in Sec. I):
  *     the decode side's element type.  The paper gives no rounding rule; the
- *     reading taken is IEEE round-to-nearest-even, and for the 8-bit e4m3fn
- *     format a per-(token, head) scale max|x|/448 in fp32 with a saturating
- *     cast.
+ *     reading taken is IEEE round-to-nearest-even, and for the 8-bit
+ *     formats (e4m3fn, e5m2) a per-(token, head) scale max|x| / (the
+ *     format's largest finite value) in fp32 with a saturating cast.
  *
  * Casts are written from the format definitions: decode the bits to an exact
  * real value (double), round that value to the nearest point of the target
@@ -51,16 +51,20 @@ static orc_fmt_desc fmt_desc(int fmt)
     switch (fmt) {
     case ORC_FP16:   f.total_bits = 16; f.exp_bits = 5; f.man_bits = 10; f.bias = 15;  break;
     case ORC_BF16:   f.total_bits = 16; f.exp_bits = 8; f.man_bits = 7;  f.bias = 127; break;
+    case ORC_E5M2:   f.total_bits = 8;  f.exp_bits = 5; f.man_bits = 2;  f.bias = 15;  break;
     default:         f.total_bits = 8;  f.exp_bits = 4; f.man_bits = 3;  f.bias = 7;   break;
     }
     return f;
 }
 
-int orc_fmt_size(int fmt) { return fmt == ORC_E4M3FN ? 1 : 2; }
+int orc_is_fp8(int fmt) { return fmt == ORC_E4M3FN || fmt == ORC_E5M2; }
 
-/* Exact value of an encoded number.  IEEE formats (fp16, bf16): all-ones
- * exponent is Inf (zero fraction) or NaN.  OCP e4m3fn: no Inf; only
- * S.1111.111 is NaN, and exponent field 15 with other fractions is finite. */
+int orc_fmt_size(int fmt) { return orc_is_fp8(fmt) ? 1 : 2; }
+
+/* Exact value of an encoded number.  IEEE-style formats (fp16, bf16 and OCP
+ * e5m2): all-ones exponent is Inf (zero fraction) or NaN.  OCP e4m3fn: no
+ * Inf; only S.1111.111 is NaN, and exponent field 15 with other fractions is
+ * finite. */
 double orc_decode(int fmt, uint32_t bits)
 {
     orc_fmt_desc f = fmt_desc(fmt);
@@ -161,11 +165,12 @@ static uint16_t f32_to_16(int fmt, float v, uint32_t nan_sign)
  * even), then rounded to the cache format.  A NaN code, or a NaN product
  * (0 * Inf in a row whose scale is infinite), gives the quiet NaN with the
  * code's sign. */
-void orc_dequant_row(int cache_fmt, int D, const uint8_t *q, float s, uint16_t *out)
+void orc_dequant_row(int code_fmt, int cache_fmt, int D, const uint8_t *q, float s,
+                     uint16_t *out)
 {
     for (int d = 0; d < D; ++d) {
         uint32_t sign = (q[d] >> 7) & 1u;
-        float x = (float)orc_decode(ORC_E4M3FN, q[d]);   /* exact */
+        float x = (float)orc_decode(code_fmt, q[d]);      /* exact (or +-Inf / NaN) */
         float v = x * s;                                   /* fp32 product */
         out[d] = f32_to_16(cache_fmt, isnan(x) ? NAN : v, sign);
     }
@@ -201,9 +206,26 @@ uint8_t orc_f32_to_e4m3fn(float v)
     return (uint8_t)encode(ORC_E4M3FN, sign, m);
 }
 
+/* fp32 -> OCP e5m2 (1 sign, 5 exponent bits with bias 15, 2 fraction bits;
+ * largest finite value 57344 = 1.75 * 2^15, subnormals m * 2^-16), round to
+ * nearest even, saturating like the e4m3fn cast (reading R26): a magnitude
+ * whose rounding would exceed 57344, an infinity included, gives +-57344.
+ * NaN gives S.11111.11 with the sign kept. */
+uint8_t orc_f32_to_e5m2(float v)
+{
+    uint32_t sign = signbit(v) ? 1u : 0u;
+    if (isnan(v)) return (uint8_t)((sign << 7) | 0x7Fu);
+    double a = fabs((double)v);
+    if (a >= 57344.0) return (uint8_t)encode(ORC_E5M2, sign, 57344.0);
+    double m = rne_to_grid(a, 3, -14);
+    if (m > 57344.0) m = 57344.0; /* unreachable: a < 57344 and 57344 is a grid point */
+    return (uint8_t)encode(ORC_E5M2, sign, m);
+}
+
 /* Per-row scale: the largest magnitude over the row (NaN elements ignored),
- * divided by 448 with one IEEE fp32 divide. */
-float orc_row_scale(const float *x, int n)
+ * divided by fmax, the 8-bit format's largest finite value, with one IEEE
+ * fp32 divide. */
+float orc_row_scale_to(const float *x, int n, float fmax)
 {
     float amax = 0.0f;
     for (int d = 0; d < n; ++d) {
@@ -211,7 +233,14 @@ float orc_row_scale(const float *x, int n)
         float a = fabsf(x[d]);
         if (a > amax) amax = a;
     }
-    return amax / 448.0f;
+    return amax / fmax;
+}
+
+float orc_row_scale(const float *x, int n) { return orc_row_scale_to(x, n, 448.0f); }
+
+void orc_f32_to_e5m2_n(const float *in, uint8_t *out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) out[k] = orc_f32_to_e5m2(in[k]);
 }
 
 void orc_bf16_to_fp16_n(const uint16_t *in, uint16_t *out, int64_t n)
@@ -232,7 +261,7 @@ void orc_f32_to_e4m3fn_n(const float *in, uint8_t *out, int64_t n)
 void orc_decode_n(int fmt, const void *in, double *out, int64_t n)
 {
     for (int64_t k = 0; k < n; ++k) {
-        uint32_t b = (fmt == ORC_E4M3FN) ? ((const uint8_t *)in)[k] : ((const uint16_t *)in)[k];
+        uint32_t b = orc_is_fp8(fmt) ? ((const uint8_t *)in)[k] : ((const uint16_t *)in)[k];
         out[k] = orc_decode(fmt, b);
     }
 }
@@ -255,12 +284,13 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
         for (int d = 0; d < D; ++d) o[d] = orc_bf16_to_fp16(s[d]);
         return;
     }
-    /* 16-bit float -> e4m3fn with a per-row fp32 scale */
+    /* 16-bit float -> e4m3fn or e5m2 with a per-row fp32 scale */
+    int e5 = dst_fmt == ORC_E5M2;
     float *x = (float *)calloc((size_t)D, sizeof(float));
     uint8_t *o = (uint8_t *)dst_row;
     if (!x) abort();
     for (int d = 0; d < D; ++d) x[d] = (float)orc_decode(src_fmt, s[d]); /* exact widening */
-    float sc = orc_row_scale(x, D);
+    float sc = orc_row_scale_to(x, D, e5 ? 57344.0f : 448.0f);
     *scale = sc;
     for (int d = 0; d < D; ++d) {
         uint32_t sign = (s[d] >> 15) & 1u;
@@ -273,7 +303,8 @@ void orc_convert_row(int src_fmt, int dst_fmt, int D, const void *src_row, void 
             /* An invalid quotient (Inf / Inf, in a row whose maximum is
              * infinite) has no defined sign; it takes the element's sign, as
              * every other quotient does (the scale is positive). */
-            o[d] = isnan(v) ? (uint8_t)((sign << 7) | 0x7Fu) : orc_f32_to_e4m3fn(v);
+            o[d] = isnan(v) ? (uint8_t)((sign << 7) | 0x7Fu)
+                            : (e5 ? orc_f32_to_e5m2(v) : orc_f32_to_e4m3fn(v));
         }
     }
     free(x);
@@ -319,12 +350,12 @@ int orc_validate(const orc_problem *p)
     int sf = p->src_fmt, df = p->dst_fmt, cf = orc_cache_fmt(p);
     if (sf != ORC_FP16 && sf != ORC_BF16) return -2;
     /* a cache format other than the transfer format: only the dequantising
-     * unpack e4m3fn -> fp16 / bf16 */
-    if (cf != df && !(df == ORC_E4M3FN && (cf == ORC_FP16 || cf == ORC_BF16))) return -2;
+     * unpack of 8-bit codes (e4m3fn, e5m2) into fp16 / bf16 */
+    if (cf != df && !(orc_is_fp8(df) && (cf == ORC_FP16 || cf == ORC_BF16))) return -2;
     if (sf == df) return 0;
     if (sf == ORC_FP16 && df == ORC_BF16) return 0;
     if (sf == ORC_BF16 && df == ORC_FP16) return 0;
-    if (df == ORC_E4M3FN) return 0;
+    if (orc_is_fp8(df)) return 0;
     return -2;
 }
 
@@ -420,7 +451,7 @@ static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 /* Transfer tensor: request-major segments, each starting on a 256-byte
  * boundary; a segment is [layer][k/v][token][Hd][dim] in the destination type,
- * then (e4m3fn only) [layer][k/v][token][Hd] fp32 scales on the next 256-byte
+ * then (8-bit formats only) [layer][k/v][token][Hd] fp32 scales on the next 256-byte
  * boundary.  Returns the total size in bytes. */
 int64_t orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_off)
 {
@@ -432,7 +463,7 @@ int64_t orc_wire_layout(const orc_problem *p, int64_t *data_off, int64_t *scale_
         off = align256(off);
         if (data_off) data_off[r] = off;
         off += rows * p->head_dim * esz;
-        if (p->dst_fmt == ORC_E4M3FN) {
+        if (orc_is_fp8(p->dst_fmt)) {
             off = align256(off);
             if (scale_off) scale_off[r] = off;
             off += rows * 4;
@@ -482,7 +513,7 @@ int orc_pack(const orc_problem *p, const void *const *shards, void *wire)
                         float sc = 0.0f;
                         if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
                                                  w + doff[r] + row * D * esz, &sc) &&
-                            p->dst_fmt == ORC_E4M3FN)
+                            orc_is_fp8(p->dst_fmt))
                             memcpy(w + soff[r] + row * 4, &sc, 4);
                     }
     }
@@ -517,13 +548,13 @@ int orc_unpack(const orc_problem *p, const void *wire, void *cache, float *scale
                         if (cf != p->dst_fmt) {   /* dequantise the row */
                             float sc;
                             memcpy(&sc, w + soff[r] + row * 4, 4);
-                            orc_dequant_row(cf, D, w + doff[r] + row * D * esz, sc,
+                            orc_dequant_row(p->dst_fmt, cf, D, w + doff[r] + row * D * esz, sc,
                                             (uint16_t *)(c + orc_cache_index(p, b, l, kv, slot, i, 0) * cesz));
                             continue;
                         }
                         memcpy(c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
                                w + doff[r] + row * D * esz, (size_t)(D * esz));
-                        if (p->dst_fmt == ORC_E4M3FN)
+                        if (orc_is_fp8(p->dst_fmt))
                             memcpy(&scales[orc_cache_scale_index(p, b, l, kv, slot, i)],
                                    w + soff[r] + row * 4, 4);
                     }
@@ -557,14 +588,14 @@ int orc_repack(const orc_problem *p, const void *const *shards, void *cache, flo
                         float sc = 0.0f;
                         if (cf != p->dst_fmt) {   /* quantise, then dequantise into the cache */
                             if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, q, &sc))
-                                orc_dequant_row(cf, D, q, sc,
+                                orc_dequant_row(p->dst_fmt, cf, D, q, sc,
                                                 (uint16_t *)(c + orc_cache_index(p, b, l, kv, slot, i, 0) * 2));
                             continue;
                         }
                         if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp,
                                                  c + orc_cache_index(p, b, l, kv, slot, i, 0) * esz,
                                                  &sc) &&
-                            p->dst_fmt == ORC_E4M3FN)
+                            orc_is_fp8(p->dst_fmt))
                             scales[orc_cache_scale_index(p, b, l, kv, slot, i)] = sc;
                     }
                 }
@@ -594,11 +625,11 @@ int orc_expected_rows(const orc_problem *p, const void *const *shards, int r, in
             float sc = 0.0f;
             if (cf != p->dst_fmt) {
                 if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, q, &sc))
-                    orc_dequant_row(cf, D, q, sc, (uint16_t *)(o + row * D * 2));
+                    orc_dequant_row(p->dst_fmt, cf, D, q, sc, (uint16_t *)(o + row * D * 2));
                 continue;
             }
             if (source_row_converted(p, shards, base, r, l, kv, t, i, tmp, o + row * D * esz, &sc) &&
-                p->dst_fmt == ORC_E4M3FN && out_scales)
+                orc_is_fp8(p->dst_fmt) && out_scales)
                 out_scales[row] = sc;
         }
     free(tmp);

@@ -25,7 +25,7 @@ extern "C" {
 #endif
 
 /* element formats */
-enum { ORC_FP16 = 1, ORC_BF16 = 2, ORC_E4M3FN = 3 };
+enum { ORC_FP16 = 1, ORC_BF16 = 2, ORC_E4M3FN = 3, ORC_E5M2 = 4 };
 /* source storage orders: one (layer, k/v) plane of a request stored
  * contiguously, or the prefill side's own paged cache */
 enum {
@@ -43,7 +43,7 @@ typedef struct {
     int32_t dst_tp;      /* tensor-parallel degree of the decode side */
     int32_t dst_rank;    /* which decode rank's head shard is produced */
     int32_t src_fmt;     /* ORC_FP16 or ORC_BF16 */
-    int32_t dst_fmt;     /* ORC_FP16, ORC_BF16 or ORC_E4M3FN */
+    int32_t dst_fmt;     /* ORC_FP16, ORC_BF16, ORC_E4M3FN or ORC_E5M2 */
     int32_t src_order;   /* ORC_TOKEN_MAJOR or ORC_HEAD_MAJOR */
     int32_t block_size;  /* tokens per destination page */
     int64_t num_blocks;  /* pages in the destination pool (per plane) */
@@ -61,8 +61,8 @@ typedef struct {
     int32_t src_layer_offset, src_layers;
     int32_t dst_layer_offset, dst_layers;
     /* Element format of the decode cache; 0 means dst_fmt.  A 16-bit cache
-     * under an e4m3fn dst_fmt is a dequantising unpack: the transfer tensor
-     * carries e4m3fn codes and scales, the cache their values q * s. */
+     * under an 8-bit dst_fmt is a dequantising unpack: the transfer tensor
+     * carries 8-bit codes and scales, the cache their values q * s. */
     int32_t cache_fmt;
 } orc_problem;
 
@@ -70,16 +70,21 @@ typedef struct {
 double   orc_decode(int fmt, uint32_t bits);             /* exact value; NaN/Inf as such */
 uint16_t orc_fp16_to_bf16(uint16_t h);                   /* IEEE round-to-nearest-even */
 uint16_t orc_bf16_to_fp16(uint16_t b);                   /* RNE; overflow to +-Inf */
-/* one e4m3fn row back to a 16-bit format: each value q * s (fp32 product),
- * rounded to nearest even; NaN codes and NaN products give the format's
- * quiet NaN with the code's sign */
-void     orc_dequant_row(int cache_fmt, int D, const uint8_t *q, float s, uint16_t *out);
+/* one row of 8-bit codes (e4m3fn or e5m2) back to a 16-bit format: each
+ * value q * s (fp32 product), rounded to nearest even; NaN codes and NaN
+ * products give the format's quiet NaN with the code's sign */
+void     orc_dequant_row(int code_fmt, int cache_fmt, int D, const uint8_t *q, float s,
+                         uint16_t *out);
 int32_t  orc_cache_fmt(const orc_problem *p);
 void     orc_bf16_to_fp16_n(const uint16_t *in, uint16_t *out, int64_t n);
 uint8_t  orc_f32_to_e4m3fn(float v);                     /* RNE, saturating to +-448 */
+uint8_t  orc_f32_to_e5m2(float v);                       /* RNE, saturating to +-57344 */
 float    orc_row_scale(const float *x, int n);           /* max|x| / 448, fp32 divide */
+float    orc_row_scale_to(const float *x, int n, float fmax); /* max|x| / fmax */
+int      orc_is_fp8(int fmt);                            /* e4m3fn or e5m2 */
 void     orc_fp16_to_bf16_n(const uint16_t *in, uint16_t *out, int64_t n);
 void     orc_f32_to_e4m3fn_n(const float *in, uint8_t *out, int64_t n);
+void     orc_f32_to_e5m2_n(const float *in, uint8_t *out, int64_t n);
 void     orc_decode_n(int fmt, const void *in, double *out, int64_t n);
 /* convert one row of D source elements to the destination format; *scale is
  * written only for an e4m3fn destination */

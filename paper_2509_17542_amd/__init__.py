@@ -25,13 +25,13 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # the struct layouts below are those of this version of include/kvx.h
-ABI_VERSION = 5
+ABI_VERSION = 6
 if _lib.kvx_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements kvx ABI {_lib.kvx_abi_version()}, this binding "
                       f"ABI {ABI_VERSION}: rebuild the library")
 
 OK, EINVAL, EUNSUPPORTED, ENOMEM, EDEVICE = 0, -1, -2, -3, -4
-FP16, BF16, E4M3FN = 1, 2, 3
+FP16, BF16, E4M3FN, E5M2 = 1, 2, 3, 4
 THD, HTD, PAGED = 0, 1, 2
 _STATUS = {0: "KVX_OK", -1: "KVX_EINVAL", -2: "KVX_EUNSUPPORTED", -3: "KVX_ENOMEM",
            -4: "KVX_EDEVICE"}

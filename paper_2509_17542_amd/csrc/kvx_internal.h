@@ -46,7 +46,7 @@ enum Conv : int {
     kF16Bf16 = 1,   // fp16 -> bf16, round to nearest even
     kBf16E4m3 = 2,  // bf16 -> e4m3fn with per-row scale
     kF16E4m3 = 3,   // fp16 -> e4m3fn with per-row scale
-    kCopy8 = 4,     // 8-bit bits unchanged (+ scale copy), unpack of e4m3fn
+    kCopy8 = 4,     // 8-bit bits unchanged (+ scale copy), unpack of an 8-bit format
     kBf16F16 = 5,   // bf16 -> fp16, round to nearest even, overflow to infinity
     // dequantising unpack: e4m3fn transfer tensor (+ scales) -> 16-bit cache
     kDq8Bf16 = 6,
@@ -55,7 +55,16 @@ enum Conv : int {
     kQdBf16Bf16 = 8,
     kQdF16Bf16 = 9,
     kQdBf16F16 = 10,
-    kQdF16F16 = 11
+    kQdF16F16 = 11,
+    // the same with OCP e5m2 codes (scale max|x| / 57344)
+    kBf16E5m2 = 12,
+    kF16E5m2 = 13,
+    kDq5Bf16 = 14,
+    kDq5F16 = 15,
+    kQd5Bf16Bf16 = 16,
+    kQd5F16Bf16 = 17,
+    kQd5Bf16F16 = 18,
+    kQd5F16F16 = 19
 };
 
 // A run of the decode rank's heads that comes from one source shard: decode

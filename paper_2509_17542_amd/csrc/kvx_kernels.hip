@@ -72,6 +72,39 @@ __device__ __forceinline__ uint32_t e4m3_code(float q)
     return ((u + 0x7FFFFu + ((u >> 20) & 1u)) >> 20) - (120u << 3);
 }
 
+// The same for OCP e5m2 (2 fraction bits, bias 15): saturate at 57344
+// (0x7B); below 2^-14 the grid step is 2^-16; above, round the fp32 fraction
+// to 2 bits (ties to even) and rebias the exponent from 127 to 15.
+__device__ __forceinline__ uint32_t e5m2_code(float q)
+{
+    if (q >= 57344.0f) return 0x7Bu;
+    if (q < 0x1p-14f) return static_cast<uint32_t>(__builtin_rintf(q * 65536.0f));
+    const uint32_t u = __float_as_uint(q);
+    return ((u + 0xFFFFFu + ((u >> 21) & 1u)) >> 21) - (112u << 2);
+}
+
+// The 8-bit transfer formats: e4m3fn (kE5 false) and e5m2 (kE5 true).  Both
+// use S.1111111 (0x7F) for NaN, as the conversions write it.
+template <bool kE5>
+struct Fp8 {
+    static constexpr float kMax = kE5 ? 57344.0f : 448.0f;  // largest finite value
+    __device__ static __forceinline__ uint32_t code(float q)
+    {
+        return kE5 ? e5m2_code(q) : e4m3_code(q);
+    }
+    // hardware conversion of two fp32 values into bytes 0-1 (hi false) or
+    // 2-3 (hi true) of `old`, round to nearest even
+    __device__ static __forceinline__ int cvt_pk(float a, float b, int old, bool hi)
+    {
+        if constexpr (kE5)
+            return hi ? __builtin_amdgcn_cvt_pk_bf8_f32(a, b, old, true)
+                      : __builtin_amdgcn_cvt_pk_bf8_f32(a, b, old, false);
+        else
+            return hi ? __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, true)
+                      : __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, false);
+    }
+};
+
 // Correctly rounded a / s for a >= 0 and s in [2^-80, 2^100], given r, the
 // reciprocal of s refined by one Newton step: two remainder corrections
 // (Markstein), the unscaled form of the IEEE fp32 divide sequence.  No
@@ -89,7 +122,16 @@ __device__ __forceinline__ float quotient(float a, float s, float r)
 // source format of a quantising conversion: fp16 or bf16
 constexpr bool f16_source(int conv)
 {
-    return conv == kF16E4m3 || conv == kQdF16Bf16 || conv == kQdF16F16;
+    return conv == kF16E4m3 || conv == kQdF16Bf16 || conv == kQdF16F16 || conv == kF16E5m2 ||
+           conv == kQd5F16Bf16 || conv == kQd5F16F16;
+}
+
+// 8-bit format of a conversion that quantises or dequantises: e5m2, else e4m3fn
+constexpr bool e5_conv(int conv)
+{
+    return conv == kBf16E5m2 || conv == kF16E5m2 || conv == kDq5Bf16 || conv == kDq5F16 ||
+           conv == kQd5Bf16Bf16 || conv == kQd5F16Bf16 || conv == kQd5Bf16F16 ||
+           conv == kQd5F16F16;
 }
 
 template <int CONV>
@@ -107,16 +149,17 @@ struct SrcFmt {
 };
 
 // General path: one lane's 2*NW source elements (NW 32-bit words) -> 2*NW
-// e4m3fn bytes, every case of the definition (NaN elements, zero rows, scales
+// 8-bit codes, every case of the definition (NaN elements, zero rows, scales
 // too small or too large for the two-step divide), element by element in
 // software.  The row maximum is reduced over the lanes-per-row group (2^lg
 // lanes, consecutive, so xor shuffles stay inside the group); every lane of the
 // wave must execute the reduction.
 template <int CONV, int NW>
-__device__ __forceinline__ void e4m3_codes_general(const uint32_t (&w)[NW], int lg,
-                                                   float& scale_out, uint32_t (&out)[NW / 2])
+__device__ __forceinline__ void fp8_codes_general(const uint32_t (&w)[NW], int lg,
+                                                  float& scale_out, uint32_t (&out)[NW / 2])
 {
     using F = SrcFmt<CONV>;
+    using Q = Fp8<e5_conv(CONV)>;
     uint32_t m = 0;
 #pragma unroll
     for (int k = 0; k < NW; ++k) {
@@ -128,7 +171,7 @@ __device__ __forceinline__ void e4m3_codes_general(const uint32_t (&w)[NW], int 
     for (int o = 1; o < (1 << lg); o <<= 1)
         m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
     const float amax = F::widen(m);
-    const float s = amax / 448.0f;  // IEEE divide
+    const float s = amax / Q::kMax;  // IEEE divide
     scale_out = s;
     const bool fast = s >= 0x1p-80f && s <= 0x1p100f;
     const float r0 = __builtin_amdgcn_rcpf(s);
@@ -145,16 +188,16 @@ __device__ __forceinline__ void e4m3_codes_general(const uint32_t (&w)[NW], int 
         } else if (s == 0.0f) {
             code = 0u;                          // every finite element is zero
         } else if (fast) {
-            code = e4m3_code(quotient(F::widen(mag), s, r));
+            code = Q::code(quotient(F::widen(mag), s, r));
         } else {
             const float q = F::widen(mag) / s;  // IEEE divide (tiny, huge or infinite scale)
-            code = q != q ? 0x7Fu : e4m3_code(q);
+            code = q != q ? 0x7Fu : Q::code(q);
         }
         out[k >> 2] |= (code | ((h >> 8) & 0x80u)) << ((k & 3) * 8);
     }
 }
 
-// One lane's 2*NW source elements -> 2*NW e4m3fn bytes.  Fast path for rows with
+// One lane's 2*NW source elements -> 2*NW 8-bit codes.  Fast path for rows with
 // no NaN and a scale in [2^-80, 2^100]: the row maximum from packed 16-bit
 // maxima, the exact quotient |x| / s, the element's sign set on it, and the
 // hardware conversion v_cvt_pk_fp8_f32 (round to nearest even, OCP e4m3fn on
@@ -162,10 +205,11 @@ __device__ __forceinline__ void e4m3_codes_general(const uint32_t (&w)[NW], int 
 // quotient cannot round above 448 because |x| <= amax).  Other rows take the
 // general path.  Every lane of the wave must execute this.
 template <int CONV, int NW>
-__device__ __forceinline__ void e4m3_codes(const uint32_t (&w)[NW], int lg, float& scale_out,
-                                           uint32_t (&out)[NW / 2])
+__device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float& scale_out,
+                                          uint32_t (&out)[NW / 2])
 {
     using F = SrcFmt<CONV>;
+    using Q = Fp8<e5_conv(CONV)>;
     typedef unsigned short us2 __attribute__((ext_vector_type(2)));
     us2 mm = {0, 0};
 #pragma unroll
@@ -174,9 +218,9 @@ __device__ __forceinline__ void e4m3_codes(const uint32_t (&w)[NW], int lg, floa
     uint32_t m = max(uint32_t(mm.x), uint32_t(mm.y));
     for (int o = 1; o < (1 << lg); o <<= 1)
         m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
-    const float s = F::widen(m) / 448.0f;  // IEEE divide; NaN if the row holds a NaN
+    const float s = F::widen(m) / Q::kMax;  // IEEE divide; NaN if the row holds a NaN
     if (!(s >= 0x1p-80f && s <= 0x1p100f)) {
-        e4m3_codes_general<CONV, NW>(w, lg, scale_out, out);
+        fp8_codes_general<CONV, NW>(w, lg, scale_out, out);
         return;
     }
     scale_out = s;
@@ -191,22 +235,22 @@ __device__ __forceinline__ void e4m3_codes(const uint32_t (&w)[NW], int lg, floa
             q[e] = __uint_as_float(__float_as_uint(quotient(F::widen(h & 0x7FFFu), s, r)) |
                                    ((h & 0x8000u) << 16));
         }
-        const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
-        out[d] = uint32_t(__builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true));
+        const int lo = Q::cvt_pk(q[0], q[1], 0, false);
+        out[d] = uint32_t(Q::cvt_pk(q[2], q[3], lo, true));
     }
 }
 
-// One lane's 16 source elements (two 16-byte vectors) -> 16 e4m3fn bytes.
+// One lane's 16 source elements (two 16-byte vectors) -> 16 8-bit codes.
 template <int CONV>
-__device__ __forceinline__ uint4 to_e4m3(const uint4 (&v)[2], int lg, float& scale_out)
+__device__ __forceinline__ uint4 to_fp8(const uint4 (&v)[2], int lg, float& scale_out)
 {
     const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
     uint32_t out[4];
-    e4m3_codes<CONV, 8>(w, lg, scale_out, out);
+    fp8_codes<CONV, 8>(w, lg, scale_out, out);
     return make_uint4(out[0], out[1], out[2], out[3]);
 }
 
-// ---- dequantisation: e4m3fn codes and a row scale -> 16-bit values ----------
+// ---- dequantisation: 8-bit codes and a row scale -> 16-bit values -----------
 
 // The product q * s is rounded to fp32 before its 16-bit conversion.  Left
 // alone, the compiler folds the multiply and an f32 -> f16 conversion into
@@ -221,17 +265,30 @@ __device__ __forceinline__ T as_rounded(T v)
 }
 
 // One code -> q * s rounded to the 16-bit format: the exact value of the code
-// (3 fraction bits, bias 7, codes below 8 subnormal), one fp32 product, the
-// conversion rounding to nearest even.  NaN codes and NaN products (0 * Inf)
-// give the format's quiet NaN with the code's sign.
-template <bool kBf16>
+// (e4m3fn: 3 fraction bits, bias 7, exponent field 0 subnormal, S.1111.111
+// NaN; e5m2: 2 fraction bits, bias 15, exponent field 0 subnormal, all-ones
+// exponent infinity (fraction 0) or NaN), one fp32 product, the conversion
+// rounding to nearest even.  NaN codes and NaN products (0 * Inf) give the
+// format's quiet NaN with the code's sign.
+template <bool kBf16, bool kE5>
 __device__ __forceinline__ uint32_t dequant1(uint32_t c, float s)
 {
     const uint32_t sign = (c & 0x80u) << 8;
-    const uint32_t e = (c >> 3) & 0xFu, m = c & 7u;
     const uint32_t qnan = kBf16 ? 0x7FC0u : 0x7E00u;
-    if ((c & 0x7Fu) == 0x7Fu) return sign | qnan;
-    const float x = e ? __builtin_ldexpf(float(8u + m), int(e) - 10) : float(m) * 0x1p-9f;
+    float x;
+    if constexpr (kE5) {
+        const uint32_t e = (c >> 2) & 0x1Fu, m = c & 3u;
+        if (e == 0x1Fu) {
+            if (m) return sign | qnan;
+            x = __builtin_inff();
+        } else {
+            x = e ? __builtin_ldexpf(float(4u + m), int(e) - 17) : float(m) * 0x1p-16f;
+        }
+    } else {
+        const uint32_t e = (c >> 3) & 0xFu, m = c & 7u;
+        if ((c & 0x7Fu) == 0x7Fu) return sign | qnan;
+        x = e ? __builtin_ldexpf(float(8u + m), int(e) - 10) : float(m) * 0x1p-9f;
+    }
     const float v = as_rounded((c & 0x80u ? -x : x) * s);
     if (v != v) return sign | qnan;
     if constexpr (kBf16)
@@ -240,24 +297,37 @@ __device__ __forceinline__ uint32_t dequant1(uint32_t c, float s)
         return __builtin_bit_cast(unsigned short, static_cast<_Float16>(v));
 }
 
-// 8 codes (two dwords) -> 8 16-bit values.  Rows without NaN codes and with a
-// finite scale: the hardware decode v_cvt_pk_f32_fp8 (exact), the fp32
-// product and the packed conversion; otherwise code by code.
-template <bool kBf16>
+// Two codes (bytes 0-1 or 2-3 of a dword) -> their exact fp32 values, by the
+// hardware decode (v_cvt_pk_f32_fp8 / v_cvt_pk_f32_bf8; finite codes only).
+template <bool kE5, bool kHi>
+__device__ __forceinline__ auto decode2(uint32_t c)
+{
+    if constexpr (kE5)
+        return __builtin_amdgcn_cvt_pk_f32_bf8(int(c), kHi);
+    else
+        return __builtin_amdgcn_cvt_pk_f32_fp8(int(c), kHi);
+}
+
+// 8 codes (two dwords) -> 8 16-bit values.  Lanes whose codes are all finite
+// and whose scale is finite: the hardware decode (exact), the fp32 product and
+// the packed conversion; otherwise code by code.
+template <bool kBf16, bool kE5>
 __device__ __forceinline__ uint4 dequant8(uint32_t c0, uint32_t c1, float s)
 {
     typedef float f2 __attribute__((ext_vector_type(2)));
     typedef __bf16 b2 __attribute__((ext_vector_type(2)));
     typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-    // a byte b has (b & 0x7F) == 0x7F exactly when (b & 0x7F) + 1 sets bit 7
-    const uint32_t nan = (((c0 & 0x7F7F7F7Fu) + 0x01010101u) | ((c1 & 0x7F7F7F7Fu) + 0x01010101u)) &
-                         0x80808080u;
+    // a byte that is not finite: e4m3fn (b & 0x7F) == 0x7F, exactly when
+    // (b & 0x7F) + 1 sets bit 7; e5m2 (b & 0x7C) == 0x7C, exactly when
+    // (b & 0x7C) + 4 sets bit 7 (no carry leaves the byte either way)
+    const uint32_t mk = kE5 ? 0x7C7C7C7Cu : 0x7F7F7F7Fu, one = kE5 ? 0x04040404u : 0x01010101u;
+    const uint32_t nan = (((c0 & mk) + one) | ((c1 & mk) + one)) & 0x80808080u;
     uint32_t o[4];
     if (!nan && __builtin_fabsf(s) <= 0x1.fffffep127f) {
-        const f2 f[4] = {as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c0), false) * s),
-                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c0), true) * s),
-                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c1), false) * s),
-                         as_rounded(__builtin_amdgcn_cvt_pk_f32_fp8(int(c1), true) * s)};
+        const f2 f[4] = {as_rounded(decode2<kE5, false>(c0) * s),
+                         as_rounded(decode2<kE5, true>(c0) * s),
+                         as_rounded(decode2<kE5, false>(c1) * s),
+                         as_rounded(decode2<kE5, true>(c1) * s)};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             if constexpr (kBf16)
@@ -270,7 +340,8 @@ __device__ __forceinline__ uint4 dequant8(uint32_t c0, uint32_t c1, float s)
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const uint32_t w = c[k >> 1] >> ((k & 1) * 16);
-            o[k] = dequant1<kBf16>(w & 0xFFu, s) | (dequant1<kBf16>((w >> 8) & 0xFFu, s) << 16);
+            o[k] = dequant1<kBf16, kE5>(w & 0xFFu, s) |
+                   (dequant1<kBf16, kE5>((w >> 8) & 0xFFu, s) << 16);
         }
     }
     return make_uint4(o[0], o[1], o[2], o[3]);
@@ -372,14 +443,19 @@ __device__ __forceinline__ void warm_translation(const KArgs& a, uint32_t unit)
 template <int MODE, int CONV, int ORDER>
 __device__ __forceinline__ void convert_part(const KArgs& a)
 {
-    constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3;     // writes e4m3fn codes
+    constexpr bool kFp8 = CONV == kBf16E4m3 || CONV == kF16E4m3 ||    // writes 8-bit codes
+                          CONV == kBf16E5m2 || CONV == kF16E5m2;
     constexpr bool kQd = CONV == kQdBf16Bf16 || CONV == kQdF16Bf16 ||  // quantise + dequantise
-                         CONV == kQdBf16F16 || CONV == kQdF16F16;
-    constexpr bool kDq = CONV == kDq8Bf16 || CONV == kDq8F16;          // dequantising unpack
+                         CONV == kQdBf16F16 || CONV == kQdF16F16 || CONV == kQd5Bf16Bf16 ||
+                         CONV == kQd5F16Bf16 || CONV == kQd5Bf16F16 || CONV == kQd5F16F16;
+    constexpr bool kDq = CONV == kDq8Bf16 || CONV == kDq8F16 ||        // dequantising unpack
+                         CONV == kDq5Bf16 || CONV == kDq5F16;
+    constexpr bool kE5 = e5_conv(CONV);                                // e5m2 codes
     constexpr bool kQuant = kFp8 || kQd;                               // row maximum over lanes
     constexpr bool kScalesIn = CONV == kCopy8 || kDq;                  // unpack reads row scales
     constexpr bool kScales = kFp8 || CONV == kCopy8;                   // rows written with a scale
-    constexpr bool kToBf16 = CONV == kDq8Bf16 || CONV == kQdBf16Bf16 || CONV == kQdF16Bf16;
+    constexpr bool kToBf16 = CONV == kDq8Bf16 || CONV == kQdBf16Bf16 || CONV == kQdF16Bf16 ||
+                             CONV == kDq5Bf16 || CONV == kQd5Bf16Bf16 || CONV == kQd5F16Bf16;
     // Lanes follow the transfer-tensor row: lane `sub` of a row owns its 16-byte
     // chunk sub.  A dequantising lane owns the 16 codes of chunk sub and writes
     // them as the two 16-byte cache chunks sub and sub + cpr (and reads, for
@@ -550,16 +626,16 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
 
     uint4 out, out2;  // out2: a dequantising lane's second cache chunk
     if constexpr (kFp8) {
-        out = to_e4m3<CONV>(v, lg, sc);  // every lane takes part in the row reduction
+        out = to_fp8<CONV>(v, lg, sc);  // every lane takes part in the row reduction
     } else if constexpr (kQd) {
         const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
         uint32_t c[4];
-        e4m3_codes<CONV, 8>(w, lg, sc, c);  // every lane takes part in the row reduction
-        out = dequant8<kToBf16>(c[0], c[1], sc);
-        out2 = dequant8<kToBf16>(c[2], c[3], sc);
+        fp8_codes<CONV, 8>(w, lg, sc, c);  // every lane takes part in the row reduction
+        out = dequant8<kToBf16, kE5>(c[0], c[1], sc);
+        out2 = dequant8<kToBf16, kE5>(c[2], c[3], sc);
     } else if constexpr (kDq) {
-        out = dequant8<kToBf16>(v[0].x, v[0].y, sc);
-        out2 = dequant8<kToBf16>(v[0].z, v[0].w, sc);
+        out = dequant8<kToBf16, kE5>(v[0].x, v[0].y, sc);
+        out2 = dequant8<kToBf16, kE5>(v[0].z, v[0].w, sc);
     } else if constexpr (CONV == kF16Bf16)
         out = to_bf16x8(v[0]);
     else if constexpr (CONV == kBf16F16)
@@ -623,6 +699,8 @@ int go_conv(int conv, const KArgs& a, void* stream)
     case kBf16F16: return go<MODE, kBf16F16, ORDER>(a, stream);
     case kBf16E4m3: return go<MODE, kBf16E4m3, ORDER>(a, stream);
     case kF16E4m3: return go<MODE, kF16E4m3, ORDER>(a, stream);
+    case kBf16E5m2: return go<MODE, kBf16E5m2, ORDER>(a, stream);
+    case kF16E5m2: return go<MODE, kF16E5m2, ORDER>(a, stream);
     default: break;
     }
     if constexpr (MODE == kRepack) {
@@ -631,6 +709,10 @@ int go_conv(int conv, const KArgs& a, void* stream)
         case kQdF16Bf16: return go<MODE, kQdF16Bf16, ORDER>(a, stream);
         case kQdBf16F16: return go<MODE, kQdBf16F16, ORDER>(a, stream);
         case kQdF16F16: return go<MODE, kQdF16F16, ORDER>(a, stream);
+        case kQd5Bf16Bf16: return go<MODE, kQd5Bf16Bf16, ORDER>(a, stream);
+        case kQd5F16Bf16: return go<MODE, kQd5F16Bf16, ORDER>(a, stream);
+        case kQd5Bf16F16: return go<MODE, kQd5Bf16F16, ORDER>(a, stream);
+        case kQd5F16F16: return go<MODE, kQd5F16F16, ORDER>(a, stream);
         default: break;
         }
     }
@@ -646,6 +728,8 @@ int launch(int mode, int conv, int order, const KArgs& a, void* stream)
         if (conv == kCopy8) return go<kUnpack, kCopy8, KVX_THD>(a, stream);
         if (conv == kDq8Bf16) return go<kUnpack, kDq8Bf16, KVX_THD>(a, stream);
         if (conv == kDq8F16) return go<kUnpack, kDq8F16, KVX_THD>(a, stream);
+        if (conv == kDq5Bf16) return go<kUnpack, kDq5Bf16, KVX_THD>(a, stream);
+        if (conv == kDq5F16) return go<kUnpack, kDq5F16, KVX_THD>(a, stream);
         return int(hipErrorInvalidValue);
     }
     if (mode == kPack) {

@@ -149,11 +149,12 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
     // the checks of the unpack side up front, so that a bad argument is
     // reported before anything is enqueued (the pack side's are the first
     // chunk's pack, which runs first)
-    const bool fp8 = q->plan->cache_dtype == KVX_FP8_E4M3FN;  // the cache holds scales
+    const bool fp8 = q->plan->cache_dtype == KVX_FP8_E4M3FN ||  // the cache holds scales
+                     q->plan->cache_dtype == KVX_FP8_E5M2;
     if (!cache || (reinterpret_cast<uintptr_t>(cache) & 15u))
         return fail(KVX_EINVAL, "NULL or misaligned cache");
     if (fp8 != (scales != nullptr) || (reinterpret_cast<uintptr_t>(scales) & 15u))
-        return fail(KVX_EINVAL, "scales must be given, 16-byte aligned, exactly for an e4m3fn cache");
+        return fail(KVX_EINVAL, "scales must be given, 16-byte aligned, exactly for an 8-bit cache");
     if (!bt || bt_stride < q->plan->max_blocks)
         return fail(KVX_EINVAL, "NULL block table or bt_stride below %d", q->plan->max_blocks);
     int cur = -1;

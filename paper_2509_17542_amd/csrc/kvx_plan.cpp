@@ -37,7 +37,11 @@ namespace {
 
 using kvx::fail;
 
-int dtype_size(int dt) { return dt == KVX_FP8_E4M3FN ? 1 : 2; }
+bool is_fp8(int dt) { return dt == KVX_FP8_E4M3FN || dt == KVX_FP8_E5M2; }
+
+bool is_dtype(int dt) { return dt == KVX_FP16 || dt == KVX_BF16 || is_fp8(dt); }
+
+int dtype_size(int dt) { return is_fp8(dt) ? 1 : 2; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -52,6 +56,8 @@ int pick_conv(int s, int d)
     if (s == KVX_BF16 && d == KVX_FP16) return kvx::kBf16F16;
     if (s == KVX_BF16 && d == KVX_FP8_E4M3FN) return kvx::kBf16E4m3;
     if (s == KVX_FP16 && d == KVX_FP8_E4M3FN) return kvx::kF16E4m3;
+    if (s == KVX_BF16 && d == KVX_FP8_E5M2) return kvx::kBf16E5m2;
+    if (s == KVX_FP16 && d == KVX_FP8_E5M2) return kvx::kF16E5m2;
     return -1;
 }
 
@@ -63,10 +69,14 @@ int heads_per_rank(int H, int tp) { return tp <= H ? H / tp : 1; }
 // unpack of an e4m3fn transfer tensor.
 int cache_dtype_of(const kvx_desc& d) { return d.cache_dtype ? d.cache_dtype : d.dst_dtype; }
 
-// repack kernel variant that quantises to e4m3fn and dequantises into a
-// 16-bit cache
-int qd_conv(int s, int c)
+// repack kernel variant that quantises to the 8-bit format w and
+// dequantises into a 16-bit cache c
+int qd_conv(int s, int w, int c)
 {
+    if (w == KVX_FP8_E5M2) {
+        if (s == KVX_BF16) return c == KVX_BF16 ? kvx::kQd5Bf16Bf16 : kvx::kQd5Bf16F16;
+        return c == KVX_BF16 ? kvx::kQd5F16Bf16 : kvx::kQd5F16F16;
+    }
     if (s == KVX_BF16) return c == KVX_BF16 ? kvx::kQdBf16Bf16 : kvx::kQdBf16F16;
     return c == KVX_BF16 ? kvx::kQdF16Bf16 : kvx::kQdF16F16;
 }
@@ -97,20 +107,17 @@ kvx_status validate(const kvx_desc* d)
         return fail(KVX_EINVAL, "unknown src_order %d", d->src_order);
     if (d->src_order == KVX_PAGED && (d->src_block_size <= 0 || d->src_num_blocks <= 0))
         return fail(KVX_EINVAL, "a paged source needs src_block_size >= 1 and src_num_blocks >= 1");
-    if (d->src_dtype != KVX_FP16 && d->src_dtype != KVX_BF16 && d->src_dtype != KVX_FP8_E4M3FN)
-        return fail(KVX_EINVAL, "unknown src_dtype %d", d->src_dtype);
-    if (d->dst_dtype != KVX_FP16 && d->dst_dtype != KVX_BF16 && d->dst_dtype != KVX_FP8_E4M3FN)
-        return fail(KVX_EINVAL, "unknown dst_dtype %d", d->dst_dtype);
+    if (!is_dtype(d->src_dtype)) return fail(KVX_EINVAL, "unknown src_dtype %d", d->src_dtype);
+    if (!is_dtype(d->dst_dtype)) return fail(KVX_EINVAL, "unknown dst_dtype %d", d->dst_dtype);
     if (pick_conv(d->src_dtype, d->dst_dtype) < 0)
         return fail(KVX_EUNSUPPORTED, "dtype pair %d -> %d is not supported", d->src_dtype,
                     d->dst_dtype);
     const int cdt = cache_dtype_of(*d);
-    if (cdt != KVX_FP16 && cdt != KVX_BF16 && cdt != KVX_FP8_E4M3FN)
-        return fail(KVX_EINVAL, "unknown cache_dtype %d", d->cache_dtype);
-    if (cdt != d->dst_dtype && d->dst_dtype != KVX_FP8_E4M3FN)
+    if (!is_dtype(cdt)) return fail(KVX_EINVAL, "unknown cache_dtype %d", d->cache_dtype);
+    if (cdt != d->dst_dtype && !(is_fp8(d->dst_dtype) && !is_fp8(cdt)))
         return fail(KVX_EUNSUPPORTED,
-                    "cache_dtype %d differs from a 16-bit dst_dtype %d (only an e4m3fn transfer "
-                    "tensor is dequantised)", cdt, d->dst_dtype);
+                    "cache_dtype %d differs from dst_dtype %d (only an 8-bit transfer tensor is "
+                    "dequantised, into a 16-bit cache)", cdt, d->dst_dtype);
     if ((int64_t(d->head_dim) * dtype_size(d->src_dtype)) % 16 ||
         (int64_t(d->head_dim) * dtype_size(d->dst_dtype)) % 16)
         return fail(KVX_EINVAL, "head_dim %d: rows must be whole 16-byte vectors on both sides",
@@ -197,7 +204,7 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     while ((1 << p->lg_lpr) < p->cpr) ++p->lg_lpr;
 
     // requests: source offsets, transfer-tensor segments, work items
-    const bool fp8 = d.dst_dtype == KVX_FP8_E4M3FN;
+    const bool fp8 = is_fp8(d.dst_dtype);  // the transfer tensor carries scales
     const bool paged = d.src_order == KVX_PAGED;
     const int64_t L2 = int64_t(d.num_layers) * 2;
     int64_t src_off = 0, wire = 0, nitems = 0;
@@ -279,9 +286,9 @@ kvx_status kvx_plan_info_get(const kvx_plan_t* p, kvx_plan_info* info)
     const int64_t D = p->d.head_dim;
     const int64_t rd = p->elems_rows * D * p->esz_src;
     const int64_t wr = p->elems_rows * D * p->esz_dst +
-                       (p->d.dst_dtype == KVX_FP8_E4M3FN ? p->elems_rows * 4 : 0);
+                       (is_fp8(p->d.dst_dtype) ? p->elems_rows * 4 : 0);
     const int64_t cw = p->elems_rows * D * p->esz_cache +
-                       (p->cache_dtype == KVX_FP8_E4M3FN ? p->elems_rows * 4 : 0);
+                       (is_fp8(p->cache_dtype) ? p->elems_rows * 4 : 0);
     info->wire_bytes = p->wire_bytes;
     info->total_tokens = p->total_tokens;
     info->read_bytes_pack = rd;
@@ -376,10 +383,15 @@ namespace {
 int conv_for(const kvx_plan_t* p, int mode)
 {
     if (mode == kvx::kUnpack) {
-        if (p->dequant) return p->cache_dtype == KVX_BF16 ? kvx::kDq8Bf16 : kvx::kDq8F16;
+        if (p->dequant) {
+            if (p->d.dst_dtype == KVX_FP8_E5M2)
+                return p->cache_dtype == KVX_BF16 ? kvx::kDq5Bf16 : kvx::kDq5F16;
+            return p->cache_dtype == KVX_BF16 ? kvx::kDq8Bf16 : kvx::kDq8F16;
+        }
         return p->esz_dst == 1 ? kvx::kCopy8 : kvx::kCopy16;
     }
-    if (mode == kvx::kRepack && p->dequant) return qd_conv(p->d.src_dtype, p->cache_dtype);
+    if (mode == kvx::kRepack && p->dequant)
+        return qd_conv(p->d.src_dtype, p->d.dst_dtype, p->cache_dtype);
     return p->conv;
 }
 
@@ -392,7 +404,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
                    int layer_shift = 0)
 {
     if (!p) return fail(KVX_EINVAL, "NULL plan");
-    const bool fp8 = p->cache_dtype == KVX_FP8_E4M3FN;  // the cache holds scales
+    const bool fp8 = is_fp8(p->cache_dtype);  // the cache holds scales
     const bool paged = p->d.src_order == KVX_PAGED;
     std::memset(&a, 0, sizeof a);
     if (mode != kvx::kUnpack && paged != paged_call)
@@ -423,7 +435,7 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
     if (!aligned16(dst)) return fail(KVX_EINVAL, "destination not 16-byte aligned");
     if (mode != kvx::kPack) {
         if (fp8 != (scales != nullptr))
-            return fail(KVX_EINVAL, fp8 ? "e4m3fn cache needs a scales buffer"
+            return fail(KVX_EINVAL, fp8 ? "8-bit cache needs a scales buffer"
                                         : "scales given for a 16-bit cache");
         if (scales && !aligned16(scales)) return fail(KVX_EINVAL, "scales not 16-byte aligned");
         if (!p->items.empty() && !bt) return fail(KVX_EINVAL, "NULL block table");

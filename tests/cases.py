@@ -96,6 +96,27 @@ SMALL_DEQUANT = {
                                                  num_blocks=16, seed=98),
 }
 
+# e5m2 transfer tensors: the e4m3fn scheme with OCP e5m2 codes (scale
+# max|x| / 57344); caches holding the codes and scales, or dequantised.
+SMALL_E5M2 = {
+    "e5m2_bf16": FP8.replace(name="e5m2_bf16", dst_dtype="e5m2", layers=2, total_layers=2,
+                             num_requests=3, len_lo=5, len_hi=70, num_blocks=64),
+    "e5m2_fp16_htd_tp2to4": QWEN.replace(name="e5m2_fp16_htd_tp2to4", dst_dtype="e5m2",
+                                         layers=2, total_layers=2, src_tp=2, dst_tp=4,
+                                         dst_rank=3, num_requests=3, len_lo=10, len_hi=150,
+                                         num_blocks=16),
+    "e5m2_paged_tp4to2": P70B.replace(name="e5m2_paged_tp4to2", dst_dtype="e5m2", layers=2,
+                                      total_layers=2, num_requests=2, len_lo=33, len_hi=90,
+                                      num_blocks=16, src_num_blocks=24),
+    "e5m2_dequant_bf16": FP8.replace(name="e5m2_dequant_bf16", dst_dtype="e5m2",
+                                     cache_dtype="bf16", layers=2, total_layers=2,
+                                     num_requests=3, len_lo=5, len_hi=70, num_blocks=64),
+    "e5m2_dequant_fp16_empty": QWEN.replace(name="e5m2_dequant_fp16_empty", dst_dtype="e5m2",
+                                            cache_dtype="fp16", layers=1, total_layers=1,
+                                            num_requests=4, lens_override=(37, 0, 16, 1),
+                                            block_size=16, num_blocks=16, seed=99),
+}
+
 # Paged sources (the prefill side's own paged cache), same shapes as the two
 # full paged workloads plus page-size ratios that do not divide each other.
 SMALL_PAGED = {
@@ -122,19 +143,24 @@ SMALL_PAGED = {
 }
 
 
+FP8_NAMES = ("e4m3fn", "e5m2")
+# 8-bit formats: torch dtype and largest finite value (the scale's divisor)
+_FP8 = {"e4m3fn": (torch.float8_e4m3fn, 448.0), "e5m2": (torch.float8_e5m2, 57344.0)}
+
+
 def fmt_codes(mod):
     """dtype name -> the integer code used by `mod` (oracle or GPU binding)."""
-    return {"fp16": mod.FP16, "bf16": mod.BF16, "e4m3fn": mod.E4M3FN}
+    return {"fp16": mod.FP16, "bf16": mod.BF16, "e4m3fn": mod.E4M3FN, "e5m2": mod.E5M2}
 
 
 def dst_size(w):
     """element size of the decode cache"""
-    return 1 if w.cdt == "e4m3fn" else 2
+    return 1 if w.cdt in FP8_NAMES else 2
 
 
 def wire_size(w):
     """element size of the transfer tensor"""
-    return 1 if w.dst_dtype == "e4m3fn" else 2
+    return 1 if w.dst_dtype in FP8_NAMES else 2
 
 
 def oracle_problem(O, w, lens, layers=None, sbt=None):
@@ -192,8 +218,9 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     Heads: the decode rank holds global heads [rank*Hd, (rank+1)*Hd), or the
     one head rank // (dst_tp / H) when dst_tp is a multiple of H.
     Casts: same type = bits; fp16->bf16 and bf16->fp16 = torch .to();
-    a 16-bit cache under an e4m3fn transfer = q.float() * s then .to();
-    e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn)."""
+    a 16-bit cache under an 8-bit transfer = q.float() * s then .to();
+    e4m3fn = s = amax/448 in fp32, q = clamp(x/s, +-448).to(float8_e4m3fn),
+    e5m2 the same with 57344 and float8_e5m2."""
     heads = rank_heads(w)
     x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers, heads))
     x = x.to(_TDT[w.src_dtype])                                     # [L][2][Hd][T][D]
@@ -203,15 +230,16 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     if w.dst_dtype in ("bf16", "fp16"):
         y = x.to(_TDT[w.dst_dtype])
         return y.view(torch.uint8).numpy().reshape(*y.shape[:4], 2 * w.head_dim), None
+    tq, fmax = _FP8[w.dst_dtype]
     xf = x.float()
-    s = xf.abs().amax(dim=-1) / torch.tensor(448.0)
+    s = xf.abs().amax(dim=-1) / torch.tensor(fmax)
     v = xf / s[..., None]
-    q = v.clamp(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8)
+    q = v.clamp(-fmax, fmax).to(tq).view(torch.uint8)
     zero_rows = (s == 0)[..., None].expand_as(q)
     signed_zero = torch.where(torch.signbit(xf), 0x80, 0).to(torch.uint8)
     q = torch.where(zero_rows, signed_zero, q)
-    if w.cdt != "e4m3fn":   # dequantising unpack: q * s in fp32, then the 16-bit cast
-        y = (q.view(torch.float8_e4m3fn).float() * s[..., None]).to(_TDT[w.cdt])
+    if w.cdt not in FP8_NAMES:   # dequantising unpack: q * s in fp32, then the 16-bit cast
+        y = (q.view(tq).float() * s[..., None]).to(_TDT[w.cdt])
         return y.view(torch.uint8).numpy().reshape(*y.shape[:4], 2 * w.head_dim), None
     return q.numpy(), s.numpy()
 

@@ -8,12 +8,12 @@ import torch
 
 import oracle as O
 import workload as W
-from cases import dst_size, oracle_problem, read_shards
+from cases import FP8_NAMES, dst_size, oracle_problem, read_shards
 
 import paper_2509_17542_amd as K
 
 DEV = "cuda"
-_F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
+_F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN, "e5m2": K.E5M2}
 
 
 def log(msg: str) -> None:
@@ -39,7 +39,7 @@ def pool(w, layers, fill=W.SENTINEL):
     n = layers * 2 * w.num_blocks * w.block_size * w.hd
     cache = torch.full((n * row,), fill, dtype=torch.uint8, device=DEV)
     scales = None
-    if w.cdt == "e4m3fn":
+    if w.cdt in FP8_NAMES:
         scales = torch.full((n * 4,), fill, dtype=torch.uint8, device=DEV).view(torch.float32)
     return cache, scales
 
@@ -108,7 +108,7 @@ def oracle_pool(w, lens, bt, stride, shards, layers=None, op="repack", wire=None
     p = oracle_problem(O, w, lens, layers, sbt=sbt)
     cache = np.full(O.cache_bytes(p), W.SENTINEL, dtype=np.uint8)
     scales = None
-    if w.cdt == "e4m3fn":
+    if w.cdt in FP8_NAMES:
         scales = np.full(4 * O.scale_count(p), W.SENTINEL, dtype=np.uint8).view(np.float32)
     if op == "repack":
         O.repack(p, shards, cache, scales, bt, stride)

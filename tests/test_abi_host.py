@@ -8,7 +8,7 @@ import re
 import numpy as np
 import pytest
 
-from cases import FULL, SMALL, SMALL_DEQUANT, SMALL_PAGED, oracle_problem
+from cases import FP8_NAMES, FULL, SMALL, SMALL_DEQUANT, SMALL_E5M2, SMALL_PAGED, oracle_problem
 from conftest import ROOT
 
 import oracle as O
@@ -30,11 +30,11 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 5
+    assert K.kvx_abi_version() == 6
 
 
 def desc_for(w, lens, **over):
-    f = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN}
+    f = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN, "e5m2": K.E5M2}
     kw = dict(num_layers=w.layers, num_kv_heads=w.heads, head_dim=w.head_dim, src_tp=w.src_tp,
               dst_tp=w.dst_tp, dst_rank=w.dst_rank, src_dtype=f[w.src_dtype],
               dst_dtype=f[w.dst_dtype],
@@ -47,16 +47,16 @@ def desc_for(w, lens, **over):
 
 
 @pytest.mark.parametrize("name", list(SMALL) + list(SMALL_PAGED) + list(SMALL_DEQUANT) +
-                         list(FULL))
+                         list(SMALL_E5M2) + list(FULL))
 def test_plan_bytes_and_segments(name):
-    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | FULL)[name]
+    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | SMALL_E5M2 | FULL)[name]
     lens = W.seq_lens(w)
     plan = K.kvx_plan(desc_for(w, lens))
     info = K.kvx_plan_info_get(plan)
     rows = w.layers * 2 * int(lens.sum()) * w.hd
 
     def row_bytes(dt):  # a row of head_dim elements, plus its scale for e4m3fn
-        return w.head_dim + 4 if dt == "e4m3fn" else 2 * w.head_dim
+        return w.head_dim + 4 if dt in FP8_NAMES else 2 * w.head_dim
 
     rd, wr, cw = rows * 2 * w.head_dim, rows * row_bytes(w.dst_dtype), rows * row_bytes(w.cdt)
     assert (info.read_bytes_repack, info.write_bytes_repack) == (rd, cw)
@@ -100,6 +100,10 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(cache_dtype=1), K.EUNSUPPORTED),               # a 16-bit transfer tensor is not dequantised
     (dict(dst_dtype=3, cache_dtype=9), K.EINVAL),
     (dict(dst_dtype=3, cache_dtype=2, head_dim=2048), K.EUNSUPPORTED),  # 2048-byte e4m3fn rows
+    (dict(dst_dtype=4, cache_dtype=3), K.EUNSUPPORTED),  # e5m2 on the wire, e4m3fn in the cache
+    (dict(dst_dtype=3, cache_dtype=4), K.EUNSUPPORTED),
+    (dict(src_dtype=4, dst_dtype=4), K.EUNSUPPORTED),    # an 8-bit source
+    (dict(dst_dtype=5), K.EINVAL),
 ])
 def test_plan_rejects(over, status):
     kw = dict(BASE)

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from cases import FULL, SMALL, SMALL_PAGED, dst_size, oracle_problem, read_shards
+from cases import FP8_NAMES, FULL, SMALL, SMALL_PAGED, dst_size, oracle_problem, read_shards
 from gpu_util import DEV, check_sampled, check_unused_pages, desc_for, dev_u16, log
 
 import oracle as O
@@ -90,7 +90,7 @@ def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
     whole = oracle_problem(O, w, lens, L)
     want_c = np.full(O.cache_bytes(whole), W.SENTINEL, dtype=np.uint8)
     want_s = None
-    if w.cdt == "e4m3fn":
+    if w.cdt in FP8_NAMES:
         want_s = np.full(4 * O.scale_count(whole), W.SENTINEL, dtype=np.uint8).view(np.float32)
     O.repack(whole, W.source_shards(w, lens, 0, L), want_c, want_s, bt, stride)
 
@@ -107,7 +107,7 @@ def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
         cache = torch.full((rows * w.head_dim * dst_size(w),), W.SENTINEL, dtype=torch.uint8,
                            device=DEV)
         scales = None
-        if w.cdt == "e4m3fn":
+        if w.cdt in FP8_NAMES:
             scales = torch.full((rows * 4,), W.SENTINEL, dtype=torch.uint8,
                                 device=DEV).view(torch.float32)
         for (s0, sn), dsh in zip(src_st, src_bufs):

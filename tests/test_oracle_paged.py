@@ -18,7 +18,7 @@ import workload as W
 def _pool(p, sentinel=W.SENTINEL):
     cache = np.full(O.cache_bytes(p), sentinel, dtype=np.uint8)
     scales = None
-    if p.dst_fmt == O.E4M3FN:
+    if p.cache_fmt_eff in O.FP8:
         scales = np.full(4 * O.scale_count(p), sentinel, dtype=np.uint8).view(np.float32)
     return cache, scales
 

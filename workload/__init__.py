@@ -82,7 +82,7 @@ class Workload:
     dst_tp: int
     dst_rank: int
     src_dtype: str         # "fp16" | "bf16"
-    dst_dtype: str         # "fp16" | "bf16" | "e4m3fn"
+    dst_dtype: str         # "fp16" | "bf16" | "e4m3fn" | "e5m2"
     src_order: str         # "thd" = [token][head][dim], "htd" = [head][token][dim],
                            # "paged" = the prefill side's own paged cache
     block_size: int
@@ -197,6 +197,10 @@ WORKLOADS = {
         # with per-(token, head) scales and dequantised into a bf16 cache
         Workload("llama3_8b_bf16_e4m3_bf16_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "e4m3fn",
                  "thd", 16, 65536, 16, 512, 4096, seed=17543, cache_dtype="bf16"),
+        # the Llama-3-8B workload (same seed and values) into an e5m2 cache with
+        # per-(token, head) fp32 scales
+        Workload("llama3_8b_bf16_e5m2_bs16", 32, 32, 8, 128, 1, 1, 0, "bf16", "e5m2", "thd",
+                 16, 65536, 16, 512, 4096, seed=17543),
     ]
 }
 
