@@ -119,6 +119,27 @@ __device__ __forceinline__ float quotient(float a, float s, float r)
     return __builtin_fmaf(e, r, q);
 }
 
+// Maximum of m over each aligned group of 2^lg consecutive lanes (lg <= 6,
+// wave-uniform).  Within a 16-lane DPP row the exchanges are VALU operands
+// (quad_perm [1,0,3,2] and [2,3,0,1] pair lanes 1 and 2 apart; after those,
+// row_half_mirror pairs the two quads of 8 lanes and row_mirror the two
+// halves of 16), so no LDS permute and no wait is needed; wider groups (rows
+// above 256 bytes) add xor shuffles.  Every lane of the wave must execute it.
+__device__ __forceinline__ uint32_t group_max(uint32_t m, int lg)
+{
+    auto dpp = [](uint32_t v, auto ctrl) {
+        return static_cast<uint32_t>(
+            __builtin_amdgcn_update_dpp(0, static_cast<int>(v), decltype(ctrl)::value, 0xF, 0xF, false));
+    };
+    if (lg >= 1) m = max(m, dpp(m, std::integral_constant<int, 0xB1>{}));   // quad_perm 1,0,3,2
+    if (lg >= 2) m = max(m, dpp(m, std::integral_constant<int, 0x4E>{}));   // quad_perm 2,3,0,1
+    if (lg >= 3) m = max(m, dpp(m, std::integral_constant<int, 0x141>{}));  // row_half_mirror
+    if (lg >= 4) m = max(m, dpp(m, std::integral_constant<int, 0x140>{}));  // row_mirror
+    for (int o = 16; o < (1 << lg); o <<= 1)
+        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    return m;
+}
+
 // source format of a quantising conversion: fp16 or bf16
 constexpr bool f16_source(int conv)
 {
@@ -168,8 +189,7 @@ __device__ __forceinline__ void fp8_codes_general(const uint32_t (&w)[NW], int l
         hi = hi > F::kInf ? 0u : hi;
         m = max(m, max(lo, hi));
     }
-    for (int o = 1; o < (1 << lg); o <<= 1)
-        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    m = group_max(m, lg);
     const float amax = F::widen(m);
     const float s = amax / Q::kMax;  // IEEE divide
     scale_out = s;
@@ -216,8 +236,7 @@ __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float
     for (int k = 0; k < NW; ++k)  // magnitudes, NaN included
         mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
     uint32_t m = max(uint32_t(mm.x), uint32_t(mm.y));
-    for (int o = 1; o < (1 << lg); o <<= 1)
-        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    m = group_max(m, lg);
     const float s = F::widen(m) / Q::kMax;  // IEEE divide; NaN if the row holds a NaN
     if (!(s >= 0x1p-80f && s <= 0x1p100f)) {
         fp8_codes_general<CONV, NW>(w, lg, scale_out, out);
