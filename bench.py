@@ -311,8 +311,8 @@ def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_
         log(f"layer stream leg: {name} {ms:.2f} ms ({nbytes / (ms * 1e-3) / 1e9:.1f} GB/s each way)")
     res["pipe_GB/s_each_way"] = round(nbytes / (res["pipe_ms"] * 1e-3) / 1e9, 2)
     res["serial_over_pipe"] = round(res["serial_ms"] / res["pipe_ms"], 3)
-    res["note"] = ("layer chunks packed, copied to pinned host memory and back, unpacked; "
-                   "host-link bound, not an HBM figure")
+    res["note"] = ("layer chunks packed straight into pinned host memory, copied back to the "
+                   "device, unpacked; host-link bound, not an HBM figure")
     del pipe, wire, back, host
     return res
 

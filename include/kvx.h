@@ -263,17 +263,17 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * The transfer of Sec. III-B-1 moves the KV cache through a pinned host
  * memory pool, and the paper's conclusion names by-layer transmission as the
  * next step.  A pipe moves a plan's layers in chunks of chunk_layers layers:
- * each chunk is packed into a device send slot (on the caller's stream),
- * copied to a slot of a pinned host ring (device to host), copied into a
- * device receive slot (host to device) and unpacked into the cache (on a
- * stream of the pipe).  With `slots` slots per stage, chunk c + 1 is packed
- * and chunk c - 1 unpacked while chunk c crosses the bus.  The cache and
- * scales written equal kvx_pack followed by kvx_unpack of the whole plan.
+ * each chunk is packed straight into a slot of a pinned host ring (the pack
+ * kernel's stores cross the host link; on the caller's stream), copied into
+ * a device receive slot (host to device, a DMA copy) and unpacked into the
+ * cache (on a stream of the pipe).  With `slots` slots, chunk c + 1 is
+ * packed and chunk c - 1 unpacked while chunk c crosses the bus.  The cache
+ * and scales written equal kvx_pack followed by kvx_unpack of the whole plan.
  *
  * kvx_pipe_create allocates the pinned host ring (slots x the largest
- * chunk's transfer-tensor bytes, with hipHostMalloc), device send and
- * receive slots of the same size, two copy streams, one unpack stream and
- * their events (all default priority), on the plan's device.  The plan must
+ * chunk's transfer-tensor bytes, hipHostMalloc with hipHostMallocMapped),
+ * device receive slots of the same size, one copy stream, one unpack stream
+ * and their events (all default priority), on the plan's device.  The plan must
  * outlive the pipe.  KVX_EINVAL for a NULL plan or out, chunk_layers outside
  * [1, num_layers] or slots < 1; KVX_EDEVICE for a host-only plan;
  * KVX_ENOMEM if an allocation fails.
@@ -292,7 +292,7 @@ typedef struct {
     int32_t reserved;
     uint64_t slot_bytes;       /* transfer-tensor bytes of the largest chunk */
     uint64_t host_bytes;       /* pinned host ring: slots x slot_bytes */
-    uint64_t device_bytes;     /* send + receive slots: 2 x slots x slot_bytes */
+    uint64_t device_bytes;     /* receive slots: slots x slot_bytes */
     uint64_t bus_bytes;        /* bytes each direction moves per run: the plan's wire bytes, by chunk */
 } kvx_pipe_info;
 

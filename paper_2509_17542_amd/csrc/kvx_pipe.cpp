@@ -1,7 +1,10 @@
 // Layer-streamed transfer through a pinned host ring: the plan's layers move
-// in chunks, each packed into a device send slot, copied to a slot of pinned
-// host memory and back into a device receive slot, and unpacked, with the
-// stages of consecutive chunks overlapped on four streams.
+// in chunks, each packed straight into a slot of pinned host memory (the pack
+// kernel's stores cross the host link), copied by DMA into a device receive
+// slot and unpacked, with the stages of consecutive chunks overlapped on three
+// streams.  Writing the host slot from the kernel leaves the DMA engines one
+// direction only: two DMA copies in opposite directions overlapped in some
+// processes and ran one after the other in others.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -19,12 +22,12 @@ struct kvx_pipe_s {
     kvx_plan_t* full = nullptr;   // plan of chunk_layers layers
     kvx_plan_t* tail = nullptr;   // plan of the last, shorter chunk (or none)
     uint64_t slot_bytes = 0, bus_bytes = 0;
-    char* host = nullptr;         // pinned ring, slots x slot_bytes
-    char* send = nullptr;         // device, slots x slot_bytes
+    char* host = nullptr;         // pinned ring, slots x slot_bytes, mapped for the device
+    char* host_dev = nullptr;     // the ring's device address (the pack writes through it)
     char* recv = nullptr;         // device, slots x slot_bytes
-    hipStream_t d2h = nullptr, h2d = nullptr, unpack = nullptr;
+    hipStream_t h2d = nullptr, unpack = nullptr;
     hipEvent_t start = nullptr;
-    std::vector<hipEvent_t> packed, sent, received, unpacked;  // one per slot
+    std::vector<hipEvent_t> packed, received, unpacked;  // one per slot
 };
 
 namespace {
@@ -34,16 +37,15 @@ using kvx::fail;
 void release(kvx_pipe_s* q)
 {
     if (!q) return;
-    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+    for (hipStream_t s : {q->h2d, q->unpack})
         if (s) (void)hipStreamSynchronize(s);
-    for (auto* v : {&q->packed, &q->sent, &q->received, &q->unpacked})
+    for (auto* v : {&q->packed, &q->received, &q->unpacked})
         for (hipEvent_t e : *v)
             if (e) (void)hipEventDestroy(e);
     if (q->start) (void)hipEventDestroy(q->start);
-    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+    for (hipStream_t s : {q->h2d, q->unpack})
         if (s) (void)hipStreamDestroy(s);
     if (q->host) (void)hipHostFree(q->host);
-    if (q->send) (void)hipFree(q->send);
     if (q->recv) (void)hipFree(q->recv);
     kvx_plan_destroy(q->full);
     kvx_plan_destroy(q->tail);
@@ -99,19 +101,20 @@ kvx_status kvx_pipe_create(const kvx_plan_t* p, int32_t chunk_layers, int32_t sl
                    (q->tail ? q->tail->wire_bytes : 0);
     const size_t ring = size_t(q->slot_bytes) * size_t(slots);
     if (ring) {
-        if (!ok(hipHostMalloc(reinterpret_cast<void**>(&q->host), ring, hipHostMallocDefault)) ||
-            !ok(hipMalloc(reinterpret_cast<void**>(&q->send), ring)) ||
+        // mapped pinned memory: the pack kernel stores to the ring through
+        // its device address
+        if (!ok(hipHostMalloc(reinterpret_cast<void**>(&q->host), ring, hipHostMallocMapped)) ||
+            !ok(hipHostGetDevicePointer(reinterpret_cast<void**>(&q->host_dev), q->host, 0)) ||
             !ok(hipMalloc(reinterpret_cast<void**>(&q->recv), ring))) {
             (void)hipGetLastError();
             release(q);
-            return fail(KVX_ENOMEM, "pipe buffers (3 x %zu bytes) could not be allocated", ring);
+            return fail(KVX_ENOMEM, "pipe buffers (2 x %zu bytes) could not be allocated", ring);
         }
     }
-    bool good = ok(hipStreamCreateWithFlags(&q->d2h, hipStreamNonBlocking)) &&
-                ok(hipStreamCreateWithFlags(&q->h2d, hipStreamNonBlocking)) &&
+    bool good = ok(hipStreamCreateWithFlags(&q->h2d, hipStreamNonBlocking)) &&
                 ok(hipStreamCreateWithFlags(&q->unpack, hipStreamNonBlocking)) &&
                 ok(hipEventCreateWithFlags(&q->start, hipEventDisableTiming));
-    for (auto* v : {&q->packed, &q->sent, &q->received, &q->unpacked}) {
+    for (auto* v : {&q->packed, &q->received, &q->unpacked}) {
         v->assign(size_t(slots), nullptr);
         for (hipEvent_t& e : *v) good = good && ok(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     }
@@ -133,7 +136,7 @@ kvx_status kvx_pipe_info_get(const kvx_pipe_t* q, kvx_pipe_info* info)
     info->slots = q->slots;
     info->slot_bytes = q->slot_bytes;
     info->host_bytes = q->slot_bytes * uint64_t(q->slots);
-    info->device_bytes = 2 * info->host_bytes;
+    info->device_bytes = info->host_bytes;
     info->bus_bytes = q->bus_bytes;
     return KVX_OK;
 }
@@ -164,7 +167,7 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
 
     // the pipe's streams start after the caller's earlier work
     if (!ok(hipEventRecord(q->start, s0))) return fail(KVX_EDEVICE, "event record failed");
-    for (hipStream_t s : {q->d2h, q->h2d, q->unpack})
+    for (hipStream_t s : {q->h2d, q->unpack})
         if (!ok(hipStreamWaitEvent(s, q->start, 0))) return fail(KVX_EDEVICE, "stream wait failed");
 
     for (int c = 0; c < q->num_chunks; ++c) {
@@ -173,24 +176,20 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
         const kvx_plan_t* cp = (q->tail && c == q->num_chunks - 1) ? q->tail : q->full;
         const int shift = c * q->chunk_layers;
         const size_t bytes = size_t(cp->wire_bytes);
-        char* send = q->send + size_t(s) * q->slot_bytes;
         char* host = q->host + size_t(s) * q->slot_bytes;
+        char* host_dev = q->host_dev + size_t(s) * q->slot_bytes;
         char* recv = q->recv + size_t(s) * q->slot_bytes;
 
-        // pack (caller's stream): the send slot must have left for the host
-        if (reuse && !ok(hipStreamWaitEvent(s0, q->sent[s], 0)))
+        // pack into the host slot (caller's stream): the slot's previous
+        // chunk must have been copied to the device
+        if (reuse && !ok(hipStreamWaitEvent(s0, q->received[s], 0)))
             return fail(KVX_EDEVICE, "stream wait failed");
         kvx_status st = kvx::launch_shifted(cp, kvx::kPack, shift, shards, sbt, sbt_stride,
-                                            nullptr, send, nullptr, nullptr, 0, stream);
+                                            nullptr, host_dev, nullptr, nullptr, 0, stream);
         if (st != KVX_OK) return st;
         bool good = ok(hipEventRecord(q->packed[s], s0));
-        // device -> host: the host slot must have been read back
-        good = good && ok(hipStreamWaitEvent(q->d2h, q->packed[s], 0));
-        if (reuse) good = good && ok(hipStreamWaitEvent(q->d2h, q->received[s], 0));
-        good = good && ok(hipMemcpyAsync(host, send, bytes, hipMemcpyDeviceToHost, q->d2h)) &&
-               ok(hipEventRecord(q->sent[s], q->d2h));
         // host -> device: the receive slot must have been unpacked
-        good = good && ok(hipStreamWaitEvent(q->h2d, q->sent[s], 0));
+        good = good && ok(hipStreamWaitEvent(q->h2d, q->packed[s], 0));
         if (reuse) good = good && ok(hipStreamWaitEvent(q->h2d, q->unpacked[s], 0));
         good = good && ok(hipMemcpyAsync(recv, host, bytes, hipMemcpyHostToDevice, q->h2d)) &&
                ok(hipEventRecord(q->received[s], q->h2d));
