@@ -265,10 +265,51 @@ def main():
                                          min(args.stream_chunk, w.layers), args.stream_slots,
                                          timed)
 
+    if not args.no_extras:
+        out["pd_planner"] = planner_leg(K, w)
+
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, lens, stage_shards[0], args.cpu_seconds, value, sbt,
                                            stages[0])
     print(json.dumps(out), flush=True)
+
+
+def planner_leg(K, w):
+    """The deployment planner of Eq. 1-6 (host code) for the workload's KV
+    shape as a whole model on MI355X prefill and decode instances: the
+    strategies and P:D ratio it picks for a 4096-token prompt / 512-token
+    output service at 20 requests/s with TTFT <= 2 s and TPOT <= 50 ms, and
+    the time one search takes.  MI355X: 2.5 PFLOP/s dense bf16, 8 TB/s, 288
+    GB, 7 xGMI links of 153 GB/s; discounts 0.5 (compute), 0.8 (HBM, about
+    what the repack reaches), 0.7 (links)."""
+    # the model around the workload's KV shape: query heads, hidden size and
+    # FFN of the Llama-3 models with this many layers and KV heads
+    big = w.layers >= 80
+    hq, ffn = (64, 28672) if big else (32, 14336)
+    m = K.kvx_pd_model(w.layers, hq * w.head_dim, hq, w.heads, w.head_dim, ffn, 128256, 1, 1, 0,
+                       2.0, 2.0, 2.0)
+    g = K.kvx_pd_gpu(2.5e15, 8e12, 288e9, 7 * 153e9, 0.5, 0.8, 0.7, 8, 0)
+    p = K.kvx_pd_problem(m, g, g, 4096, 512, 20.0, 2.0, 0.05, 256, 0)
+    reps = 20
+    t = time.perf_counter()
+    for _ in range(reps):
+        sol = K.kvx_pd_search(p)
+    ms = (time.perf_counter() - t) / reps * 1e3
+
+    def choice(c):
+        return {"dp": c.dp, "tp": c.tp, "pp": c.pp, "batch": c.batch, "gpus": c.gpus,
+                "latency_s": round(c.latency, 5), "vram_GB": round(c.vram / 1e9, 2),
+                "throughput": round(c.throughput, 2)}
+
+    res = {"model": f"{w.layers} layers, {hq} query / {w.heads} KV heads, hidden {hq * w.head_dim}",
+           "prefill": choice(sol.prefill), "decode": choice(sol.decode),
+           "instances": f"{sol.prefill_instances}:{sol.decode_instances}",
+           "candidates": int(sol.candidates_prefill + sol.candidates_decode),
+           "search_ms": round(ms, 3)}
+    log(f"pd planner: P {res['prefill']['tp']}x{res['prefill']['pp']} b{res['prefill']['batch']}, "
+        f"D {res['decode']['tp']}x{res['decode']['pp']} b{res['decode']['batch']}, "
+        f"X:Y {res['instances']}, {ms:.2f} ms per search")
+    return res
 
 
 def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream,

@@ -76,7 +76,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 6
+#define KVX_ABI_VERSION 7
 
 typedef enum {
     KVX_OK = 0,
@@ -311,6 +311,95 @@ kvx_status kvx_pipe_destroy(kvx_pipe_t *pipe);
 const char *kvx_last_error(void);
 
 int32_t kvx_abi_version(void);
+
+/* ---- P:D deployment planner (host only) ----
+ *
+ * The joint optimisation of parallel strategy and P:D ratio (Sec. III-C):
+ * Eq. 1 picks the prefill instance's (dp, tp, pp, ep) that maximises the
+ * throughput per GPU T_p / (dp*tp*pp) subject to l_p <= ttft (Eq. 2) and
+ * m_p <= the GPU's VRAM (Eq. 3); Eq. 4 picks the decode instance's that
+ * maximises its throughput subject to l_d <= tpot (Eq. 5) and m_d <= VRAM
+ * (Eq. 6); the instance counts X : Y meet the request rate.  The paper
+ * gives the structure of these equations, not the cost terms; the terms
+ * used here are those of a decoder-only transformer:
+ *   l_p = c_p / (lambda R) + e_p / (beta B)   c_p: 2 FLOPs per weight per
+ *         token, causal attention 2*L*hq*D*b*s*(s+1), the LM head on the
+ *         last token; split by tp (experts by ep); e_p: 2 ring all-reduces
+ *         per layer (2(tp-1)/tp of b*s*h activations), pp-1 stage
+ *         hand-overs, 2 expert all-to-alls per layer ((ep-1)/ep);
+ *   m_p = weights on the most loaded GPU (attention, dense FFN and
+ *         embedding/head split by tp, E/ep whole experts, layers split by
+ *         pp) + one layer's activations + the batch's KV;
+ *   l_d = (weights read per step + KV of b requests at the average context
+ *         s_in + s_out/2) / (alpha B_vram) + e_d / (beta B);
+ *   m_d = weights + activations + KV of b requests at s_in + s_out;
+ *   T = dp * pp * b / l (pp batches in flight; requests/s for prefill,
+ *         tokens/s for decode); X = ceil(qps / T_p), Y = ceil(qps * s_out / T_d).
+ * KV per GPU uses H/tp heads, or one replicated head when tp is a multiple
+ * of H.  Candidates: tp divides q_heads and divides H or is a multiple of
+ * it (the head map of kvx_plan), pp divides L, ep = 1 for dense models or
+ * divides E and dp*tp, batch a power of two <= max_batch, dp*tp*pp <=
+ * max_gpus; visited in the order (GPUs, tp, pp, dp, ep, batch), the first
+ * whose objective is within a relative 1e-9 of the best wins.  All sizes in
+ * bytes, rates per second, times in seconds. */
+typedef enum { KVX_PD_PREFILL = 0, KVX_PD_DECODE = 1 } kvx_pd_side;
+
+typedef struct {
+    int32_t layers, hidden, q_heads, kv_heads, head_dim, ffn_dim, vocab;
+    int32_t experts;          /* FFN experts per layer, 1 = dense */
+    int32_t active_experts;   /* experts per token (1 when dense) */
+    int32_t reserved;
+    double weight_bytes, kv_bytes, act_bytes;   /* bytes per element */
+} kvx_pd_model;
+
+typedef struct {
+    double flops;       /* R: FLOP/s per GPU */
+    double hbm_bytes;   /* B_vram: bytes/s per GPU */
+    double vram;        /* M: bytes per GPU */
+    double link_bytes;  /* B: interconnect bytes/s per GPU */
+    double lambda, alpha, beta;  /* discount factors in (0, 1] */
+    int32_t max_gpus;   /* GPUs one instance may use, 1..4096 */
+    int32_t reserved;
+} kvx_pd_gpu;
+
+typedef struct {
+    kvx_pd_model model;
+    kvx_pd_gpu prefill, decode;
+    int32_t prompt_tokens, output_tokens;   /* s_in, s_out >= 1 */
+    double qps;          /* requests per second to serve, >= 0 */
+    double ttft, tpot;   /* thresholds L_ttft, L_tpot (s), > 0 */
+    int32_t max_batch;   /* largest batch tried, 1..2^20 */
+    int32_t reserved;
+} kvx_pd_problem;
+
+typedef struct {
+    int32_t dp, tp, pp, ep, batch, gpus;   /* gpus = dp*tp*pp; all 0 = no feasible strategy */
+    double latency;      /* l_p or l_d */
+    double vram;         /* m_p or m_d */
+    double throughput;   /* T_p (requests/s) or T_d (tokens/s) */
+    double objective;    /* T_p / gpus, or T_d */
+} kvx_pd_choice;
+
+typedef struct {
+    kvx_pd_choice prefill, decode;
+    int64_t prefill_instances, decode_instances;   /* X : Y (0 when either side is infeasible) */
+    int64_t candidates_prefill, candidates_decode;
+    int64_t feasible_prefill, feasible_decode;
+} kvx_pd_solution;
+
+/* The search of Eq. 1 and Eq. 4 (host only; no device is used).  KVX_EINVAL
+ * for a NULL argument, a dimension < 1, active_experts > experts, a
+ * non-positive byte size, rate, VRAM or threshold, a discount factor
+ * outside (0, 1], max_gpus outside [1, 4096], prompt or output tokens < 1,
+ * a negative qps or max_batch outside [1, 2^20]. */
+kvx_status kvx_pd_search(const kvx_pd_problem *problem, kvx_pd_solution *out);
+
+/* The cost terms of one strategy on one side (kvx_pd_side), without the
+ * constraints: latency, vram, throughput and objective as in kvx_pd_choice.
+ * Errors as kvx_pd_search, plus KVX_EINVAL for an unknown side or a
+ * strategy value < 1. */
+kvx_status kvx_pd_evaluate(const kvx_pd_problem *problem, int32_t side, int32_t dp, int32_t tp,
+                           int32_t pp, int32_t ep, int32_t batch, kvx_pd_choice *out);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # the struct layouts below are those of this version of include/kvx.h
-ABI_VERSION = 6
+ABI_VERSION = 7
 if _lib.kvx_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements kvx ABI {_lib.kvx_abi_version()}, this binding "
                       f"ABI {ABI_VERSION}: rebuild the library")
@@ -78,6 +78,40 @@ class kvx_pipe_info(ctypes.Structure):
     ]
 
 
+class kvx_pd_model(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("layers", "hidden", "q_heads", "kv_heads",
+                                              "head_dim", "ffn_dim", "vocab", "experts",
+                                              "active_experts", "reserved")] + \
+               [(n, ctypes.c_double) for n in ("weight_bytes", "kv_bytes", "act_bytes")]
+
+
+class kvx_pd_gpu(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("flops", "hbm_bytes", "vram", "link_bytes",
+                                               "lam", "alpha", "beta")] + \
+               [("max_gpus", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class kvx_pd_problem(ctypes.Structure):
+    _fields_ = [("model", kvx_pd_model), ("prefill", kvx_pd_gpu), ("decode", kvx_pd_gpu),
+                ("prompt_tokens", ctypes.c_int32), ("output_tokens", ctypes.c_int32),
+                ("qps", ctypes.c_double), ("ttft", ctypes.c_double), ("tpot", ctypes.c_double),
+                ("max_batch", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class kvx_pd_choice(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("dp", "tp", "pp", "ep", "batch", "gpus")] + \
+               [(n, ctypes.c_double) for n in ("latency", "vram", "throughput", "objective")]
+
+
+class kvx_pd_solution(ctypes.Structure):
+    _fields_ = [("prefill", kvx_pd_choice), ("decode", kvx_pd_choice)] + \
+               [(n, ctypes.c_int64) for n in ("prefill_instances", "decode_instances",
+                                              "candidates_prefill", "candidates_decode",
+                                              "feasible_prefill", "feasible_decode")]
+
+
+PD_PREFILL, PD_DECODE = 0, 1
+
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
 _lib.kvx_plan.restype = ctypes.c_int
@@ -115,12 +149,17 @@ _lib.kvx_last_error.restype = ctypes.c_char_p
 _lib.kvx_last_error.argtypes = []
 _lib.kvx_abi_version.restype = ctypes.c_int32
 _lib.kvx_abi_version.argtypes = []
+_lib.kvx_pd_search.restype = ctypes.c_int
+_lib.kvx_pd_search.argtypes = [ctypes.POINTER(kvx_pd_problem), ctypes.POINTER(kvx_pd_solution)]
+_lib.kvx_pd_evaluate.restype = ctypes.c_int
+_lib.kvx_pd_evaluate.argtypes = [ctypes.POINTER(kvx_pd_problem)] + [_i32] * 6 + \
+    [ctypes.POINTER(kvx_pd_choice)]
 
 EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_destroy", "kvx_pack",
            "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged",
            "kvx_check_block_table", "kvx_check_src_block_table", "kvx_pipe_create",
            "kvx_pipe_info_get", "kvx_pipe_run", "kvx_pipe_destroy", "kvx_last_error",
-           "kvx_abi_version")
+           "kvx_abi_version", "kvx_pd_search", "kvx_pd_evaluate")
 
 
 def _check(status: int) -> None:
@@ -315,3 +354,17 @@ def kvx_pipe_run(pipe: Pipe, src_shards, src_block_table, src_bt_stride: int, ca
 def kvx_pipe_destroy(pipe: Pipe) -> None:
     h, pipe.handle = pipe.handle, None
     _check(_lib.kvx_pipe_destroy(h))
+
+
+def kvx_pd_search(problem: kvx_pd_problem) -> kvx_pd_solution:
+    out = kvx_pd_solution()
+    _check(_lib.kvx_pd_search(ctypes.byref(problem), ctypes.byref(out)))
+    return out
+
+
+def kvx_pd_evaluate(problem: kvx_pd_problem, side: int, dp: int, tp: int, pp: int, ep: int,
+                    batch: int) -> kvx_pd_choice:
+    out = kvx_pd_choice()
+    _check(_lib.kvx_pd_evaluate(ctypes.byref(problem), side, dp, tp, pp, ep, batch,
+                                ctypes.byref(out)))
+    return out

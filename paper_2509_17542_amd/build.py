@@ -21,7 +21,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-I", INCLUDE, "-I", CSRC]
 DEVICE = ["-x", "hip", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
           "-packed-fp32-ops"]
-SOURCES = [("kvx_kernels.hip", True), ("kvx_plan.cpp", False), ("kvx_pipe.cpp", False)]
+SOURCES = [("kvx_kernels.hip", True), ("kvx_plan.cpp", False), ("kvx_pipe.cpp", False),
+           ("kvx_pd.cpp", False)]
 
 
 def build(verbose: bool = False) -> str:

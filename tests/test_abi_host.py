@@ -26,11 +26,11 @@ def declared_entry_points():
 
 def test_every_declared_symbol_is_exported():
     names = declared_entry_points()
-    assert len(names) == 17, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 6
+    assert K.kvx_abi_version() == 7
 
 
 def desc_for(w, lens, **over):

@@ -1,0 +1,138 @@
+"""The P:D planner of the library (kvx_pd_search / kvx_pd_evaluate, host
+code in the C ABI) against the oracle (oracle/pd.py), on the CPU: chosen
+strategies and instance counts equal, cost terms within 1e-12 relative
+(both evaluate the same closed forms in float64, in different orders), over
+the paper's experimental pairing (Llama2-7B, prefill on GPU B, decode on
+GPU A, Sec. V), dense and MoE models on MI355X, and 200 seeded random
+problems that cross the constraints' boundaries."""
+import numpy as np
+import pytest
+
+from oracle import pd as P
+
+K = pytest.importorskip("paper_2509_17542_amd")
+
+
+def to_c(p: P.Problem):
+    m = p.model
+    cm = K.kvx_pd_model(m.layers, m.hidden, m.q_heads, m.kv_heads, m.head_dim, m.ffn_dim,
+                        m.vocab, m.experts, m.active_experts, 0, m.weight_bytes, m.kv_bytes,
+                        m.act_bytes)
+
+    def gpu(g):
+        return K.kvx_pd_gpu(g.flops, g.hbm_bytes, g.vram, g.link_bytes, g.lam, g.alpha, g.beta,
+                            g.max_gpus, 0)
+
+    return K.kvx_pd_problem(cm, gpu(p.prefill), gpu(p.decode), p.prompt_tokens,
+                            p.output_tokens, p.qps, p.ttft, p.tpot, p.max_batch, 0)
+
+
+INT = ("dp", "tp", "pp", "ep", "batch", "gpus")
+FLT = ("latency", "vram", "throughput", "objective")
+
+
+def same_choice(c, o):
+    assert tuple(getattr(c, f) for f in INT) == tuple(getattr(o, f) for f in INT)
+    for f in FLT:
+        assert getattr(c, f) == pytest.approx(getattr(o, f), rel=1e-12, abs=0.0), f
+
+
+def check(p: P.Problem):
+    want = P.search(p)
+    got = K.kvx_pd_search(to_c(p))
+    same_choice(got.prefill, want.prefill)
+    same_choice(got.decode, want.decode)
+    for f in ("prefill_instances", "decode_instances", "candidates_prefill", "candidates_decode",
+              "feasible_prefill", "feasible_decode"):
+        assert getattr(got, f) == getattr(want, f), f
+    return got
+
+
+# Sec. V: GPU A (80 GB, 312 TFLOP/s) runs decode, GPU B (32 GB, 512 TFLOP/s)
+# prefill.  The paper gives no memory or link rates: 2.0 TB/s and 1.6 TB/s of
+# HBM and 300 GB/s of interconnect are assumed here.
+GPU_A = P.Gpu(312e12, 2.0e12, 80e9, 300e9, 0.5, 0.8, 0.7, 8)
+GPU_B = P.Gpu(512e12, 1.6e12, 32e9, 300e9, 0.5, 0.8, 0.7, 8)
+MI355X = P.Gpu(2.5e15, 8e12, 288e9, 7 * 153e9, 0.5, 0.8, 0.7, 8)
+LLAMA2_7B = P.Model(32, 4096, 32, 32, 128, 11008, 32000)
+LLAMA3_8B = P.Model(32, 4096, 32, 8, 128, 14336, 128256)
+LLAMA3_70B = P.Model(80, 8192, 64, 8, 128, 28672, 128256)
+MIXTRAL = P.Model(32, 4096, 32, 8, 128, 14336, 32000, experts=8, active_experts=2)
+
+
+def test_paper_pairing_llama2_7b():
+    for s_in, s_out in ((512, 128), (2048, 512), (4096, 1024)):
+        p = P.Problem(LLAMA2_7B, GPU_B, GPU_A, s_in, s_out, qps=2.0, ttft=1.0, tpot=0.05)
+        sol = check(p)
+        assert sol.prefill.gpus and sol.decode.gpus
+
+
+@pytest.mark.parametrize("m", [LLAMA3_8B, LLAMA3_70B, MIXTRAL])
+def test_mi355x(m):
+    for ttft, tpot in ((0.5, 0.02), (2.0, 0.05), (8.0, 0.2)):
+        check(P.Problem(m, MI355X, MI355X, 4096, 512, qps=50.0, ttft=ttft, tpot=tpot,
+                        max_batch=128))
+
+
+def test_random_problems():
+    rng = np.random.default_rng(27)
+    for _ in range(200):
+        H = int(rng.choice([1, 2, 4, 8]))
+        hq = H * int(rng.choice([1, 2, 4, 8]))
+        D = int(rng.choice([64, 128]))
+        E = int(rng.choice([1, 1, 4, 8]))
+        m = P.Model(int(rng.choice([2, 4, 6, 8, 12])), hq * D, hq, H, D,
+                    int(rng.integers(64, 4096)), int(rng.integers(100, 50000)), E,
+                    int(rng.integers(1, E + 1)), float(rng.choice([1, 2])),
+                    float(rng.choice([1, 2])), 2.0)
+
+        def gpu():
+            return P.Gpu(10 ** rng.uniform(11, 15), 10 ** rng.uniform(10, 13), 10 ** rng.uniform(8, 11),
+                         10 ** rng.uniform(9, 12), rng.uniform(0.2, 1), rng.uniform(0.2, 1),
+                         rng.uniform(0.2, 1), int(rng.integers(1, 17)))
+
+        p = P.Problem(m, gpu(), gpu(), int(rng.integers(1, 8192)), int(rng.integers(1, 2048)),
+                      float(rng.uniform(0, 100)), 10 ** rng.uniform(-3, 1), 10 ** rng.uniform(-4, -1),
+                      int(rng.choice([1, 7, 64, 1000])))
+        check(p)
+
+
+def test_evaluate_matches_cost_terms():
+    """Cost terms of single strategies, also ones the search would not try
+    (tp that does not divide the heads, odd batch sizes)."""
+    rng = np.random.default_rng(28)
+    for m in (LLAMA3_8B, LLAMA3_70B, MIXTRAL, LLAMA2_7B):
+        p = P.Problem(m, MI355X, GPU_A, 1024, 256, 10.0, 1.0, 0.05)
+        cp = to_c(p)
+        for _ in range(50):
+            dp, tp, pp = (int(x) for x in rng.integers(1, 9, 3))
+            ep = int(rng.choice([1, 2, 4, 8]))
+            b = int(rng.integers(1, 300))
+            for side, fn in ((K.PD_PREFILL, P.prefill_cost), (K.PD_DECODE, P.decode_cost)):
+                got = K.kvx_pd_evaluate(cp, side, dp, tp, pp, ep, b)
+                lat, mem, thr = fn(p, dp, tp, pp, ep, b)
+                assert got.latency == pytest.approx(lat, rel=1e-12)
+                assert got.vram == pytest.approx(mem, rel=1e-12)
+                assert got.throughput == pytest.approx(thr, rel=1e-12)
+
+
+@pytest.mark.parametrize("field,value", [("layers", 0), ("active_experts", 3), ("kv_bytes", 0.0)])
+def test_invalid_models(field, value):
+    p = to_c(P.Problem(LLAMA3_8B, MI355X, MI355X, 128, 16, 1.0, 1.0, 0.1))
+    setattr(p.model, field, value)
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_pd_search(p)
+    assert e.value.status == K.EINVAL
+
+
+@pytest.mark.parametrize("field,value", [("lam", 1.5), ("alpha", 0.0), ("max_gpus", 0),
+                                         ("vram", -1.0)])
+def test_invalid_gpus(field, value):
+    p = to_c(P.Problem(LLAMA3_8B, MI355X, MI355X, 128, 16, 1.0, 1.0, 0.1))
+    setattr(p.decode, field, value)
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_pd_search(p)
+    assert e.value.status == K.EINVAL
+    with pytest.raises(K.KvxError):
+        K.kvx_pd_evaluate(to_c(P.Problem(LLAMA3_8B, MI355X, MI355X, 128, 16, 1.0, 1.0, 0.1)),
+                          2, 1, 1, 1, 1, 1)   # unknown side
