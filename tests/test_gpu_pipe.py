@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-from cases import FULL, SMALL, SMALL_DEQUANT, SMALL_PAGED, dst_size, inputs
+from cases import FULL, SMALL, SMALL_DEQUANT, SMALL_E5M2, SMALL_PAGED, dst_size, inputs
 from gpu_util import (DEV, check_sampled, check_shapes, check_unused_pages, desc_for, dev_u16, log,
                       oracle_pool, pool)
 
@@ -54,12 +54,13 @@ CASES = [("llama3_8b_small", 1, 1), ("fp8_small", 1, 2), ("qwen_htd_small", 2, 3
          ("llama3_70b_small_r1", 1, 3), ("fp16_e4m3_htd_empty", 1, 1),
          ("paged16_tp4to2_bs32_small", 1, 2), ("paged16_e4m3_bs24", 2, 1),
          ("gqa_src_rep_tp8to2_r1", 2, 2), ("bf16_fp16_overflow", 1, 2),
-         ("dequant_bf16_e4m3_bf16", 1, 2), ("dequant_paged_tp4to2_bf16", 2, 1)]
+         ("dequant_bf16_e4m3_bf16", 1, 2), ("dequant_paged_tp4to2_bf16", 2, 1),
+         ("e5m2_bf16", 2, 2), ("e5m2_dequant_fp16_empty", 1, 1)]
 
 
 @pytest.mark.parametrize("name,chunk,slots", CASES)
 def test_pipe_small(name, chunk, slots):
-    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT)[name]
+    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | SMALL_E5M2)[name]
     lens, bt, stride, shards = inputs(w)
     log(f"pipe {name}: chunk {chunk} of {w.layers} layers, {slots} slots")
     want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
