@@ -117,6 +117,37 @@ SMALL_E5M2 = {
                                             block_size=16, num_blocks=16, seed=99),
 }
 
+# Shapes at the limits of the lane layout: rows of 16 to 2048 bytes (1 to 64
+# lanes per row, chunk counts that are not powers of two), 1024 heads per
+# decode rank, 64 head segments.
+_S = dict(layers=1, total_layers=1, num_requests=2, len_lo=5, len_hi=40, num_blocks=16)
+SMALL_SHAPES = {
+    # 1024-byte rows: 64 lanes per row, a whole wave; 4 rows per pass
+    "hd512_bf16": L8B.replace(name="hd512_bf16", heads=2, head_dim=512, **_S),
+    # 1024-byte e4m3fn rows: the row maximum exchanges beyond a 16-lane row
+    "hd1024_e4m3": FP8.replace(name="hd1024_e4m3", heads=2, head_dim=1024, **_S),
+    # ... dequantised into 2048-byte bf16 cache rows
+    "hd1024_e4m3_bf16": FP8.replace(name="hd1024_e4m3_bf16", heads=2, head_dim=1024,
+                                    cache_dtype="bf16", **_S),
+    # 160-byte rows: 10 chunks on 16 lanes; TP1 -> TP2
+    "hd80_fp16_bf16": TINY.replace(name="hd80_fp16_bf16", head_dim=80, **_S),
+    # 48-byte 8-bit rows from head-major fp16: 3 chunks on 4 lanes
+    "hd48_fp16_e5m2": QWEN.replace(name="hd48_fp16_e5m2", head_dim=48, dst_dtype="e5m2",
+                                   block_size=16, **_S),
+    "hd48_fp16_e4m3_fp16": QWEN.replace(name="hd48_fp16_e4m3_fp16", head_dim=48,
+                                        dst_dtype="e4m3fn", cache_dtype="fp16", block_size=16,
+                                        **_S),
+    # 16-byte e4m3fn rows: one lane per row, 256 rows per pass; 256 heads
+    "hd16_e4m3_256heads": FP8.replace(name="hd16_e4m3_256heads", heads=256, head_dim=16,
+                                      block_size=4, **_S),
+    # 16-byte bf16 rows and the most heads a decode rank may hold (1024)
+    "hd8_bf16_1024heads": L8B.replace(name="hd8_bf16_1024heads", heads=1024, head_dim=8,
+                                      block_size=2, **dict(_S, num_blocks=64)),
+    # the most head segments (64): prefill TP64 -> decode TP1
+    "tp64to1_64segs": L8B.replace(name="tp64to1_64segs", heads=64, head_dim=16, src_tp=64,
+                                  **_S),
+}
+
 # Paged sources (the prefill side's own paged cache), same shapes as the two
 # full paged workloads plus page-size ratios that do not divide each other.
 SMALL_PAGED = {

@@ -5,7 +5,7 @@ cases, round-trip identities and write-set enumeration."""
 import numpy as np
 import pytest
 
-from cases import (SMALL, TINY, L8B, consumer_rows, dst_size, gather_pages, inputs,
+from cases import (SMALL, SMALL_SHAPES, TINY, L8B, consumer_rows, dst_size, gather_pages, inputs,
                    oracle_problem, written_mask)
 from conftest import golden_lines
 
@@ -76,9 +76,9 @@ def test_head_map_with_replicated_heads(H, ts, td):
 
 # ---- the decode side reads what the prefill side wrote ------------------------
 
-@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_SHAPES))
 def test_repack_matches_paged_reader(name):
-    w = SMALL[name]
+    w = (SMALL | SMALL_SHAPES)[name]
     lens, bt, stride, shards = inputs(w)
     p = oracle_problem(O, w, lens)
     cache, scales = _pool(p)
