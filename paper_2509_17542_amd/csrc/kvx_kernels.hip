@@ -119,6 +119,22 @@ __device__ __forceinline__ float quotient(float a, float s, float r)
     return __builtin_fmaf(e, r, q);
 }
 
+// a / s with one remainder correction, for the fast path's 8-bit codes.  Its
+// result is not always the correctly rounded quotient, but its code always
+// is that quotient's: an exhaustive GPU check over every pair of 16-bit
+// magnitudes (row maximum, element <= it), bf16 and fp16, with s = amax /
+// fmax in [2^-80, 2^100], gives the same e4m3fn and e5m2 codes as
+// `quotient` for every pair (the bare product a * r differs on 9,000-25,000
+// pairs per source and format).  a may be negative: every step is odd in a
+// (rounding to nearest is symmetric), and the residual is formed as s*q - a
+// and subtracted, so a signed zero keeps its sign (q - (+0) * r is -0 for
+// q = -0, where q + (+0) * r would be +0).
+__device__ __forceinline__ float quotient_for_code(float a, float s, float r)
+{
+    const float q = a * r;
+    return __builtin_fmaf(-__builtin_fmaf(s, q, -a), r, q);
+}
+
 // Maximum of m over each aligned group of 2^lg consecutive lanes (lg <= 6,
 // wave-uniform).  Within a 16-lane DPP row the exchanges are VALU operands
 // (quad_perm [1,0,3,2] and [2,3,0,1] pair lanes 1 and 2 apart; after those,
@@ -158,7 +174,7 @@ constexpr bool e5_conv(int conv)
 template <int CONV>
 struct SrcFmt {
     static constexpr uint32_t kInf = f16_source(CONV) ? 0x7C00u : 0x7F80u;
-    // magnitude bits (sign cleared) -> fp32
+    // 16-bit pattern (sign included) -> fp32, exactly
     __device__ static __forceinline__ float widen(uint32_t m)
     {
         if constexpr (f16_source(CONV))
@@ -219,11 +235,13 @@ __device__ __forceinline__ void fp8_codes_general(const uint32_t (&w)[NW], int l
 
 // One lane's 2*NW source elements -> 2*NW 8-bit codes.  Fast path for rows with
 // no NaN and a scale in [2^-80, 2^100]: the row maximum from packed 16-bit
-// maxima, the exact quotient |x| / s, the element's sign set on it, and the
-// hardware conversion v_cvt_pk_fp8_f32 (round to nearest even, OCP e4m3fn on
-// gfx950; it equals e4m3_code on every fp32 magnitude up to 448, and a
-// quotient cannot round above 448 because |x| <= amax).  Other rows take the
-// general path.  Every lane of the wave must execute this.
+// maxima, the quotient x / s (quotient_for_code: the code of the exact
+// quotient, sign included), and the hardware conversion
+// v_cvt_pk_fp8_f32 / v_cvt_pk_bf8_f32 (round to nearest even, OCP e4m3fn and
+// e5m2 on gfx950; they equal e4m3_code / e5m2_code on every fp32 magnitude up
+// to 448 / 57344, and a quotient cannot round above those because |x| <=
+// amax).  Other rows take the general path.  Every lane of the wave must
+// execute this.
 template <int CONV, int NW>
 __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float& scale_out,
                                           uint32_t (&out)[NW / 2])
@@ -251,10 +269,11 @@ __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const uint32_t h = (w[2 * d + (e >> 1)] >> ((e & 1) * 16)) & 0xFFFFu;
-            q[e] = __uint_as_float(__float_as_uint(quotient(F::widen(h & 0x7FFFu), s, r)) |
-                                   ((h & 0x8000u) << 16));
+            q[e] = quotient_for_code(F::widen(h), s, r);  // the element's sign carried through
         }
-        const int lo = Q::cvt_pk(q[0], q[1], 0, false);
+        // bytes 2-3 of the first conversion's `old` operand are overwritten by
+        // the second, so any register serves (no zeroing move)
+        const int lo = Q::cvt_pk(q[0], q[1], __float_as_int(q[2]), false);
         out[d] = uint32_t(Q::cvt_pk(q[2], q[3], lo, true));
     }
 }
