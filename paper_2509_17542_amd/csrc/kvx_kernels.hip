@@ -255,7 +255,15 @@ __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float
         mm = __builtin_elementwise_max(mm, __builtin_bit_cast(us2, w[k] & 0x7FFF7FFFu));
     uint32_t m = max(uint32_t(mm.x), uint32_t(mm.y));
     m = group_max(m, lg);
-    const float s = F::widen(m) / Q::kMax;  // IEEE divide; NaN if the row holds a NaN
+    // s = amax / fmax by the reciprocal and one remainder correction: equal
+    // to the IEEE quotient for every 16-bit row maximum, and inside the fast
+    // range exactly when the IEEE quotient is (exhaustive check of all bf16
+    // and fp16 maxima for both formats, in exact rational arithmetic); NaN
+    // when the row holds a NaN or an infinity
+    constexpr float kInv = 1.0f / Q::kMax;
+    const float amax = F::widen(m);
+    const float q0 = amax * kInv;
+    const float s = __builtin_fmaf(__builtin_fmaf(-Q::kMax, q0, amax), kInv, q0);
     if (!(s >= 0x1p-80f && s <= 0x1p100f)) {
         fp8_codes_general<CONV, NW>(w, lg, scale_out, out);
         return;
