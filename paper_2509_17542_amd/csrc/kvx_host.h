@@ -16,7 +16,7 @@ struct kvx_plan_s {
     std::vector<kvx::Item> items;
     int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
     int cache_dtype = 0, esz_cache = 0;  // the cache's element type (dst_dtype unless dequantising)
-    bool dequant = false;                // e4m3fn transfer tensor, 16-bit cache
+    bool dequant = false;                // 8-bit transfer tensor, 16-bit cache
     std::vector<int> read_shards;  // prefill shards the decode rank reads, in slot order
     // lanes per row (from the transfer-tensor row; a dequantising lane covers
     // two 16-byte cache chunks) and workgroup passes per (page, segment)

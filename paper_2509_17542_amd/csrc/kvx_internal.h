@@ -83,7 +83,7 @@ struct KArgs {
     Segment seg[kMaxReadShards];      // pack/repack: the head segments; unpack: one, all heads
     const void* wire_in;              // unpack source
     void* dst;                        // pack: transfer tensor; else cache
-    float* dscale;                    // cache scales (unpack/repack, e4m3fn)
+    float* dscale;                    // cache scales (unpack/repack into an 8-bit cache)
     const Item* items;
     const int32_t* bt;
     int64_t num_blocks;

@@ -7,12 +7,13 @@
 // segment: the decode heads that come from one source shard) x (part).  A page
 // holds ntok <= block_size tokens; a segment of n heads gives it ntok * n
 // "rows" of head_dim elements.  Each row is covered by a power-of-two group of
-// lanes, one 16-byte destination vector per lane (global_load_dwordx4 /
-// global_store_dwordx4), so a 256-thread workgroup covers 256 / lanes-per-row
-// rows: one part.  The shard, its first head and the segment's place in the
-// decode row are the same for the whole workgroup (scalar registers), so a
-// lane's load address needs no table lookup; every lane issues its load(s),
-// converts and stores once.
+// lanes, one per 16-byte chunk of the transfer-tensor row (global_load_dwordx4
+// / global_store_dwordx4; a lane that dequantises 8-bit codes into a 16-bit
+// cache writes two cache chunks), so a 256-thread workgroup covers 256 /
+// lanes-per-row rows: one part.  The shard, its first head and the segment's
+// place in the decode row are the same for the whole workgroup (scalar
+// registers), so a lane's load address needs no table lookup; every lane
+// issues its load(s), converts and stores once.
 //
 // Units are numbered plane-major, page, segment, then part, so consecutive
 // units read consecutive source bytes.  The 1-D grid is dealt to the 8 XCDs
@@ -33,10 +34,11 @@
 // the time that page's workgroups store to it.  Stores are non-temporal: the
 // destination is not read again by this launch.
 //
-// The path is a gather/scatter stream with no reuse and no contraction: it is
-// bound by HBM bandwidth, so there is no MFMA and no LDS staging (every row is
-// at least 128 contiguous bytes, i.e. whole cache lines on both sides, so a
-// [token][head] <-> [head][token] reorder is a change of row addresses only).
+// The path is a gather/scatter stream with no reuse and no contraction: the
+// 16-bit conversions are bound by HBM bandwidth, the 8-bit ones (e4m3fn,
+// e5m2, per-row scales) by the vector ALUs and HBM together.  There is no
+// MFMA and no LDS staging: rows are whole 16-byte vectors on both sides, so a
+// [token][head] <-> [head][token] reorder is a change of row addresses only.
 #include <hip/hip_runtime.h>
 
 #include "kvx_internal.h"
@@ -109,7 +111,7 @@ struct Fp8 {
 // reciprocal of s refined by one Newton step: two remainder corrections
 // (Markstein), the unscaled form of the IEEE fp32 divide sequence.  No
 // intermediate under- or overflows for quotients >= 2^-24; smaller quotients
-// are only ever rounded to e4m3fn zero, which this result also gives.
+// are only ever rounded to an 8-bit zero, which this result also gives.
 __device__ __forceinline__ float quotient(float a, float s, float r)
 {
     float q = a * r;
@@ -519,7 +521,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
     // the lookups, the row loads and the paged source's page lookup overlap
     // instead of following one another.  Measured faster for repacks from
     // paged sources (+16%) and 16-bit token-major rows (+2%); the head-major
-    // and e4m3fn paths measure 2-4% faster with the row load inside the
+    // and 8-bit paths measure 2-4% faster with the row load inside the
     // branch, and the pack from paged sources the same either way.
     constexpr bool kEarly =
         (ORDER == KVX_PAGED && MODE != kPack) ||

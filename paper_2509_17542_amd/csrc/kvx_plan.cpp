@@ -66,7 +66,7 @@ int pick_conv(int s, int d)
 int heads_per_rank(int H, int tp) { return tp <= H ? H / tp : 1; }
 
 // The cache's element type: dst_dtype, or the 16-bit type of a dequantising
-// unpack of an e4m3fn transfer tensor.
+// unpack of an 8-bit transfer tensor.
 int cache_dtype_of(const kvx_desc& d) { return d.cache_dtype ? d.cache_dtype : d.dst_dtype; }
 
 // repack kernel variant that quantises to the 8-bit format w and

@@ -138,8 +138,10 @@ class Workload:
         return dataclasses.replace(self, **kw)
 
 
-# The five workloads: the decode-side shapes of four model families plus a
-# tiny one.  Sizes: layers x KV heads x head_dim, tokens per request.
+# The workloads: the decode-side shapes of four model families plus a tiny
+# one, then variants of them (paged sources, pipeline stages, replicated GQA
+# heads, other casts and 8-bit formats).  Sizes: layers x KV heads x
+# head_dim, tokens per request.
 WORKLOADS = {
     w.name: w
     for w in [
