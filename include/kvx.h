@@ -282,7 +282,10 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * then waits for the last unpack.  Arguments as kvx_repack (kvx_repack_paged
  * for a paged plan, whose source block table is passed; otherwise it must be
  * NULL).  Two runs of one pipe must not overlap (they share the slots);
- * runs of different pipes may. */
+ * runs of different pipes may.  A bad argument is reported before anything is
+ * enqueued; a launch or enqueue failure part way through returns its status
+ * with the cache partly written, and the caller's stream still waits for the
+ * chunks already enqueued. */
 typedef struct kvx_pipe_s kvx_pipe_t; /* opaque, library-owned */
 
 typedef struct {

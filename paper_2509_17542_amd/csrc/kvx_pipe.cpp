@@ -65,6 +65,16 @@ kvx_status chunk_plan(const kvx_plan_t* p, int n, kvx_plan_t** out)
 
 bool ok(hipError_t e) { return e == hipSuccess; }
 
+// A run that fails part way has chunks enqueued on the pipe's streams: the
+// caller's stream still waits for them, so that buffers it releases after the
+// failure are no longer in use.
+kvx_status stop(kvx_pipe_s* q, hipStream_t s0, kvx_status st)
+{
+    for (hipStream_t s : {q->h2d, q->unpack})
+        if (ok(hipEventRecord(q->start, s))) (void)hipStreamWaitEvent(s0, q->start, 0);
+    return st;
+}
+
 }  // namespace
 
 extern "C" {
@@ -183,10 +193,10 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
         // pack into the host slot (caller's stream): the slot's previous
         // chunk must have been copied to the device
         if (reuse && !ok(hipStreamWaitEvent(s0, q->received[s], 0)))
-            return fail(KVX_EDEVICE, "stream wait failed");
+            return stop(q, s0, fail(KVX_EDEVICE, "stream wait failed"));
         kvx_status st = kvx::launch_shifted(cp, kvx::kPack, shift, shards, sbt, sbt_stride,
                                             nullptr, host_dev, nullptr, nullptr, 0, stream);
-        if (st != KVX_OK) return st;
+        if (st != KVX_OK) return stop(q, s0, st);
         bool good = ok(hipEventRecord(q->packed[s], s0));
         // host -> device: the receive slot must have been unpacked
         good = good && ok(hipStreamWaitEvent(q->h2d, q->packed[s], 0));
@@ -195,18 +205,20 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
                ok(hipEventRecord(q->received[s], q->h2d));
         // unpack (pipe's stream)
         good = good && ok(hipStreamWaitEvent(q->unpack, q->received[s], 0));
-        if (!good) return fail(KVX_EDEVICE, "copy or event enqueue failed: %s",
-                               hipGetErrorString(hipGetLastError()));
+        if (!good)
+            return stop(q, s0, fail(KVX_EDEVICE, "copy or event enqueue failed: %s",
+                                    hipGetErrorString(hipGetLastError())));
         st = kvx::launch_shifted(cp, kvx::kUnpack, shift, nullptr, nullptr, 0, recv, cache,
                                  scales, bt, bt_stride, q->unpack);
-        if (st != KVX_OK) return st;
+        if (st != KVX_OK) return stop(q, s0, st);
         if (!ok(hipEventRecord(q->unpacked[s], q->unpack)))
-            return fail(KVX_EDEVICE, "event record failed");
+            return stop(q, s0, fail(KVX_EDEVICE, "event record failed"));
     }
     // the caller's stream continues after the last unpack (the unpack stream
     // runs its chunks in order)
     const int last = (q->num_chunks - 1) % q->slots;
-    if (!ok(hipStreamWaitEvent(s0, q->unpacked[last], 0))) return fail(KVX_EDEVICE, "stream wait failed");
+    if (!ok(hipStreamWaitEvent(s0, q->unpacked[last], 0)))
+        return stop(q, s0, fail(KVX_EDEVICE, "stream wait failed"));
     return KVX_OK;
 }
 
