@@ -174,7 +174,70 @@ SMALL_PAGED = {
 }
 
 
+
+def random_workloads(seed: int, n: int) -> dict:
+    """n small valid workloads drawn over every option of the descriptor:
+    heads 1..16 with every TP degree that divides them or that they divide
+    (replicated heads included), any decode rank, all dtype pairs and
+    dequantising caches, the three source orders, head_dim 8..1024, page
+    sizes that are not powers of two, empty requests, value scales over five
+    decades.  Each pool stays under 8 MiB so that the oracle runs in
+    milliseconds."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    while len(out) < n:
+        H = int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16]))
+        tps = [t for t in range(1, H + 1) if H % t == 0] + [2 * H, 4 * H]
+        src_tp, dst_tp = int(rng.choice(tps)), int(rng.choice(tps))
+        src = str(rng.choice(["fp16", "bf16"]))
+        dst = str(rng.choice(["fp16", "bf16", "e4m3fn", "e5m2"]))
+        cache = str(rng.choice(["fp16", "bf16"])) if dst in FP8_NAMES and rng.random() < 0.4 else ""
+        esz = 1 if dst in FP8_NAMES else 2
+        dims = [d for d in (8, 16, 24, 32, 40, 48, 64, 80, 96, 128, 192, 256, 512, 1024)
+                if d * esz <= 1024 and (d * esz) % 16 == 0]
+        D = int(rng.choice(dims))
+        order = str(rng.choice(["thd", "htd", "paged"]))
+        bs = int(rng.choice([1, 2, 3, 5, 8, 16, 17, 32, 64]))
+        R = int(rng.integers(0, 6))
+        lens = [0 if rng.random() < 0.15 else int(rng.integers(1, 121)) for _ in range(R)]
+        L = int(rng.integers(1, 4))
+        nb = sum((t + bs - 1) // bs for t in lens) + int(rng.integers(0, 7))
+        sbs = snb = 0
+        if order == "paged":
+            sbs = int(rng.choice([1, 3, 4, 7, 16, 32]))
+            snb = max(1, sum((t + sbs - 1) // sbs for t in lens) + int(rng.integers(0, 7)))
+        hd = H // dst_tp if dst_tp <= H else 1
+        hs = H // src_tp if src_tp <= H else 1
+        csz = 1 if (cache or dst) in FP8_NAMES else 2
+        if L * 2 * max(nb, 1) * bs * hd * D * csz > 8 << 20 or \
+                L * 2 * max(sum(lens), snb * sbs) * hs * D * 2 > 8 << 20:
+            continue
+        sigma = float(10.0 ** rng.uniform(-2.0, 2.5))
+        frac = float(rng.choice([0.0, 0.01]))
+        k = len(out)
+        out[f"rand{k}"] = W.Workload(
+            f"rand{k}", L, L, H, D, src_tp, dst_tp, int(rng.integers(0, dst_tp)), src, dst, order,
+            bs, max(nb, 1), R, 0, 0, seed=int(rng.integers(1, 1 << 30)), sigma=sigma,
+            outlier_frac=frac, outlier_value=float(rng.uniform(100.0, 60000.0)),
+            head_scale_log10=(-2.0, 2.0) if rng.random() < 0.3 else None,
+            lens_override=tuple(lens), src_block_size=sbs, src_num_blocks=snb, cache_dtype=cache)
+    return out
+
+
+
+def out_of_pool(table, limit, rng, frac=0.1):
+    """A copy of a block table with about `frac` of its used entries (>= 0)
+    replaced by ids outside [0, limit): -1 .. -3 or limit .. limit + 99.
+    Rows that map to such a page are neither read nor written."""
+    t = np.array(table, dtype=np.int32, copy=True)
+    used = np.argwhere(t >= 0)
+    pick = used[rng.random(len(used)) < frac]
+    for i, j in pick:
+        t[i, j] = -int(rng.integers(1, 4)) if rng.random() < 0.5 else limit + int(rng.integers(0, 100))
+    return t
+
 FP8_NAMES = ("e4m3fn", "e5m2")
+RANDOM = random_workloads(2509_17542, 64)
 # 8-bit formats: torch dtype and largest finite value (the scale's divisor)
 _FP8 = {"e4m3fn": (torch.float8_e4m3fn, 448.0), "e5m2": (torch.float8_e5m2, 57344.0)}
 
@@ -256,6 +319,10 @@ def consumer_rows(w, lens, r, layer0, nlayers):
     x = torch.from_numpy(W.logical_values(w, lens, r, layer0, nlayers, heads))
     x = x.to(_TDT[w.src_dtype])                                     # [L][2][Hd][T][D]
     x = x.permute(0, 1, 3, 2, 4).contiguous()                      # [L][2][T][Hd][D]
+    if x.numel() == 0:   # an empty request: no rows (torch cannot view empty tensors as bytes)
+        row = w.head_dim * (1 if w.cdt in FP8_NAMES else 2)
+        return (np.zeros((*x.shape[:4], row), np.uint8),
+                np.zeros(x.shape[:4], np.float32) if w.cdt in FP8_NAMES else None)
     if w.dst_dtype == w.src_dtype:
         return x.view(torch.uint8).numpy().reshape(*x.shape[:4], 2 * w.head_dim), None
     if w.dst_dtype in ("bf16", "fp16"):

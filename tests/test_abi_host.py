@@ -8,7 +8,8 @@ import re
 import numpy as np
 import pytest
 
-from cases import FP8_NAMES, FULL, SMALL, SMALL_DEQUANT, SMALL_E5M2, SMALL_PAGED, oracle_problem
+from cases import (FP8_NAMES, FULL, RANDOM, SMALL, SMALL_DEQUANT, SMALL_E5M2, SMALL_PAGED,
+                   oracle_problem)
 from conftest import ROOT
 
 import oracle as O
@@ -47,9 +48,9 @@ def desc_for(w, lens, **over):
 
 
 @pytest.mark.parametrize("name", list(SMALL) + list(SMALL_PAGED) + list(SMALL_DEQUANT) +
-                         list(SMALL_E5M2) + list(FULL))
+                         list(SMALL_E5M2) + list(FULL) + list(RANDOM))
 def test_plan_bytes_and_segments(name):
-    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | SMALL_E5M2 | FULL)[name]
+    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT | SMALL_E5M2 | FULL | RANDOM)[name]
     lens = W.seq_lens(w)
     plan = K.kvx_plan(desc_for(w, lens))
     info = K.kvx_plan_info_get(plan)

@@ -5,8 +5,8 @@ cases, round-trip identities and write-set enumeration."""
 import numpy as np
 import pytest
 
-from cases import (SMALL, SMALL_SHAPES, TINY, L8B, consumer_rows, dst_size, gather_pages, inputs,
-                   oracle_problem, written_mask)
+from cases import (RANDOM, SMALL, SMALL_SHAPES, TINY, L8B, consumer_rows, dst_size, gather_pages,
+                   inputs, oracle_problem, out_of_pool, wire_size, written_mask)
 from conftest import golden_lines
 
 import oracle as O
@@ -76,9 +76,9 @@ def test_head_map_with_replicated_heads(H, ts, td):
 
 # ---- the decode side reads what the prefill side wrote ------------------------
 
-@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_SHAPES))
+@pytest.mark.parametrize("name", list(SMALL) + list(SMALL_SHAPES) + list(RANDOM))
 def test_repack_matches_paged_reader(name):
-    w = (SMALL | SMALL_SHAPES)[name]
+    w = (SMALL | SMALL_SHAPES | RANDOM)[name]
     lens, bt, stride, shards = inputs(w)
     p = oracle_problem(O, w, lens)
     cache, scales = _pool(p)
@@ -91,22 +91,23 @@ def test_repack_matches_paged_reader(name):
             assert np.array_equal(got_s.view(np.uint32), want_s.view(np.uint32)), (name, r)
 
 
-@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("name", list(SMALL) + list(RANDOM))
 def test_pack_matches_flat_logical_layout(name):
     """The transfer tensor of request r is [L][2][T][Hd][D] (+ [L][2][T][Hd]
     scales), 256-byte aligned segments, padding untouched."""
-    w = SMALL[name]
+    w = (SMALL | RANDOM)[name]
     lens, bt, stride, shards = inputs(w)
     p = oracle_problem(O, w, lens)
     doff, soff, total = O.wire_layout(p)
     wire = O.pack(p, shards)
     touched = np.zeros(total, dtype=bool)
     end = 0
+    wt = w.replace(cache_dtype="")   # the transfer tensor's rows (8-bit codes before dequantising)
     for r in range(len(lens)):
         T = int(lens[r])
-        n = w.layers * 2 * T * w.hd * w.head_dim * dst_size(w)
+        n = w.layers * 2 * T * w.hd * w.head_dim * wire_size(w)
         assert doff[r] % 256 == 0 and doff[r] >= end
-        want, want_s = consumer_rows(w, lens, r, 0, w.layers)
+        want, want_s = consumer_rows(wt, lens, r, 0, w.layers)
         got = wire[doff[r]:doff[r] + n].reshape(want.shape)
         assert np.array_equal(got, want), (name, r)
         touched[doff[r]:doff[r] + n] = True
@@ -122,12 +123,12 @@ def test_pack_matches_flat_logical_layout(name):
     assert np.all(wire[~touched] == W.SENTINEL)
 
 
-@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("name", list(SMALL) + list(RANDOM))
 def test_write_set_is_exactly_the_used_slots(name):
     """Two runs with different pool fills: the bytes that differ were never
     written.  They must be exactly the slots outside every request's pages
     (unused pages, and slots past T in a last page)."""
-    w = SMALL[name]
+    w = (SMALL | RANDOM)[name]
     lens, bt, stride, shards = inputs(w)
     p = oracle_problem(O, w, lens)
     runs = []
@@ -146,9 +147,9 @@ def test_write_set_is_exactly_the_used_slots(name):
         assert np.array_equal((s0 == s1).all(-1), m)
 
 
-@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("name", list(SMALL) + list(RANDOM))
 def test_unpack_of_pack_equals_repack(name):
-    w = SMALL[name]
+    w = (SMALL | RANDOM)[name]
     lens, bt, stride, shards = inputs(w)
     p = oracle_problem(O, w, lens)
     c1, s1 = _pool(p)
@@ -158,6 +159,46 @@ def test_unpack_of_pack_equals_repack(name):
     assert np.array_equal(c1, c2)
     if s1 is not None:
         assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+@pytest.mark.parametrize("name", list(RANDOM))
+def test_out_of_pool_pages_are_skipped(name):
+    """Block-table entries outside the pool (decode pages, and for paged
+    sources the prefill pages) are skipped, not errors: the repack with about
+    10% of the entries moved out of range equals the repack with the valid
+    tables, except that the slots of a skipped decode page, and the token
+    slots whose source page was skipped, keep the pool's fill."""
+    w = RANDOM[name]
+    rng = np.random.default_rng(int(name[4:]))
+    lens, bt, stride, shards = inputs(w)
+    sbt = sbt2 = None
+    if w.src_order == "paged":
+        sbt, _ = W.src_block_table(w, lens)
+        sbt2 = out_of_pool(sbt, w.src_num_blocks, rng)
+    bt2 = out_of_pool(bt, w.num_blocks, rng)
+    p = oracle_problem(O, w, lens, sbt=sbt)
+    full, full_s = _pool(p)
+    O.repack(p, shards, full, full_s, bt, stride)
+    got, got_s = _pool(p)
+    O.repack(oracle_problem(O, w, lens, sbt=sbt2), shards, got, got_s, bt2, stride)
+    row = w.hd * w.head_dim * dst_size(w)
+    want = full.reshape(w.layers, 2, w.num_blocks, w.block_size, row).copy()
+    want_s = None if full_s is None else \
+        full_s.view(np.uint32).reshape(w.layers, 2, w.num_blocks, w.block_size, w.hd).copy()
+    fill = np.full(4, W.SENTINEL, np.uint8).view(np.uint32)[0]
+    for r, T in enumerate(lens):
+        for t in range(int(T)):
+            k = t // w.block_size
+            skipped = bt2[r, k] != bt[r, k]
+            if sbt is not None:
+                skipped |= sbt2[r, t // w.src_block_size] != sbt[r, t // w.src_block_size]
+            if skipped:
+                want[:, :, bt[r, k], t % w.block_size] = W.SENTINEL
+                if want_s is not None:
+                    want_s[:, :, bt[r, k], t % w.block_size] = fill
+    assert np.array_equal(got.reshape(want.shape), want)
+    if want_s is not None:
+        assert np.array_equal(got_s.view(np.uint32).reshape(want_s.shape), want_s)
 
 
 # ---- special cases and identities ----------------------------------------------
