@@ -151,12 +151,31 @@ def main():
         kern = [a.elapsed_time(b) for a, b in ev]
         return wall * 1e3, statistics.mean(kern), min(kern), statistics.median(kern)
 
+    # Prefill stages are independent transfers: each stage's launch goes on a
+    # stream of its own (default priority), forked from the timed stream and
+    # joined back into it, so that the stages write their halves of the pool
+    # at the same time.
+    side = [torch.cuda.Stream() for _ in stages[1:]]
+    fork = torch.cuda.Event()
+
+    def per_stage(launch):
+        if side:
+            fork.record(stream)
+            for s in side:
+                s.wait_event(fork)
+        for k, st in enumerate([stream] + side):
+            launch(k, st)
+        for s in side:
+            stream.wait_stream(s)
+
     def repack():
-        for plan, dsh in zip(plans, stage_dshards):
+        def launch(k, st):
             if paged:
-                K.kvx_repack_paged(plan, dsh, sbt_d, sstride, cache, scales, bt_d, stride, stream)
+                K.kvx_repack_paged(plans[k], stage_dshards[k], sbt_d, sstride, cache, scales, bt_d,
+                                   stride, st)
             else:
-                K.kvx_repack(plan, dsh, cache, scales, bt_d, stride, stream)
+                K.kvx_repack(plans[k], stage_dshards[k], cache, scales, bt_d, stride, st)
+        per_stage(launch)
 
     log(f"repack: {args.warmup} warm-up + {args.steps} timed steps")
     ms_step, k_mean, k_min, k_med = timed(repack, args.steps, args.warmup)
@@ -178,7 +197,8 @@ def main():
                    **({"cache_dtype": w.cache_dtype} if w.cache_dtype else {}),
                    "src_order": w.src_order, "block_size": w.block_size,
                    "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes},
-        **({"prefill_stages": [list(st) for st in stages], "launches_per_step": len(stages)}
+        **({"prefill_stages": [list(st) for st in stages], "launches_per_step": len(stages),
+            "streams_per_step": len(stages)}
            if len(stages) > 1 else {}),
         **({"src_pages": {"block_size": w.src_block_size, "pool_blocks": w.src_num_blocks}}
            if paged else {}),
@@ -199,15 +219,16 @@ def main():
         wires = [torch.empty(int(i.wire_bytes), dtype=torch.uint8, device="cuda") for i in infos]
 
         def pack():
-            for plan, dsh, wire in zip(plans, stage_dshards, wires):
+            def launch(k, st):
                 if paged:
-                    K.kvx_pack_paged(plan, dsh, sbt_d, sstride, wire, stream)
+                    K.kvx_pack_paged(plans[k], stage_dshards[k], sbt_d, sstride, wires[k], st)
                 else:
-                    K.kvx_pack(plan, dsh, wire, stream)
+                    K.kvx_pack(plans[k], stage_dshards[k], wires[k], st)
+            per_stage(launch)
 
         def unpack():
-            for plan, wire in zip(plans, wires):
-                K.kvx_unpack(plan, wire, cache, scales, bt_d, stride, stream)
+            per_stage(lambda k, st: K.kvx_unpack(plans[k], wires[k], cache, scales, bt_d, stride,
+                                                 st))
 
         pack_bytes = sum(i.read_bytes_pack + i.write_bytes_pack for i in infos)
         unpack_bytes = sum(i.read_bytes_unpack + i.write_bytes_unpack for i in infos)
@@ -219,7 +240,9 @@ def main():
         del wires
 
         # per-request latency: single-request plans (one per prefill stage) per
-        # request, host call to completion
+        # request, host call to completion; the stages of one request go on the
+        # timed stream one after the other (for launches this small a fork and
+        # join across streams costs more than it overlaps)
         lat = []
         src_off = 0
         for r, T in enumerate(lens.tolist()):
