@@ -76,7 +76,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 7
+#define KVX_ABI_VERSION 8
 
 typedef enum {
     KVX_OK = 0,
@@ -171,7 +171,8 @@ typedef struct {
  * transfer-tensor row (head_dim
  * * dst element size) above 1024 bytes; more than 1024 heads per decode rank; more than
  * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
- * (sum over requests of ceil(T_r / block_size)).  KVX_ENOMEM / KVX_EDEVICE if
+ * (sum over requests of ceil(T_r / block_size)); a decode cache, source
+ * shard or transfer tensor of 2^62 bytes or more.  KVX_ENOMEM / KVX_EDEVICE if
  * the table cannot be allocated. */
 kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);
 
@@ -181,6 +182,29 @@ kvx_status kvx_plan_info_get(const kvx_plan_t *plan, kvx_plan_info *info);
  * (scale_off = -1 unless dst is 8-bit).  KVX_EINVAL for r out of range. */
 kvx_status kvx_plan_segment(const kvx_plan_t *plan, int32_t r, int64_t *data_off,
                             int64_t *scale_off);
+
+/* Sizes of the buffers that launches with this plan touch.  The launch calls
+ * take bare pointers and cannot check them: these are what a caller
+ * allocates and what a binding checks before it launches (host only).
+ * KVX_EINVAL for a NULL argument. */
+typedef struct {
+    uint64_t wire_bytes;    /* transfer tensor, as kvx_plan_info.wire_bytes */
+    uint64_t cache_bytes;   /* decode cache [dst layers][2][NB][bs][Hd][D] of the cache type */
+    uint64_t scale_bytes;   /* its fp32 scales [dst layers][2][NB][bs][Hd]; 0 for a 16-bit cache */
+    int32_t num_requests;   /* rows of the block table (and of a source block table) */
+    int32_t src_tp;         /* entries of the src_shards array */
+} kvx_buffer_sizes;
+
+kvx_status kvx_plan_buffer_sizes(const kvx_plan_t *plan, kvx_buffer_sizes *out);
+
+/* Bytes from the start of prefill shard j within which a pack or repack
+ * reads: the shard's requests back to back (2 x src layers x T_r x Hs x D
+ * elements each) for a contiguous source, its whole pool (2 x src layers x
+ * src_num_blocks x src_block_size x Hs x D elements) for a paged one; 0 when
+ * the decode rank reads nothing from shard j (its pointer may then be NULL)
+ * or the plan has no tokens.  KVX_EINVAL for a NULL argument or j outside
+ * [0, src_tp). */
+kvx_status kvx_plan_shard_bytes(const kvx_plan_t *plan, int32_t j, uint64_t *bytes);
 
 /* Frees the plan and its device table (synchronous; the caller ensures no
  * launch using it is still pending).  NULL is accepted. */

@@ -25,7 +25,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # the struct layouts below are those of this version of include/kvx.h
-ABI_VERSION = 7
+ABI_VERSION = 8
 if _lib.kvx_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements kvx ABI {_lib.kvx_abi_version()}, this binding "
                       f"ABI {ABI_VERSION}: rebuild the library")
@@ -66,6 +66,14 @@ class kvx_plan_info(ctypes.Structure):
         ("read_bytes_repack", ctypes.c_int64), ("write_bytes_repack", ctypes.c_int64),
         ("max_blocks_per_request", ctypes.c_int32), ("num_items", ctypes.c_int32),
         ("device", ctypes.c_int32), ("max_src_blocks_per_request", ctypes.c_int32),
+    ]
+
+
+class kvx_buffer_sizes(ctypes.Structure):
+    _fields_ = [
+        ("wire_bytes", ctypes.c_uint64), ("cache_bytes", ctypes.c_uint64),
+        ("scale_bytes", ctypes.c_uint64), ("num_requests", ctypes.c_int32),
+        ("src_tp", ctypes.c_int32),
     ]
 
 
@@ -121,6 +129,10 @@ _lib.kvx_plan_info_get.argtypes = [_vp, ctypes.POINTER(kvx_plan_info)]
 _lib.kvx_plan_segment.restype = ctypes.c_int
 _lib.kvx_plan_segment.argtypes = [_vp, _i32, ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64)]
+_lib.kvx_plan_buffer_sizes.restype = ctypes.c_int
+_lib.kvx_plan_buffer_sizes.argtypes = [_vp, ctypes.POINTER(kvx_buffer_sizes)]
+_lib.kvx_plan_shard_bytes.restype = ctypes.c_int
+_lib.kvx_plan_shard_bytes.argtypes = [_vp, _i32, ctypes.POINTER(ctypes.c_uint64)]
 _lib.kvx_plan_destroy.restype = ctypes.c_int
 _lib.kvx_plan_destroy.argtypes = [_vp]
 _lib.kvx_pack.restype = ctypes.c_int
@@ -155,7 +167,8 @@ _lib.kvx_pd_evaluate.restype = ctypes.c_int
 _lib.kvx_pd_evaluate.argtypes = [ctypes.POINTER(kvx_pd_problem)] + [_i32] * 6 + \
     [ctypes.POINTER(kvx_pd_choice)]
 
-EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_destroy", "kvx_pack",
+EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_buffer_sizes",
+           "kvx_plan_shard_bytes", "kvx_plan_destroy", "kvx_pack",
            "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged",
            "kvx_check_block_table", "kvx_check_src_block_table", "kvx_pipe_create",
            "kvx_pipe_info_get", "kvx_pipe_run", "kvx_pipe_destroy", "kvx_last_error",
@@ -185,12 +198,24 @@ def _stream(stream) -> int | None:
 
 
 class Plan:
-    """Owns a kvx_plan_t*; destroyed with kvx_plan_destroy."""
+    """Owns a kvx_plan_t*; destroyed with kvx_plan_destroy.  Holds the sizes
+    its launches touch (kvx_plan_buffer_sizes, kvx_plan_shard_bytes) for the
+    checks of tensor arguments."""
 
     _destroy = _lib.kvx_plan_destroy  # kept reachable during interpreter shutdown
 
     def __init__(self, handle: int):
         self.handle = handle
+        self.sizes = kvx_buffer_sizes()
+        _check(_lib.kvx_plan_buffer_sizes(self, ctypes.byref(self.sizes)))
+        self.shard_bytes = []
+        b = ctypes.c_uint64()
+        for j in range(self.sizes.src_tp):
+            _check(_lib.kvx_plan_shard_bytes(self, j, ctypes.byref(b)))
+            self.shard_bytes.append(b.value)
+        info = kvx_plan_info()
+        _check(_lib.kvx_plan_info_get(self, ctypes.byref(info)))
+        self.touches = info.num_items > 0   # launches read or write anything
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
@@ -259,42 +284,103 @@ def kvx_plan_segment(plan: Plan, r: int) -> tuple[int, int]:
     return d.value, s.value
 
 
+def kvx_plan_buffer_sizes(plan: Plan) -> kvx_buffer_sizes:
+    out = kvx_buffer_sizes()
+    _check(_lib.kvx_plan_buffer_sizes(plan, ctypes.byref(out)))
+    return out
+
+
+def kvx_plan_shard_bytes(plan: Plan, j: int) -> int:
+    b = ctypes.c_uint64()
+    _check(_lib.kvx_plan_shard_bytes(plan, j, ctypes.byref(b)))
+    return b.value
+
+
 def kvx_plan_destroy(plan: Plan) -> None:
     h, plan.handle = plan.handle, None
     _check(_lib.kvx_plan_destroy(h))
 
 
-def _shard_array(shards):
+def _need(x, nbytes: int, what: str, dtype=None) -> None:
+    """A torch tensor argument must be a contiguous device tensor (of `dtype`
+    where given) holding at least the `nbytes` the plan's launches touch
+    through it.  Bare addresses (ints) and None pass unchecked: the C calls
+    check NULL and alignment, sizes are the caller's contract there."""
+    if not isinstance(x, torch.Tensor) or nbytes <= 0:
+        return
+    if x.device.type != "cuda":
+        raise ValueError(f"{what} must be a device tensor, not one on {x.device}")
+    if not x.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and x.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, not {x.dtype}")
+    have = x.numel() * x.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what} holds {have} bytes; the plan touches {nbytes}")
+
+
+def _shard_array(plan: Plan, shards):
+    """The host array of src_tp shard addresses, each read shard checked."""
+    shards = list(shards)
+    if len(shards) < plan.sizes.src_tp:
+        raise ValueError(f"{len(shards)} source shards given; the plan has src_tp = "
+                         f"{plan.sizes.src_tp}")
     arr = (_vp * max(len(shards), 1))()
     for j, s in enumerate(shards):
+        if j < plan.sizes.src_tp:
+            _need(s, plan.shard_bytes[j], f"src_shards[{j}]")
         arr[j] = _addr(s)
     return arr
 
 
+def _table_bytes(plan: Plan, stride: int) -> int:
+    """int32 bytes of a [num_requests][stride] block table, if launches read it."""
+    return 4 * plan.sizes.num_requests * max(int(stride), 0) if plan.touches else 0
+
+
+def _need_pool(plan: Plan, cache, scales, block_table, bt_stride: int) -> None:
+    if not plan.touches:
+        return
+    _need(cache, plan.sizes.cache_bytes, "cache")
+    _need(scales, plan.sizes.scale_bytes, "scales", torch.float32)
+    _need(block_table, _table_bytes(plan, bt_stride), "block_table", torch.int32)
+
+
 def kvx_pack(plan: Plan, src_shards, wire, stream=None) -> None:
-    _check(_lib.kvx_pack(plan, _shard_array(src_shards), _addr(wire), _stream(stream)))
+    if plan.touches:
+        _need(wire, plan.sizes.wire_bytes, "wire")
+    _check(_lib.kvx_pack(plan, _shard_array(plan, src_shards), _addr(wire), _stream(stream)))
 
 
 def kvx_unpack(plan: Plan, wire, cache, scales, block_table, bt_stride: int, stream=None) -> None:
+    if plan.touches:
+        _need(wire, plan.sizes.wire_bytes, "wire")
+    _need_pool(plan, cache, scales, block_table, bt_stride)
     _check(_lib.kvx_unpack(plan, _addr(wire), _addr(cache), _addr(scales), _addr(block_table),
                            bt_stride, _stream(stream)))
 
 
 def kvx_repack(plan: Plan, src_shards, cache, scales, block_table, bt_stride: int,
                stream=None) -> None:
-    _check(_lib.kvx_repack(plan, _shard_array(src_shards), _addr(cache), _addr(scales),
+    _need_pool(plan, cache, scales, block_table, bt_stride)
+    _check(_lib.kvx_repack(plan, _shard_array(plan, src_shards), _addr(cache), _addr(scales),
                            _addr(block_table), bt_stride, _stream(stream)))
 
 
 def kvx_pack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int, wire,
                    stream=None) -> None:
-    _check(_lib.kvx_pack_paged(plan, _shard_array(src_shards), _addr(src_block_table),
+    if plan.touches:
+        _need(wire, plan.sizes.wire_bytes, "wire")
+    _need(src_block_table, _table_bytes(plan, src_bt_stride), "src_block_table", torch.int32)
+    _check(_lib.kvx_pack_paged(plan, _shard_array(plan, src_shards), _addr(src_block_table),
                                src_bt_stride, _addr(wire), _stream(stream)))
 
 
 def kvx_repack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int, cache, scales,
                      block_table, bt_stride: int, stream=None) -> None:
-    _check(_lib.kvx_repack_paged(plan, _shard_array(src_shards), _addr(src_block_table),
+    _need_pool(plan, cache, scales, block_table, bt_stride)
+    _need(src_block_table, _table_bytes(plan, src_bt_stride), "src_block_table", torch.int32)
+    _check(_lib.kvx_repack_paged(plan, _shard_array(plan, src_shards), _addr(src_block_table),
                                  src_bt_stride, _addr(cache), _addr(scales), _addr(block_table),
                                  bt_stride, _stream(stream)))
 
@@ -302,7 +388,8 @@ def kvx_repack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int
 def _host_table(table):
     """(keep-alive object, address) of a contiguous int32 host table."""
     if isinstance(table, torch.Tensor):
-        assert table.device.type == "cpu" and table.dtype == torch.int32
+        if table.device.type != "cpu" or table.dtype != torch.int32:
+            raise ValueError("a host block table must be an int32 CPU tensor or array")
         keep = table.contiguous()
         return keep, keep.data_ptr()
     import numpy as np
@@ -346,7 +433,9 @@ def kvx_pipe_info_get(pipe: Pipe) -> kvx_pipe_info:
 
 def kvx_pipe_run(pipe: Pipe, src_shards, src_block_table, src_bt_stride: int, cache, scales,
                  block_table, bt_stride: int, stream=None) -> None:
-    _check(_lib.kvx_pipe_run(pipe, _shard_array(src_shards), _addr(src_block_table),
+    _need_pool(pipe.plan, cache, scales, block_table, bt_stride)
+    _need(src_block_table, _table_bytes(pipe.plan, src_bt_stride), "src_block_table", torch.int32)
+    _check(_lib.kvx_pipe_run(pipe, _shard_array(pipe.plan, src_shards), _addr(src_block_table),
                              src_bt_stride, _addr(cache), _addr(scales), _addr(block_table),
                              bt_stride, _stream(stream)))
 

@@ -25,6 +25,7 @@ struct kvx_plan_s {
     int32_t max_blocks = 0;
     int32_t max_src_blocks = 0;   // paged sources: pages per request on the prefill side
     uint64_t wire_bytes = 0;
+    int64_t src_elems = 0;        // elements of a read source shard the launches may touch
     int64_t total_tokens = 0;
     int64_t elems_rows = 0;       // sum over requests of L*2*T*Hd
     int device = -1;

@@ -140,6 +140,26 @@ kvx_status validate(const kvx_desc* d)
                     d->dst_layer_offset + d->num_layers, dst_layers_of(*d));
     if (int64_t(src_layers_of(*d)) * 2 > 65535 || int64_t(dst_layers_of(*d)) * 2 > 65535)
         return fail(KVX_EUNSUPPORTED, "2 * layers above 65535");
+    // every buffer stays below 2^62 bytes, so that the 64-bit offsets of the
+    // planner and the kernels cannot overflow (sizes are compared in double
+    // precision: relative error below 2^-50, far inside the 2x margin)
+    const double lim = 4611686018427387904.0;  // 2^62
+    const double hs = heads_per_rank(d->num_kv_heads, d->src_tp);
+    const double hd = heads_per_rank(d->num_kv_heads, d->dst_tp);
+    const double row_cache = hd * d->head_dim * dtype_size(cdt);
+    if (2.0 * dst_layers_of(*d) * double(d->num_blocks) * d->block_size * row_cache > lim)
+        return fail(KVX_EUNSUPPORTED, "decode cache above 2^62 bytes");
+    const double row_src = hs * d->head_dim * dtype_size(d->src_dtype);
+    double src = 0, wire = 0;
+    if (d->src_order == KVX_PAGED)
+        src = 2.0 * src_layers_of(*d) * double(d->src_num_blocks) * d->src_block_size * row_src;
+    for (int r = 0; r < d->num_requests; ++r) {
+        if (d->src_order != KVX_PAGED) src += 2.0 * src_layers_of(*d) * d->seq_lens[r] * row_src;
+        wire += 2.0 * d->num_layers * d->seq_lens[r] * hd *
+                    (double(d->head_dim) * dtype_size(d->dst_dtype) + 4) + 512;
+    }
+    if (src > lim) return fail(KVX_EUNSUPPORTED, "source shard above 2^62 bytes");
+    if (wire > lim) return fail(KVX_EUNSUPPORTED, "transfer tensor above 2^62 bytes");
     return KVX_OK;
 }
 
@@ -236,6 +256,9 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
         p->elems_rows += rows;
     }
     p->wire_bytes = uint64_t(align256(wire));
+    p->src_elems = paged ? 2 * int64_t(src_layers_of(d)) * d.src_num_blocks * d.src_block_size *
+                               p->hs * d.head_dim
+                         : src_off;
     const int64_t rpp = kvx::kThreads >> p->lg_lpr;  // rows per workgroup pass
     int max_n = 0;
     for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
@@ -311,6 +334,34 @@ kvx_status kvx_plan_segment(const kvx_plan_t* p, int32_t r, int64_t* data_off, i
         return fail(KVX_EINVAL, "request %d outside [0, %d)", r, p->d.num_requests);
     if (data_off) *data_off = p->wire_data[r];
     if (scale_off) *scale_off = p->wire_scale[r];
+    return KVX_OK;
+}
+
+kvx_status kvx_plan_buffer_sizes(const kvx_plan_t* p, kvx_buffer_sizes* out)
+{
+    if (!p || !out) return fail(KVX_EINVAL, "NULL plan or out");
+    std::memset(out, 0, sizeof *out);
+    const kvx_desc& d = p->d;
+    const uint64_t slots = 2 * uint64_t(dst_layers_of(d)) * uint64_t(d.num_blocks) *
+                           uint64_t(d.block_size) * uint64_t(p->hd);
+    out->wire_bytes = p->wire_bytes;
+    out->cache_bytes = slots * uint64_t(d.head_dim) * uint64_t(p->esz_cache);
+    out->scale_bytes = is_fp8(p->cache_dtype) ? slots * 4 : 0;
+    out->num_requests = d.num_requests;
+    out->src_tp = d.src_tp;
+    return KVX_OK;
+}
+
+kvx_status kvx_plan_shard_bytes(const kvx_plan_t* p, int32_t j, uint64_t* bytes)
+{
+    if (!p || !bytes) return fail(KVX_EINVAL, "NULL plan or bytes");
+    if (j < 0 || j >= p->d.src_tp)
+        return fail(KVX_EINVAL, "shard %d outside [0, %d)", j, p->d.src_tp);
+    *bytes = 0;
+    if (p->items.empty() ||
+        std::find(p->read_shards.begin(), p->read_shards.end(), j) == p->read_shards.end())
+        return KVX_OK;
+    *bytes = uint64_t(p->src_elems) * uint64_t(p->esz_src);
     return KVX_OK;
 }
 

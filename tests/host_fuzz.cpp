@@ -18,6 +18,7 @@ int main()
 {
     std::mt19937_64 rng(17542);
     auto pick = [&](std::initializer_list<int> v) { return *(v.begin() + rng() % v.size()); };
+    auto pick64 = [&](std::initializer_list<int64_t> v) { return *(v.begin() + rng() % v.size()); };
     int ok = 0, rejected = 0;
     for (int it = 0; it < 100000; ++it) {
         std::vector<int32_t> lens(rng() % 6);
@@ -33,11 +34,11 @@ int main()
         d.dst_dtype = pick({1, 2, 3, 4, 9});
         d.src_order = pick({0, 1, 2, 5});
         d.block_size = pick({0, 1, 5, 16, 64});
-        d.num_blocks = pick({0, 1, 64, 1 << 20});
+        d.num_blocks = pick64({0, 1, 64, 1 << 20, int64_t(1) << 45, int64_t(1) << 62});
         d.num_requests = int32_t(lens.size());
         d.seq_lens = lens.empty() ? nullptr : lens.data();
         d.src_block_size = pick({0, 5, 16});
-        d.src_num_blocks = pick({0, 8, 4096});
+        d.src_num_blocks = pick64({0, 8, 4096, int64_t(1) << 50});
         d.src_layer_offset = pick({0, 0, 1, -1});
         d.src_layers = pick({0, 0, 2, 100});
         d.dst_layer_offset = pick({0, 0, 2});
@@ -48,6 +49,12 @@ int main()
         ++ok;
         kvx_plan_info info;
         kvx_plan_info_get(p, &info);
+        kvx_buffer_sizes sz;
+        kvx_plan_buffer_sizes(p, &sz);
+        for (int j = -1; j <= d.src_tp; ++j) {
+            uint64_t n = 0;
+            kvx_plan_shard_bytes(p, j, &n);
+        }
         for (int r = -1; r <= d.num_requests; ++r) {
             int64_t a, b;
             kvx_plan_segment(p, r, &a, &b);

@@ -2,6 +2,7 @@
 every entry point declared in include/kvx.h; plans validate their problem,
 report the algorithmic byte counts and transfer-tensor segments; argument
 errors come back as status codes."""
+import ctypes
 import os
 import re
 
@@ -9,7 +10,7 @@ import numpy as np
 import pytest
 
 from cases import (FP8_NAMES, FULL, RANDOM, SMALL, SMALL_DEQUANT, SMALL_E5M2, SMALL_PAGED,
-                   oracle_problem)
+                   oracle_problem, rank_heads, read_shards)
 from conftest import ROOT
 
 import oracle as O
@@ -27,11 +28,11 @@ def declared_entry_points():
 
 def test_every_declared_symbol_is_exported():
     names = declared_entry_points()
-    assert len(names) == 19, names
+    assert len(names) == 21, names
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 7
+    assert K.kvx_abi_version() == 8
 
 
 def desc_for(w, lens, **over):
@@ -77,6 +78,26 @@ def test_plan_bytes_and_segments(name):
     assert info.wire_bytes == total
     for r in range(len(lens)):
         assert K.kvx_plan_segment(plan, r) == (int(doff[r]), int(soff[r]))
+    # buffer sizes: the pool the tests allocate, the generator's source shards
+    sz = K.kvx_plan_buffer_sizes(plan)
+    slots = w.layers * 2 * w.num_blocks * w.block_size * w.hd
+    assert sz.wire_bytes == total
+    assert sz.cache_bytes == slots * w.head_dim * (1 if w.cdt in FP8_NAMES else 2)
+    assert sz.scale_bytes == (4 * slots if w.cdt in FP8_NAMES else 0)
+    assert (sz.num_requests, sz.src_tp) == (len(lens), w.src_tp)
+    if w.src_order == "paged":
+        elems = w.layers * 2 * w.src_num_blocks * w.src_block_size * w.hs * w.head_dim
+    else:
+        elems = sum(w.layers * 2 * int(t) * w.hs * w.head_dim for t in lens)
+    # the shard read for each head of the rank: the one holding it, or with
+    # replicated prefill heads its first replica (reading R2)
+    lo, hi = rank_heads(w)
+    read = {g // w.hs if w.src_tp <= w.heads else g * (w.src_tp // w.heads) for g in range(lo, hi)}
+    read = read if info.num_items else set()
+    assert read <= set(read_shards(w))
+    for j in range(w.src_tp):
+        assert K.kvx_plan_shard_bytes(plan, j) == (2 * elems if j in read else 0), j
+    assert plan.shard_bytes == [K.kvx_plan_shard_bytes(plan, j) for j in range(w.src_tp)]
 
 
 BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_rank=0,
@@ -293,3 +314,42 @@ def test_pipe_create_errors_on_the_host():
         with pytest.raises(K.KvxError) as e:
             K.kvx_pipe_create(plan, 1, 2)
         assert e.value.status == K.EDEVICE
+
+
+def test_buffer_size_queries_reject_bad_arguments():
+    plan = K.kvx_plan(desc_for(SMALL["tiny"], W.seq_lens(SMALL["tiny"])))
+    for j in (-1, SMALL["tiny"].src_tp):
+        with pytest.raises(K.KvxError) as e:
+            K.kvx_plan_shard_bytes(plan, j)
+        assert e.value.status == K.EINVAL
+    assert K._lib.kvx_plan_buffer_sizes(plan, None) == K.EINVAL
+    assert K._lib.kvx_plan_buffer_sizes(None, ctypes.byref(K.kvx_buffer_sizes())) == K.EINVAL
+
+
+@pytest.mark.parametrize("over", [dict(num_blocks=1 << 62), dict(num_blocks=1 << 46),
+                                  dict(seq_lens=[(1 << 31) - 1] * 64, num_layers=32767)])
+def test_plan_rejects_buffers_of_2_62_bytes(over):
+    w = SMALL["llama3_8b_small"]
+    d = desc_for(w, W.seq_lens(w), **over)
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_plan(d)
+    assert e.value.status == K.EUNSUPPORTED and "2^62" in str(e.value)
+
+
+def test_binding_checks_tensor_arguments_before_any_launch():
+    """Host tensors, short shard lists and wrong table types are refused by
+    the binding before the C call (on a machine without a GPU the plan is
+    host-only, and nothing reaches a device either way)."""
+    import torch
+    w = SMALL["llama3_8b_small"]
+    lens = W.seq_lens(w)
+    plan = K.kvx_plan(desc_for(w, lens))
+    cpu = torch.empty(16, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="device tensor"):
+        K.kvx_repack(plan, [cpu], None, None, None, 1)
+    with pytest.raises(ValueError, match="source shards"):
+        K.kvx_repack(plan, [], None, None, None, 1)
+    with pytest.raises(ValueError, match="device tensor"):
+        K.kvx_pack(plan, [None], cpu)
+    with pytest.raises(ValueError, match="device tensor"):
+        K.kvx_unpack(plan, None, cpu, None, None, 1)
