@@ -12,10 +12,12 @@ import pytest
 import torch
 
 from cases import (FULL, SMALL, e4m3_sweep_rows, inputs, oracle_problem, pad_rows,
-                   read_shards, sweep_case)
-from gpu_util import (DEV, check_sampled, check_unused_pages, gpu_run, log, oracle_pool)
+                   read_shards, sweep_case, wire_size)
+from gpu_util import (DEV, check_sampled, check_unused_pages, desc_for, dev_u16, gpu_run, log,
+                      oracle_pool, pool)
 
 import oracle as O
+import paper_2509_17542_amd as K
 import workload as W
 
 pytestmark = [pytest.mark.gpu,
@@ -206,3 +208,51 @@ def test_full_fp8_decode_layer_group(group):
     w = FULL["fp8_decode_61l_bf16_e4m3_bs16"]
     l0, nl = w.group_layers(group)
     _full_case(w.name, l0, nl, extra_planes=1, n_req=3)
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_bf16_bs16", "llama3_70b_tp4to2_bf16_bs32",
+                                  "qwen7b_htd_fp16_bf16_bs64", "fp8_decode_61l_bf16_e4m3_bs16"])
+def test_full_pack_then_unpack(name):
+    """The benchmark's pack and unpack at full size: the transfer tensor on
+    sampled (request, plane) segments against the oracle's rows (every request
+    in the first and last plane), then the unpack of that same device
+    transfer tensor on sampled pages, plus sampled unused pages."""
+    w = FULL[name]   # the fp8 decode workload: its first 4-layer group
+    rng = np.random.default_rng(11)
+    lens = W.seq_lens(w)
+    bt, stride = W.block_table(w, lens)
+    log(f"full {name}: generating inputs")
+    shards = W.source_shards(w, lens, 0, w.layers, read_shards(w))
+    plan = K.kvx_plan(desc_for(w, lens))
+    info = K.kvx_plan_info_get(plan)
+    dsh = [dev_u16(s) for s in shards]
+    wire = torch.full((int(info.wire_bytes),), W.SENTINEL, dtype=torch.uint8, device=DEV)
+    log(f"full {name}: pack on GPU")
+    K.kvx_pack(plan, dsh, wire)
+    torch.cuda.synchronize()
+    p = oracle_problem(O, w, lens)
+    doff, soff, _ = O.wire_layout(p)
+    row = w.head_dim * wire_size(w)
+    samples = [(r, 0, 0) for r in range(len(lens))] + \
+              [(r, w.layers - 1, 1) for r in range(len(lens))] + \
+              [(int(rng.integers(len(lens))), int(rng.integers(w.layers)), int(rng.integers(2)))
+               for _ in range(4)]
+    for r, l, kv in samples:
+        T = int(lens[r])
+        want, want_s = O.expected_rows(p, shards, r, l, kv, 0, T)
+        off = int(doff[r]) + (l * 2 + kv) * T * w.hd * row
+        got = wire[off:off + T * w.hd * row].cpu().numpy()
+        assert np.array_equal(got, want.reshape(-1)), (name, r, l, kv)
+        if want_s is not None:
+            so = int(soff[r]) + (l * 2 + kv) * T * w.hd * 4
+            gs = wire[so:so + T * w.hd * 4].cpu().numpy()
+            assert np.array_equal(gs.view(np.uint32), want_s.view(np.uint32)), (name, r, l, kv)
+    log(f"full {name}: unpack on GPU")
+    del dsh
+    cache, scales = pool(w, w.layers)
+    K.kvx_unpack(plan, wire, cache, scales, torch.from_numpy(bt).to(DEV), stride)
+    torch.cuda.synchronize()
+    edge = [(0, 0), (w.layers - 1, 1)]
+    n = check_sampled(w, lens, bt, shards, cache, scales, w.layers, edge, range(len(lens)), rng)
+    check_unused_pages(w, lens, bt, cache, w.layers, rng)
+    log(f"full {name}: {len(samples)} transfer-tensor segments, {n} cache rows checked")
