@@ -90,3 +90,28 @@ def test_pipe_full_llama3_8b():
     n = check_sampled(w, lens, bt, shards, cache, None, w.layers, planes, range(len(lens)), rng)
     check_unused_pages(w, lens, bt, cache, w.layers, rng)
     log(f"pipe full 8B: {n} rows checked")
+
+
+def test_pipe_run_with_a_missing_shard_fails_then_runs():
+    """A run whose first pack is refused (a NULL shard, passed straight to the
+    C call) returns KVX_EINVAL with nothing but stream waits enqueued; the
+    caller's stream still completes, and the next run of the same pipe gives
+    the whole-plan result."""
+    w = SMALL["llama3_8b_small"]
+    lens, bt, stride, shards = inputs(w)
+    plan = K.kvx_plan(desc_for(w, lens))
+    pipe = K.kvx_pipe_create(plan, 1, 2)
+    dsh = [dev_u16(s) for s in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    cache, scales = pool(w, w.layers)
+    null = (K._vp * 1)()
+    st = K._lib.kvx_pipe_run(pipe, null, None, 0, cache.data_ptr(), None, bt_d.data_ptr(), stride,
+                             torch.cuda.current_stream().cuda_stream)
+    assert st == K.EINVAL and "NULL" in K.kvx_last_error()
+    torch.cuda.synchronize()
+    assert bool((cache == W.SENTINEL).all())
+    K.kvx_pipe_run(pipe, dsh, None, 0, cache, scales, bt_d, stride)
+    torch.cuda.synchronize()
+    want_c, _ = oracle_pool(w, lens, bt, stride, shards)
+    assert np.array_equal(cache.cpu().numpy(), want_c)
+    del pipe
