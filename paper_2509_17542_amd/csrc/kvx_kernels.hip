@@ -31,8 +31,9 @@
 // translation.  The first workgroup of each page (part 0, segment 0) therefore
 // also reads one dword of the destination page kPrefetchPages pages further
 // along its XCD's run; the value is discarded, and the translation is cached by
-// the time that page's workgroups store to it.  Stores are non-temporal: the
-// destination is not read again by this launch.
+// the time that page's workgroups store to it.  Row loads and stores are
+// non-temporal: every row is read once and the destination is not read again
+// by this launch.
 //
 // The path is a gather/scatter stream with no reuse and no contraction: the
 // 16-bit conversions are bound by HBM bandwidth, the 8-bit ones (e4m3fn,
@@ -469,6 +470,16 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f)
     return uint32_t((uint64_t(__umulhi(n, f.mul)) + n) >> f.shift);
 }
 
+// One 16-byte vector of a row that this launch reads once (source row or
+// transfer-tensor row): a non-temporal load (global_load_dwordx4 ... nt), so
+// the line is not kept in the caches at the expense of other data.
+__device__ __forceinline__ uint4 load_stream(const char* p)
+{
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    const v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Read one dword at the start of the destination page of the unit
 // kPrefetchPages pages after `unit` (same plane-major order), so that its
 // address translation is cached before that page's workgroups store to it.
@@ -627,7 +638,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         } else {
 #pragma unroll
             for (int k = 0; k < kVecs; ++k)
-                v[k] = *reinterpret_cast<const uint4*>(pl + (ok ? k * second : 0));
+                v[k] = load_stream(pl + (ok ? k * second : 0));
         }
         if constexpr (MODE == kUnpack && kScalesIn)
             sc = *(ok ? sp : reinterpret_cast<const float*>(base));
@@ -649,7 +660,7 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
             } else {
 #pragma unroll
                 for (int k = 0; k < kVecs; ++k)
-                    v[k] = *reinterpret_cast<const uint4*>(p + k * second);
+                    v[k] = load_stream(p + k * second);
             }
             if constexpr (MODE == kUnpack && kScalesIn)
                 if (kDq || sub == 0) sc = *sp;  // every dequantising lane needs the scale
