@@ -445,3 +445,58 @@ def e4m3_sweep_rows(fmt, amaxes, rng):
     special[5, 11] = inf | 0x8000                  # and -Inf: the row maximum is Inf
     out.append(special)
     return np.concatenate(out)
+
+
+# ---- exhaustive 8-bit sweep: every row maximum, every element under it ----
+
+FINITE_MAX = {"bf16": 0x7F7F, "fp16": 0x7BFF}   # largest finite magnitude pattern
+NAN_BITS = {"bf16": 0x7FC0, "fp16": 0x7E00}     # a quiet NaN of each format
+
+
+def pair_rows(fmt, mags, nan=False, block=512, threads=None):
+    """Rows of 128 16-bit patterns such that, for each magnitude pattern m in
+    `mags` (finite, > 0), some rows have row maximum exactly m and together
+    hold every finite pattern x with |x| <= m, in both signs.  Each row holds
+    127 of those patterns (the last row of each m padded with +0) plus m
+    itself at column (row index mod 128), its sign flipping every 128 rows,
+    so the maximum visits every lane of a row.  With nan=True each row holds
+    126 patterns, m and a NaN (sign and payload varying by row) at column
+    (row index + 64) mod 128: rows whose row maximum, and so their scale, is
+    finite but which contain a NaN.  Returns uint16 [rows, 128]."""
+    from concurrent.futures import ThreadPoolExecutor
+    import os
+
+    mags = np.asarray(mags, dtype=np.int64)
+    assert mags.size and mags.min() >= 1 and mags.max() <= FINITE_MAX[fmt]
+    per = 127 - int(nan)                       # patterns per row besides m (and the NaN)
+    k_all = -(-(2 * (mags + 1)) // per)        # rows per maximum
+    first_all = np.cumsum(k_all) - k_all       # first row of each maximum
+    out = np.empty((int(k_all.sum()), 128), dtype=np.uint16)
+    col = np.arange(128, dtype=np.int32)[None, :]
+
+    def fill(b):
+        m_b, k_b = mags[b:b + block], k_all[b:b + block]
+        r0, n = int(first_all[b]), int(k_b.sum())
+        m = np.repeat(m_b, k_b).astype(np.int32)[:, None]      # row maximum of each row
+        i = (np.arange(r0, r0 + n) - np.repeat(first_all[b:b + block], k_b)).astype(np.int32)
+        g = np.arange(r0, r0 + n, dtype=np.int64)              # global row index
+        pos = (g % 128).astype(np.int32)[:, None]
+        npos = (pos + 64) % 128
+        # value index under m of each column (the columns of m and the NaN skipped)
+        v = (i * per)[:, None] + col
+        v -= col > pos
+        if nan:
+            v -= col > npos
+        neg = v > m                                            # second half: the negative patterns
+        v -= np.where(neg, m + 1, 0)
+        v |= np.where(neg, 0x8000, 0)
+        v[v >= 0x8000 + m + 1] = 0                             # padding past -m: +0
+        rows = np.arange(n)
+        v[rows, pos[:, 0]] = m[:, 0] | (((g // 128) & 1) << 15).astype(np.int32)
+        if nan:
+            v[rows, npos[:, 0]] = NAN_BITS[fmt] | (g % 7 + 1) | (((g // 2) & 1) << 15)
+        out[r0:r0 + n] = v
+
+    with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(fill, range(0, mags.size, block)))
+    return out
