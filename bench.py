@@ -53,16 +53,27 @@ def measured_traffic(workload: str):
     return t.get("bytes_per_launch")
 
 
+CONFIG_WORKLOADS = ("tiny_tp1to2_fp16_bf16", "llama3_8b_bf16_bs16", "llama3_70b_tp4to2_bf16_bs32",
+                    "qwen7b_htd_fp16_bf16_bs64", "fp8_decode_61l_bf16_e4m3_bs16")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3_8b_bf16_bs16")
+    ap.add_argument("--configs", default=",".join(CONFIG_WORKLOADS),
+                    help="comma-separated workloads measured one after another after the headline "
+                         "one (repack, pack, unpack, request latency), each freed before the next; "
+                         "'none' = skip")
+    ap.add_argument("--pages", choices=("random", "consecutive"), default="random",
+                    help="destination pages of the decode pool: the workload's seeded random "
+                         "block table, or consecutive pages (a diagnostic of page scatter)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="time the repack only (no pack/unpack/latency legs)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--stream-chunk", type=int, default=4,
                     help="layers per chunk of the layer-streamed transfer leg (0 = skip it)")
     ap.add_argument("--stream-slots", type=int, default=3)
@@ -83,7 +94,6 @@ def main():
               "has no multi-GPU path (run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_2509_17542_amd as K
@@ -93,49 +103,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
-    w = W.WORKLOADS[args.workload]
-    if w.layers != w.total_layers:
-        w = w.replace()   # layer-group workloads time their first group
-    lens = W.seq_lens(w)
-    bt, stride = W.block_table(w, lens)
-    # The decode side's paged pool is allocated first, as a serving engine
-    # reserves it at start-up; the source buffers and transfer tensors of the
-    # requests come after it.
-    esz = 1 if w.cdt in ("e4m3fn", "e5m2") else 2   # the cache's element size
-    n_rows = w.layers * 2 * w.num_blocks * w.block_size * w.hd
-    cache = torch.empty(n_rows * w.head_dim * esz, dtype=torch.uint8, device="cuda")
-    scales = torch.empty(n_rows, dtype=torch.float32, device="cuda") if esz == 1 else None
-    log(f"pool {cache.numel() / 2**30:.1f} GiB allocated")
-    log(f"{w.name}: {len(lens)} requests, {int(lens.sum())} tokens; generating inputs")
-    t0 = time.time()
-    # prefill pipeline stages: each holds a layer range in its own buffers and
-    # gets its own plan; all of them fill the one decode cache
-    stages = W.src_stages(w)
-    stage_shards = [W.source_shards(w, lens, l0, n) for l0, n in stages]
-    log(f"inputs generated in {time.time() - t0:.1f}s; uploading")
-    stage_dshards = [[None if s is None else torch.from_numpy(s.view(np.int16)).cuda() for s in sh]
-                     for sh in stage_shards]
-    bt_d = torch.from_numpy(bt).cuda()
-    F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN, "e5m2": K.E5M2}
-    order = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order]
-    paged = w.src_order == "paged"
-    sbt = sbt_d = None
-    sstride = 0
-    if paged:   # the prefill side's own paged cache and its block table
-        sbt, sstride = W.src_block_table(w, lens)
-        sbt_d = torch.from_numpy(sbt).cuda()
-
-    def desc(seq, stage):
-        l0, n = stage
-        return K.make_desc(n, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
-                           F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks, seq,
-                           w.src_block_size, w.src_num_blocks, 0, n, l0, w.layers,
-                           F[w.cache_dtype] if w.cache_dtype else 0)
-
-    plans = [K.kvx_plan(desc(list(lens), st)) for st in stages]
-    infos = [K.kvx_plan_info_get(p) for p in plans]
     stream = torch.cuda.current_stream()
-    rep_bytes = sum(i.read_bytes_repack + i.write_bytes_repack for i in infos)
 
     def timed(fn, steps, warmup):
         for _ in range(warmup):
@@ -154,38 +122,18 @@ def main():
         kern = [a.elapsed_time(b) for a, b in ev]
         return wall * 1e3, statistics.mean(kern), min(kern), statistics.median(kern)
 
-    # Prefill stages are independent transfers: each stage's launch goes on a
-    # stream of its own (default priority), forked from the timed stream and
-    # joined back into it, so that the stages write their halves of the pool
-    # at the same time.
-    side = [torch.cuda.Stream() for _ in stages[1:]]
-    fork = torch.cuda.Event()
-
-    def per_stage(launch):
-        if side:
-            fork.record(stream)
-            for s in side:
-                s.wait_event(fork)
-        for k, st in enumerate([stream] + side):
-            launch(k, st)
-        for s in side:
-            stream.wait_stream(s)
-
-    def repack():
-        def launch(k, st):
-            if paged:
-                K.kvx_repack_paged(plans[k], stage_dshards[k], sbt_d, sstride, cache, scales, bt_d,
-                                   stride, st)
-            else:
-                K.kvx_repack(plans[k], stage_dshards[k], cache, scales, bt_d, stride, st)
-        per_stage(launch)
+    w = W.WORKLOADS[args.workload]
+    wb = Workbench(K, W, torch, w, stream, all_shards=True,
+                   consecutive=args.pages == "consecutive")
+    rep_bytes = wb.bytes("repack")
 
     log(f"repack: {args.warmup} warm-up + {args.steps} timed steps")
-    ms_step, k_mean, k_min, k_med = timed(repack, args.steps, args.warmup)
+    ms_step, k_mean, k_min, k_med = timed(wb.repack, args.steps, args.warmup)
     value = rep_bytes / (ms_step * 1e-3) / 1e9
     achieved = rep_bytes / (k_mean * 1e-3) / 1e9
     log(f"repack {ms_step:.3f} ms/step, kernel mean {k_mean:.3f} ms -> {achieved:.0f} GB/s")
 
+    stages, paged, lens = wb.stages, wb.paged, wb.lens
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -199,7 +147,9 @@ def main():
                    "src_dtype": w.src_dtype, "dst_dtype": w.dst_dtype,
                    **({"cache_dtype": w.cache_dtype} if w.cache_dtype else {}),
                    "src_order": w.src_order, "block_size": w.block_size,
-                   "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes},
+                   "pool_blocks": w.num_blocks, "bytes_per_step": rep_bytes,
+                   **({"dst_pages": "consecutive (diagnostic)"} if args.pages != "random"
+                      else {})},
         **({"prefill_stages": [list(st) for st in stages], "launches_per_step": len(stages),
             "streams_per_step": len(stages)}
            if len(stages) > 1 else {}),
@@ -218,53 +168,181 @@ def main():
                        "traffic": traffic, "kernel": "kvx_repack_kernel",
                        "algorithmic_bytes_per_launch": rep_bytes}
 
+    headline = {"repack": {"kernel_ms": round(k_mean, 4), "GB/s": round(achieved, 1),
+                           "frac": round(achieved / HBM_PEAK_GBS, 4)}}
     if not args.no_extras:
-        wires = [torch.empty(int(i.wire_bytes), dtype=torch.uint8, device="cuda") for i in infos]
-
-        def pack():
-            def launch(k, st):
-                if paged:
-                    K.kvx_pack_paged(plans[k], stage_dshards[k], sbt_d, sstride, wires[k], st)
-                else:
-                    K.kvx_pack(plans[k], stage_dshards[k], wires[k], st)
-            per_stage(launch)
-
-        def unpack():
-            per_stage(lambda k, st: K.kvx_unpack(plans[k], wires[k], cache, scales, bt_d, stride,
-                                                 st))
-
-        pack_bytes = sum(i.read_bytes_pack + i.write_bytes_pack for i in infos)
-        unpack_bytes = sum(i.read_bytes_unpack + i.write_bytes_unpack for i in infos)
-        for name, fn, nbytes in (("pack", pack, pack_bytes), ("unpack", unpack, unpack_bytes)):
-            ms, km, _, _ = timed(fn, max(5, args.steps // 2), 2)
+        for name in ("pack", "unpack"):
+            ms, km, _, _ = timed(getattr(wb, name), max(5, args.steps // 2), 2)
+            gbs = wb.bytes(name) / (km * 1e-3) / 1e9
             out[name] = {"ms_per_step": round(ms, 4), "kernel_ms": round(km, 4),
-                         "GB/s": round(nbytes / (km * 1e-3) / 1e9, 1)}
+                         "GB/s": round(gbs, 1)}
+            headline[name] = {"kernel_ms": round(km, 4), "GB/s": round(gbs, 1),
+                              "frac": round(gbs / HBM_PEAK_GBS, 4)}
             log(f"{name}: kernel {km:.3f} ms")
-        del wires
+        wb.free_wires()
+        out["latency_ms_per_request"] = wb.latency()
+        out["latency_ms_per_request"]["batch_over_requests"] = round(ms_step / len(lens), 4)
+        headline["latency_ms_per_request"] = out["latency_ms_per_request"]
+        log(f"latency p50 {out['latency_ms_per_request']['p50']} ms")
 
-        # per-request latency: single-request plans (one per prefill stage) per
-        # request, host call to completion; the stages of one request go on the
-        # timed stream one after the other (for launches this small a fork and
-        # join across streams costs more than it overlaps)
+    if not args.no_extras and args.stream_chunk > 0 and len(stages) == 1:
+        out["layer_stream"] = stream_leg(K, torch, wb.plans[0], wb.infos[0], wb.dshards[0],
+                                         wb.sbt_d, wb.sstride, wb.cache, wb.scales, wb.bt_d,
+                                         wb.stride, stream, min(args.stream_chunk, w.layers),
+                                         args.stream_slots, timed)
+
+    if not args.no_extras:
+        out["pd_planner"] = planner_leg(K, w)
+
+    host_shards = wb.host_shards[0]
+    sbt = wb.sbt
+    wb.free()
+    del wb
+    torch.cuda.empty_cache()
+
+    names = [] if args.configs == "none" else [n for n in args.configs.split(",") if n]
+    if names:
+        out["configs"] = configs_leg(K, W, torch, stream, timed, names, w.name, headline,
+                                     args.steps, args.warmup)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, lens, host_shards, args.cpu_seconds, value, sbt,
+                                           stages[0])
+    print(json.dumps(out), flush=True)
+
+
+class Workbench:
+    """One workload resident on the device, ready to launch.  The decode
+    side's paged pool is allocated first, as a serving engine reserves it at
+    start-up; the source buffers of the requests come after it.  Prefill
+    pipeline stages hold a layer range each in their own buffers and get a
+    plan each; all of them fill the one decode cache.  Layer-group workloads
+    hold their first group."""
+
+    def __init__(self, K, W, torch, w, stream, all_shards=False, consecutive=False):
+        import numpy as np
+        self.K, self.torch, self.w, self.stream = K, torch, w, stream
+        lens = self.lens = W.seq_lens(w)
+        self.bt, self.stride = W.block_table(w, lens, consecutive)
+        esz = 1 if w.cdt in ("e4m3fn", "e5m2") else 2   # the cache's element size
+        n_rows = w.layers * 2 * w.num_blocks * w.block_size * w.hd
+        self.cache = torch.empty(n_rows * w.head_dim * esz, dtype=torch.uint8, device="cuda")
+        self.scales = (torch.empty(n_rows, dtype=torch.float32, device="cuda") if esz == 1
+                       else None)
+        log(f"{w.name}: pool {self.cache.numel() / 2**30:.1f} GiB allocated; {len(lens)} "
+            f"requests, {int(lens.sum())} tokens; generating inputs")
+        F = {"fp16": K.FP16, "bf16": K.BF16, "e4m3fn": K.E4M3FN, "e5m2": K.E5M2}
+        order = {"thd": K.THD, "htd": K.HTD, "paged": K.PAGED}[w.src_order]
+        self.paged = w.src_order == "paged"
+        self.stages = W.src_stages(w)
+
+        def desc(seq, stage):
+            l0, n = stage
+            return K.make_desc(n, w.heads, w.head_dim, w.src_tp, w.dst_tp, w.dst_rank,
+                               F[w.src_dtype], F[w.dst_dtype], order, w.block_size, w.num_blocks,
+                               seq, w.src_block_size, w.src_num_blocks, 0, n, l0, w.layers,
+                               F[w.cache_dtype] if w.cache_dtype else 0)
+
+        self.desc = desc
+        self.plans = [K.kvx_plan(desc(list(lens), st)) for st in self.stages]
+        self.infos = [K.kvx_plan_info_get(p) for p in self.plans]
+        read = None if all_shards else \
+            [j for j in range(w.src_tp) if K.kvx_plan_shard_bytes(self.plans[0], j) > 0]
+        t0 = time.time()
+        self.host_shards = [W.source_shards(w, lens, l0, n, read) for l0, n in self.stages]
+        log(f"inputs generated in {time.time() - t0:.1f}s; uploading")
+        self.dshards = [[None if s is None else torch.from_numpy(s.view(np.int16)).cuda()
+                         for s in sh] for sh in self.host_shards]
+        self.bt_d = torch.from_numpy(self.bt).cuda()
+        self.sbt = self.sbt_d = None
+        self.sstride = 0
+        if self.paged:   # the prefill side's own paged cache and its block table
+            self.sbt, self.sstride = W.src_block_table(w, lens)
+            self.sbt_d = torch.from_numpy(self.sbt).cuda()
+        self.wires = None
+        # Prefill stages are independent transfers: each stage's launch goes
+        # on a stream of its own (default priority), forked from the timed
+        # stream and joined back into it, so that the stages write their
+        # halves of the pool at the same time.
+        self.side = [torch.cuda.Stream() for _ in self.stages[1:]]
+        self.fork = torch.cuda.Event()
+
+    def bytes(self, op):
+        return sum(getattr(i, f"read_bytes_{op}") + getattr(i, f"write_bytes_{op}")
+                   for i in self.infos)
+
+    def _per_stage(self, launch):
+        if self.side:
+            self.fork.record(self.stream)
+            for s in self.side:
+                s.wait_event(self.fork)
+        for k, st in enumerate([self.stream] + self.side):
+            launch(k, st)
+        for s in self.side:
+            self.stream.wait_stream(s)
+
+    def repack(self):
+        K = self.K
+
+        def launch(k, st):
+            if self.paged:
+                K.kvx_repack_paged(self.plans[k], self.dshards[k], self.sbt_d, self.sstride,
+                                   self.cache, self.scales, self.bt_d, self.stride, st)
+            else:
+                K.kvx_repack(self.plans[k], self.dshards[k], self.cache, self.scales, self.bt_d,
+                             self.stride, st)
+        self._per_stage(launch)
+
+    def _wires(self):
+        if self.wires is None:
+            self.wires = [self.torch.empty(int(i.wire_bytes), dtype=self.torch.uint8,
+                                           device="cuda") for i in self.infos]
+        return self.wires
+
+    def pack(self):
+        K, wires = self.K, self._wires()
+
+        def launch(k, st):
+            if self.paged:
+                K.kvx_pack_paged(self.plans[k], self.dshards[k], self.sbt_d, self.sstride,
+                                 wires[k], st)
+            else:
+                K.kvx_pack(self.plans[k], self.dshards[k], wires[k], st)
+        self._per_stage(launch)
+
+    def unpack(self):
+        wires = self._wires()
+        self._per_stage(lambda k, st: self.K.kvx_unpack(self.plans[k], wires[k], self.cache,
+                                                        self.scales, self.bt_d, self.stride, st))
+
+    def free_wires(self):
+        self.wires = None
+
+    def latency(self):
+        """Per-request latency: single-request plans (one per prefill stage)
+        per request, host call to completion; the stages of one request go on
+        the timed stream one after the other (for launches this small a fork
+        and join across streams costs more than it overlaps)."""
+        K, w, torch, stream = self.K, self.w, self.torch, self.stream
         lat = []
         src_off = 0
-        for r, T in enumerate(lens.tolist()):
-            p1s = [K.kvx_plan(desc([T], st)) for st in stages]
-            row = bt_d[r:r + 1]
-            if paged:   # the same pools, this request's row of the source block table
-                srow = sbt_d[r:r + 1]
+        for r, T in enumerate(self.lens.tolist()):
+            p1s = [K.kvx_plan(self.desc([T], st)) for st in self.stages]
+            row = self.bt_d[r:r + 1]
+            if self.paged:   # the same pools, this request's row of the source block table
+                srow = self.sbt_d[r:r + 1]
 
                 def one():
-                    for p1, dsh in zip(p1s, stage_dshards):
-                        K.kvx_repack_paged(p1, dsh, srow, sstride, cache, scales, row, stride,
-                                           stream)
+                    for p1, dsh in zip(p1s, self.dshards):
+                        K.kvx_repack_paged(p1, dsh, srow, self.sstride, self.cache, self.scales,
+                                           row, self.stride, stream)
             else:
                 shs = [[None if s is None else s[src_off * n // w.layers:] for s in dsh]
-                       for (_, n), dsh in zip(stages, stage_dshards)]
+                       for (_, n), dsh in zip(self.stages, self.dshards)]
 
                 def one():
                     for p1, sh in zip(p1s, shs):
-                        K.kvx_repack(p1, sh, cache, scales, row, stride, stream)
+                        K.kvx_repack(p1, sh, self.cache, self.scales, row, self.stride, stream)
             src_off += w.layers * 2 * T * w.hs * w.head_dim
             ev = torch.cuda.Event()
             one()   # warm
@@ -277,27 +355,57 @@ def main():
                 ev.synchronize()
                 reps.append((time.perf_counter() - t) * 1e3)
             lat.append(statistics.median(reps))
-        lat_sorted = sorted(lat)
-        out["latency_ms_per_request"] = {
-            "p50": round(statistics.median(lat), 4),
-            "p90": round(lat_sorted[min(len(lat) - 1, int(0.9 * len(lat)))], 4),
-            "max": round(max(lat), 4), "batch_over_requests": round(ms_step / len(lens), 4),
-            "note": "single-request plan, host call to event completion, median of 5"}
-        log(f"latency p50 {out['latency_ms_per_request']['p50']} ms")
+        s = sorted(lat)
+        return {"p50": round(statistics.median(lat), 4),
+                "p90": round(s[min(len(s) - 1, int(0.9 * len(s)))], 4), "max": round(max(lat), 4),
+                "requests": len(lat),
+                "note": "single-request plan, host call to event completion, median of 5"}
 
-    if not args.no_extras and args.stream_chunk > 0 and len(stages) == 1:
-        out["layer_stream"] = stream_leg(K, torch, plans[0], infos[0], stage_dshards[0], sbt_d,
-                                         sstride, cache, scales, bt_d, stride, stream,
-                                         min(args.stream_chunk, w.layers), args.stream_slots,
-                                         timed)
+    def free(self):
+        self.cache = self.scales = self.dshards = self.bt_d = self.sbt_d = self.wires = None
+        self.plans = self.side = None
 
-    if not args.no_extras:
-        out["pd_planner"] = planner_leg(K, w)
 
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, lens, stage_shards[0], args.cpu_seconds, value, sbt,
-                                           stages[0])
-    print(json.dumps(out), flush=True)
+def configs_leg(K, W, torch, stream, timed, names, headline_name, headline, steps, warmup):
+    """Each named workload measured after the headline one: repack, pack and
+    unpack kernel time (HIP events, mean of the timed launches), GB/s over the
+    algorithmic bytes, the fraction of the 8 TB/s HBM peak and per-request
+    latency.  Each workload's buffers are freed before the next is
+    allocated.  The headline workload's own figures are copied, not
+    re-measured.  The 8-bit decode workload runs as 4-layer groups (its
+    2^20-page pool over 61 layers does not fit in HBM); it reports its first
+    group."""
+    res = {}
+    for name in names:
+        w = W.WORKLOADS[name]
+        entry = {"layers": w.layers, "requests": w.num_requests, "src_tp": w.src_tp,
+                 "dst_tp": w.dst_tp, "dtype": f"{w.src_dtype}->{w.cdt}", "order": w.src_order,
+                 "block_size": w.block_size, "pool_blocks": w.num_blocks}
+        if w.layers != w.total_layers:
+            entry["layer_group"] = (f"first {w.layers}-layer group of {w.total_layers} layers "
+                                    f"({w.layer_groups} groups)")
+        if name == headline_name:
+            res[name] = {**entry, **headline, "measured": "headline run"}
+            continue
+        wb = Workbench(K, W, torch, w, stream)
+        entry["tokens"] = int(wb.lens.sum())
+        for op in ("repack", "pack", "unpack"):
+            n = steps if op == "repack" else max(5, steps // 2)
+            _, km, kmin, _ = timed(getattr(wb, op), n, warmup)
+            nbytes = wb.bytes(op)
+            gbs = nbytes / (km * 1e-3) / 1e9
+            entry[op] = {"bytes_per_launch": nbytes, "kernel_ms": round(km, 4),
+                         "kernel_ms_min": round(kmin, 4), "GB/s": round(gbs, 1),
+                         "frac": round(gbs / HBM_PEAK_GBS, 4)}
+            log(f"config {name}: {op} {km:.3f} ms -> {gbs:.0f} GB/s")
+        wb.free_wires()
+        entry["latency_ms_per_request"] = wb.latency()
+        log(f"config {name}: latency p50 {entry['latency_ms_per_request']['p50']} ms")
+        wb.free()
+        del wb
+        torch.cuda.empty_cache()
+        res[name] = entry
+    return res
 
 
 def planner_leg(K, w):
@@ -454,16 +562,38 @@ def derive_traffic(fetch_csv, write_csv, workload, calib_gib):
     print(json.dumps(rec))
 
 
+CPU_THREAD_CAP = 16   # the host CPU share of a one-GPU job on the MI355X boxes
+
+
+def host_cpu():
+    """nproc, the cores this process may run on, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = os.cpu_count() or 1
+    return {"nproc": os.cpu_count(), "cores_allowed": allowed, "model": model}
+
+
 def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
     """The oracle as it stands, on whole requests of the same workload, decode
     pages renumbered into a compact host pool (same rows, same bytes); a paged
     source is read in place through the request's row of the source block
     table; with prefill stages, the first stage's layers.  Two runs: one
-    thread until about budget_s seconds of CPU work, then the independent
-    requests spread over the host's cores (at most 16 threads; the C oracle
-    releases the GIL) until about budget_s seconds of wall time.  `value` is
-    the multi-threaded rate."""
-    import os
+    thread over the requests one by one (each a single-request problem, so
+    its time is the oracle's per-request latency) until all are done or
+    about budget_s seconds of CPU work; then the independent requests spread
+    over the host's cores (at most CPU_THREAD_CAP threads; the C oracle
+    releases the GIL) until all are done or about budget_s seconds of wall
+    time.  `value` is the multi-threaded rate, `cores` the threads it used."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -504,18 +634,21 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
         rows = L * 2 * T * w.hd
         return rows * w.head_dim * (2 + esz) + (rows * 4 if esz == 1 else 0), T, dt
 
-    # one thread
+    host = host_cpu()
+    # one thread: every request in turn, each timed alone
     done = spent = 0.0
     n1 = tok1 = 0
+    per_req = []
     while n1 < len(lens) and spent < budget_s:
         b, T, dt = one(n1)
         done, spent, n1, tok1 = done + b, spent + dt, n1 + 1, tok1 + T
+        per_req.append(dt * 1e3)
     gbs1 = done / spent / 1e9 if spent > 0 else None
     log(f"cpu oracle, 1 thread: {n1} requests, {done / 1e9:.2f} GB in {spent:.1f}s -> "
         f"{gbs1:.3f} GB/s")
 
     # independent requests on the host's cores
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = max(1, min(CPU_THREAD_CAP, host["cores_allowed"]))
     done = 0.0
     n = tok = 0
     t0 = time.perf_counter()
@@ -529,14 +662,23 @@ def cpu_baseline(w, lens, shards, budget_s, gpu_value, sbt=None, stage=None):
     gbs = done / wall / 1e9 if wall > 0 else None
     log(f"cpu oracle, {threads} threads: {n} requests, {done / 1e9:.2f} GB in {wall:.1f}s -> "
         f"{gbs:.3f} GB/s")
+    s = sorted(per_req)
     return {"value": round(gbs, 4) if gbs else None, "unit": "GB/s", "cores": threads,
             "kind": "oracle",
             "sample": f"first {n} of {len(lens)} requests ({tok} tokens, {done / 1e9:.2f} GB read+"
                       f"written) of {w.name}, plain-C oracle, one request per thread on "
                       f"{threads} threads, pages renumbered into a compact host pool",
+            "host": {**host, "threads_used": threads,
+                     "thread_cap": f"{CPU_THREAD_CAP}: the host CPU share of a one-GPU job on "
+                                   "this machine, whatever nproc reports"},
             "seconds": round(wall, 2),
             "single_thread": {"value": round(gbs1, 4) if gbs1 else None, "requests": n1,
                               "tokens": tok1, "seconds": round(spent, 2)},
+            "latency_ms_per_request": {
+                "p50": round(statistics.median(per_req), 3) if per_req else None,
+                "p90": round(s[min(len(s) - 1, int(0.9 * len(s)))], 3) if s else None,
+                "max": round(max(per_req), 3) if per_req else None, "requests": len(per_req),
+                "note": "one thread, single-request problem, oracle call time"},
             "gpu_over_cpu": round(gpu_value / gbs, 1) if gbs else None}
 
 

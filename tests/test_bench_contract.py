@@ -29,7 +29,7 @@ def test_bench_refuses_more_than_one_gpu():
 def test_bench_prints_one_json_line():
     r = subprocess.run([sys.executable, BENCH, "--workload", "tiny_tp1to2_fp16_bf16", "--steps", "3",
                         "--warmup", "1", "--stream-chunk", "0", "--calib-gib", "0.25",
-                        "--cpu-seconds", "0.5"],
+                        "--cpu-seconds", "0.5", "--configs", "tiny_tp1to2_fp16_bf16"],
                        capture_output=True, text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
@@ -54,5 +54,9 @@ def test_bench_prints_one_json_line():
     cpu = out["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["unit"] == "GB/s"
     assert cpu["value"] > 0 and cpu["cores"] >= 1 and cpu["sample"]
+    assert cpu["host"]["nproc"] >= 1 and cpu["host"]["threads_used"] == cpu["cores"]
+    assert cpu["latency_ms_per_request"]["p50"] > 0
+    cfg_leg = out["configs"]["tiny_tp1to2_fp16_bf16"]
+    assert cfg_leg["repack"]["GB/s"] > 0 and cfg_leg["latency_ms_per_request"]["p50"] > 0
     assert out["latency_ms_per_request"]["p50"] > 0
     assert out["pack"]["GB/s"] > 0 and out["unpack"]["GB/s"] > 0

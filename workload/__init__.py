@@ -223,15 +223,18 @@ def permutation(seed: int, n: int, stream: int = S_TABLE) -> np.ndarray:
     return out
 
 
-def block_table(w: Workload, lens: np.ndarray) -> tuple[np.ndarray, int]:
+def block_table(w: Workload, lens: np.ndarray, consecutive: bool = False) -> tuple[np.ndarray, int]:
     """Pages for each request, drawn in order from a seeded permutation of the
-    pool.  Returns ([R, stride] int32 with -1 in unused entries, stride)."""
+    pool (or, with consecutive=True, pages 0, 1, 2, ... in request order: the
+    same page counts with no scatter).  Returns ([R, stride] int32 with -1 in
+    unused entries, stride)."""
     nblk = [(int(t) + w.block_size - 1) // w.block_size for t in lens]
     stride = max(nblk + [1])
     need = sum(nblk)
     if need > w.num_blocks:
         raise ValueError(f"{w.name}: {need} pages needed, pool has {w.num_blocks}")
-    perm = permutation(w.seed, w.num_blocks)
+    perm = np.arange(w.num_blocks, dtype=np.int64) if consecutive else \
+        permutation(w.seed, w.num_blocks)
     bt = np.full((len(lens), stride), -1, dtype=np.int32)
     pos = 0
     for r, n in enumerate(nblk):
