@@ -6,6 +6,10 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
+# The mutation test runs the oracle's pins against a modified copy of the
+# oracle package: the directory holding that copy goes first on the path.
+if os.environ.get("KVX_ORACLE_COPY"):
+    sys.path.insert(0, os.environ["KVX_ORACLE_COPY"])
 
 GOLDEN = os.path.join(ROOT, "tests", "golden")
 

@@ -50,6 +50,15 @@ def test_dequant_fp16_overflow_and_subnormals():
     assert got[2] == 0x0000                               # 2^-25: tie to even, 0
     assert got[3] == 0x0004                               # 2^-22 = 4 units of 2^-24
     assert got[4] == 0x0100                               # 2^-16 = 256 units
+    # the edge of the fp16 range: the fp32 product 448 * 146.2 (about 65497.6)
+    # lies between the fp16 points 65472 and 65504 (spacing 32 in [2^15,
+    # 2^16)), nearer 65504 = 0x7BFF, so it stays finite; 448 * 146.25 = 65520
+    # is the midpoint of 65504 (odd significand) and 65536 (even, past the
+    # largest finite value), so it rounds to infinity
+    got = O.dequant_row(O.FP16, codes[:2], np.float32(146.2))
+    assert list(got) == [0x7BFF, 0xFBFF]
+    got = O.dequant_row(O.FP16, codes[:2], np.float32(146.25))
+    assert list(got) == [0x7C00, 0xFC00]
 
 
 @pytest.mark.parametrize("name", list(SMALL_DEQUANT))

@@ -1,6 +1,6 @@
 """Pins of the oracle's layer ranges (pipeline-parallel stages on either side:
 the prefill side's pipeline stages each hold a range of layers, Sec. III-B-3
-and the strategy search of Sec. IV; here the decode side may be staged
+and the strategy search of Sec. III-C; here the decode side may be staged
 differently).  A plan converts layers that lie in one source stage and one
 decode stage; the pins reduce a set of stage plans to the whole-model
 conversion, which the layout pins already fix."""

@@ -324,3 +324,21 @@ def test_bf16_to_fp16_case_overflows_and_keeps_the_rest():
 def test_validate_rejects_negative_length():
     p = O.OracleProblem(1, 4, 64, 1, 1, 0, O.BF16, O.BF16, O.TOKEN_MAJOR, 16, 8, [3, -1])
     assert O.validate(p) == -1
+
+
+def test_wire_layout_hand_worked():
+    """Segment offsets of the transfer tensor against hand-worked values
+    (tests/golden/wire_layout.txt)."""
+    f = {"bf16": O.BF16, "fp16": O.FP16, "e4m3fn": O.E4M3FN, "e5m2": O.E5M2}
+    rows = golden_lines("wire_layout.txt")
+    assert len(rows) == 3
+    for ln in rows:
+        head, toks, doffs, soffs, total = (part.split() for part in ln.split("|"))
+        fmt = f[head[0]]
+        L, H, ts, td, rank, D = map(int, head[1:])
+        lens = [int(t) for t in toks]
+        p = O.OracleProblem(L, H, D, ts, td, rank, O.BF16, fmt, O.TOKEN_MAJOR, 16, 64, lens)
+        d, s, n = O.wire_layout(p)
+        assert list(d) == [int(x) for x in doffs], ln
+        assert list(s) == [int(x) for x in soffs], ln
+        assert n == int(total[0]), ln

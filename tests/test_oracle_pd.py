@@ -155,3 +155,39 @@ def test_tensor_parallel_degrees_follow_the_head_map():
     assert tps == {1, 2, 4, 8, 16, 32, 64}
     tps = {c[1] for c in P.candidates(P.Model(28, 3584, 28, 4, 128, 18944, 152064), 8, 1)}
     assert tps == {1, 2, 4}           # 28 query heads: 8 does not divide them
+
+
+def test_instance_counts_hand_worked():
+    """R30 on the tiny model with one candidate per side (1 GPU, batch 1):
+    prefill T_p = 1 / 14.912 requests/s (first row of pd_costs.txt); decode
+    at batch 1 reads the 2528 weight bytes of that file plus the KV of a
+    4-token context (4 x 2 x 2 layers x 1 head x 4 dims x 2 B = 128 B), so
+    l_d = 2656 / 500 = 5.312 s and T_d = 1 / 5.312 tokens/s.  At 0.5
+    requests/s of 2 output tokens: X = ceil(0.5 x 14.912) = ceil(7.456) = 8
+    prefill and Y = ceil(0.5 x 2 x 5.312) = ceil(5.312) = 6 decode
+    instances."""
+    g = P.Gpu(1000.0, 1000.0, 1e9, 100.0, 0.5, 0.5, 0.5, max_gpus=1)
+    p = _tiny_problem(prefill=g, decode=g, qps=0.5, max_batch=1)
+    sol = P.search(p)
+    assert sol.decode.latency == pytest.approx(5.312, rel=1e-12)
+    assert (sol.prefill_instances, sol.decode_instances) == (8, 6)
+
+
+def test_tie_goes_to_fewest_gpus():
+    """R31's tie rule on a case where it decides.  With an unlimited
+    interconnect every prefill strategy's compute splits exactly, so the
+    per-GPU objective b / (l_p tp) is the same for all of them; 280 kB of
+    VRAM leaves out tp = 1 with pp = 1 or 2 (weights and one layer's
+    activations do not fit) and admits tp = 2 with pp = 1 and tp = 1 with
+    pp = 4.  Among equal objectives the fewest GPUs win: tp 2, pp 1 (2 GPUs)
+    over tp 1, pp 4 (4 GPUs), although the latter has the smaller tp."""
+    m = P.Model(4, 64, 4, 1, 16, 16, 100)
+    g = P.Gpu(1e9, 1e9, 280000.0, 1e30, max_gpus=4)
+    p = P.Problem(m, g, g, 256, 2, 1.0, 1e9, 1e9, max_batch=1)
+    assert P.prefill_cost(p, 1, 1, 1, 1, 1)[1] > g.vram
+    assert P.prefill_cost(p, 1, 1, 2, 1, 1)[1] > g.vram
+    a, b = P.prefill_cost(p, 1, 2, 1, 1, 1), P.prefill_cost(p, 1, 1, 4, 1, 1)
+    assert a[1] <= g.vram and b[1] <= g.vram
+    assert a[2] / 2 == pytest.approx(b[2] / 4, rel=1e-12)
+    ch = P.search(p).prefill
+    assert (ch.dp, ch.tp, ch.pp, ch.gpus) == (1, 2, 1, 2)

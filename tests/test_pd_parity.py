@@ -3,7 +3,7 @@ code in the C ABI) against the oracle (oracle/pd.py), on the CPU: chosen
 strategies and instance counts equal, cost terms within 1e-12 relative
 (both evaluate the same closed forms in float64, in different orders), over
 the paper's experimental pairing (Llama2-7B, prefill on GPU B, decode on
-GPU A, Sec. V), dense and MoE models on MI355X, and 200 seeded random
+GPU A, Sec. IV), dense and MoE models on MI355X, and 200 seeded random
 problems that cross the constraints' boundaries."""
 import numpy as np
 import pytest
@@ -48,7 +48,7 @@ def check(p: P.Problem):
     return got
 
 
-# Sec. V: GPU A (80 GB, 312 TFLOP/s) runs decode, GPU B (32 GB, 512 TFLOP/s)
+# Sec. IV: GPU A (80 GB, 312 TFLOP/s) runs decode, GPU B (32 GB, 512 TFLOP/s)
 # prefill.  The paper gives no memory or link rates: 2.0 TB/s and 1.6 TB/s of
 # HBM and 300 GB/s of interconnect are assumed here.
 GPU_A = P.Gpu(312e12, 2.0e12, 80e9, 300e9, 0.5, 0.8, 0.7, 8)
