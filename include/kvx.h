@@ -76,7 +76,7 @@
 extern "C" {
 #endif
 
-#define KVX_ABI_VERSION 8
+#define KVX_ABI_VERSION 9
 
 typedef enum {
     KVX_OK = 0,
@@ -270,6 +270,27 @@ kvx_status kvx_repack_paged(const kvx_plan_t *plan, const void *const *src_shard
                             const int32_t *src_block_table, int32_t src_bt_stride, void *cache,
                             float *scales, const int32_t *block_table, int32_t bt_stride,
                             void *hip_stream);
+
+/* Repack without any allocation, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The same conversion as kvx_plan + kvx_repack of *desc
+ * (token- or head-major sources), with no plan: the work-item table that
+ * kvx_plan would allocate lives in a static device array of the library (one
+ * per device, 65536 entries of 40 bytes), written by a small kernel on
+ * hip_stream before the repack kernel.  Nothing is allocated on the host
+ * heap or the device; the call enqueues two kernels and returns.
+ *   desc:        as kvx_plan (copied; seq_lens read during the call only);
+ *                at most 256 requests and 65536 destination pages in all
+ *                (sum of ceil(T_r / block_size)), else KVX_EUNSUPPORTED.
+ *   other arguments: as kvx_repack.
+ * Calls on one device share its table: calls that overlap on one device (two
+ * streams, or two threads) race and must be ordered by the caller.  Errors:
+ * those of kvx_plan and kvx_repack; KVX_EINVAL for a KVX_PAGED source;
+ * KVX_EDEVICE when the table's device address cannot be found or a launch
+ * fails. */
+kvx_status kvx_repack_noalloc(const kvx_desc *desc, const void *const *src_shards, void *cache,
+                              float *scales, const int32_t *block_table, int32_t bt_stride,
+                              void *hip_stream);
 
 /* Host-side check of a block table: every used entry in [0, num_blocks) and no
  * page used twice.  KVX_EINVAL (with a message) otherwise. */

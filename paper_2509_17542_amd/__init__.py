@@ -25,7 +25,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 # the struct layouts below are those of this version of include/kvx.h
-ABI_VERSION = 8
+ABI_VERSION = 9
 if _lib.kvx_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} implements kvx ABI {_lib.kvx_abi_version()}, this binding "
                       f"ABI {ABI_VERSION}: rebuild the library")
@@ -145,6 +145,8 @@ _lib.kvx_pack_paged.restype = ctypes.c_int
 _lib.kvx_pack_paged.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp]
 _lib.kvx_repack_paged.restype = ctypes.c_int
 _lib.kvx_repack_paged.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp]
+_lib.kvx_repack_noalloc.restype = ctypes.c_int
+_lib.kvx_repack_noalloc.argtypes = [ctypes.POINTER(kvx_desc), _vp, _vp, _vp, _vp, _i32, _vp]
 _lib.kvx_check_block_table.restype = ctypes.c_int
 _lib.kvx_check_block_table.argtypes = [_vp, _vp, _i32]
 _lib.kvx_check_src_block_table.restype = ctypes.c_int
@@ -169,7 +171,7 @@ _lib.kvx_pd_evaluate.argtypes = [ctypes.POINTER(kvx_pd_problem)] + [_i32] * 6 + 
 
 EXPORTS = ("kvx_plan", "kvx_plan_info_get", "kvx_plan_segment", "kvx_plan_buffer_sizes",
            "kvx_plan_shard_bytes", "kvx_plan_destroy", "kvx_pack",
-           "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged",
+           "kvx_unpack", "kvx_repack", "kvx_pack_paged", "kvx_repack_paged", "kvx_repack_noalloc",
            "kvx_check_block_table", "kvx_check_src_block_table", "kvx_pipe_create",
            "kvx_pipe_info_get", "kvx_pipe_run", "kvx_pipe_destroy", "kvx_last_error",
            "kvx_abi_version", "kvx_pd_search", "kvx_pd_evaluate")
@@ -365,6 +367,35 @@ def kvx_repack(plan: Plan, src_shards, cache, scales, block_table, bt_stride: in
     _need_pool(plan, cache, scales, block_table, bt_stride)
     _check(_lib.kvx_repack(plan, _shard_array(plan, src_shards), _addr(cache), _addr(scales),
                            _addr(block_table), bt_stride, _stream(stream)))
+
+
+def kvx_repack_noalloc(desc: kvx_desc, src_shards, cache, scales, block_table, bt_stride: int,
+                       stream=None) -> None:
+    """kvx_repack of `desc` with no plan and no allocation (the C call keeps
+    its work-item table in a static device array).  Tensor arguments are
+    checked against the sizes the descriptor implies: every shard given must
+    hold one shard's bytes, whether the decode rank reads it or not."""
+    lens = [desc.seq_lens[r] for r in range(desc.num_requests)]
+    if sum(lens) > 0:
+        H, D = desc.num_kv_heads, desc.head_dim
+        hs = H // desc.src_tp if 0 < desc.src_tp <= H else 1
+        hd = H // desc.dst_tp if 0 < desc.dst_tp <= H else 1
+        cdt = desc.cache_dtype or desc.dst_dtype
+        esz = 1 if cdt in (E4M3FN, E5M2) else 2
+        src_layers = desc.src_layers or desc.num_layers
+        dst_layers = desc.dst_layers or desc.num_layers
+        slots = 2 * dst_layers * desc.num_blocks * desc.block_size * hd
+        _need(cache, slots * D * esz, "cache")
+        _need(scales, slots * 4 if esz == 1 else 0, "scales", torch.float32)
+        _need(block_table, 4 * desc.num_requests * max(int(bt_stride), 0), "block_table",
+              torch.int32)
+        for j, sh in enumerate(src_shards):
+            _need(sh, 2 * src_layers * sum(lens) * hs * D * 2, f"src_shards[{j}]")
+    arr = (_vp * max(len(src_shards), 1))()
+    for j, sh in enumerate(src_shards):
+        arr[j] = _addr(sh)
+    _check(_lib.kvx_repack_noalloc(ctypes.byref(desc), arr, _addr(cache), _addr(scales),
+                                   _addr(block_table), bt_stride, _stream(stream)))
 
 
 def kvx_pack_paged(plan: Plan, src_shards, src_block_table, src_bt_stride: int, wire,

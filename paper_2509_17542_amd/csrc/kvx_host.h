@@ -9,8 +9,30 @@
 #include "kvx.h"
 #include "kvx_internal.h"
 
+namespace kvx {
+
+// What a problem descriptor fixes about the launches, independent of the
+// requests' lengths: heads per rank, element sizes, the conversion, the head
+// segments and the lanes and passes per row.  Fixed-size, so that it can be
+// derived without allocating.
+struct Shape {
+    int hs = 0, hd = 0, esz_src = 0, esz_dst = 0, conv = 0;
+    int cache_dtype = 0, esz_cache = 0;  // the cache's element type (dst_dtype unless dequantising)
+    bool dequant = false;                // 8-bit transfer tensor, 16-bit cache
+    // lanes per row (from the transfer-tensor row; a dequantising lane covers
+    // two 16-byte cache chunks) and workgroup passes per (page, segment)
+    int cpr = 0, lg_lpr = 0, parts = 0, parts_unpack = 0;
+    int nsegs = 0;                       // head segments of the decode rank
+    Segment segs[kMaxReadShards];
+    int nread = 0;                       // prefill shards the decode rank reads, in slot order
+    int read_shards[kMaxReadShards];
+};
+
+}  // namespace kvx
+
 struct kvx_plan_s {
     kvx_desc d;                   // seq_lens points into lens
+    kvx::Shape sh;                // the launches' shape (the fields below repeat it)
     std::vector<int32_t> lens;
     std::vector<int64_t> wire_data, wire_scale;  // per request, transfer-tensor offsets
     std::vector<kvx::Item> items;
@@ -34,6 +56,10 @@ struct kvx_plan_s {
 };
 
 namespace kvx {
+
+// The shape of a validated descriptor; KVX_EUNSUPPORTED when the decode rank
+// needs more than kMaxReadShards head segments.
+kvx_status derive_shape(const kvx_desc& d, Shape& s);
 
 // Sets the calling thread's last-error message; returns s.
 kvx_status fail(kvx_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));

@@ -119,6 +119,30 @@ struct KArgs {
 // Launch one conversion over a.units work units; returns a hipError_t value.
 int launch(int mode, int conv, int order, const KArgs& a, void* stream);
 
+// The allocation-free repack keeps its work-item table in a static device
+// array of kNoAllocItems entries (40 B each: 2.5 MiB per device) and takes at
+// most kNoAllocRequests requests, whose lengths travel in the arguments of the
+// kernel that writes that table.
+constexpr int kNoAllocItems = 65536;
+constexpr int kNoAllocRequests = 256;
+
+struct ItemsArgs {
+    int32_t lens[kNoAllocRequests];   // tokens per request
+    int32_t num_requests;
+    int32_t block_size;               // destination page size
+    int64_t src_elems_per_token;      // elements of one token in a source shard (2 x layers x Hs x D)
+    Item* items;                      // the table to write
+};
+
+// The current device's static work-item table; the address is looked up once
+// per device.  Returns a hipError_t value.
+int scratch_items(Item** out);
+
+// Enqueue the kernel that writes the work-item table of a.lens (one page of
+// a request per item, requests in order) on `stream`.  Returns a hipError_t
+// value.
+int build_items(const ItemsArgs& a, void* stream);
+
 FastDiv make_fastdiv(uint32_t d);
 
 }  // namespace kvx

@@ -42,6 +42,8 @@
 // [token][head] <-> [head][token] reorder is a change of row addresses only.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "kvx_internal.h"
 
 namespace kvx {
@@ -778,7 +780,82 @@ int go_conv(int conv, const KArgs& a, void* stream)
     return int(hipErrorInvalidValue);
 }
 
+// ---- the work-item table of the allocation-free repack ---------------------
+
+// One workgroup: prefix sums of the pages and tokens of the requests (one
+// thread, at most kNoAllocRequests terms), then every thread writes items
+// idx = tid, tid + 256, ...: the request whose pages cover idx is the last one
+// whose first page is <= idx (requests without pages share their first page
+// with the next request and are skipped by that rule).  The source offset of a
+// request is its preceding tokens times the elements of one token.
+__global__ void __launch_bounds__(kThreads) kvx_items_kernel(const ItemsArgs a)
+{
+    __shared__ int32_t first[kNoAllocRequests + 1];
+    __shared__ int64_t before[kNoAllocRequests + 1];
+    const int R = a.num_requests;
+    if (threadIdx.x == 0) {
+        first[0] = 0;
+        before[0] = 0;
+        for (int r = 0; r < R; ++r) {
+            first[r + 1] = first[r] + (a.lens[r] + a.block_size - 1) / a.block_size;
+            before[r + 1] = before[r] + a.lens[r];
+        }
+    }
+    __syncthreads();
+    const int n = first[R];
+    for (int idx = threadIdx.x; idx < n; idx += kThreads) {
+        int lo = 0, hi = R - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) / 2;
+            if (first[mid] <= idx) lo = mid;
+            else hi = mid - 1;
+        }
+        Item it;
+        it.src_base = before[lo] * a.src_elems_per_token;
+        it.wire_data = 0;
+        it.wire_scale = -1;
+        it.req = lo;
+        it.blk = idx - first[lo];
+        it.tokens = a.lens[lo];
+        it.pad = 0;
+        a.items[idx] = it;
+    }
+}
+
 }  // namespace
+
+// Per device, for the calls that cannot allocate: their work-item table.
+// Every call on a device rewrites it, so calls that overlap on one device
+// race.  Host code never uses this name as an address: scratch_items() looks
+// the device address up.
+static __device__ __align__(256) Item scratch[kNoAllocItems];
+
+int scratch_items(Item** out)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static Item* table[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return int(e);
+    if (dev < 0 || dev >= kMaxDevices) return int(hipErrorInvalidDevice);
+    std::lock_guard<std::mutex> lock(mu);
+    if (!table[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return int(e);
+        table[dev] = static_cast<Item*>(p);
+    }
+    *out = table[dev];
+    return int(hipSuccess);
+}
+
+int build_items(const ItemsArgs& a, void* stream)
+{
+    void* args[] = {const_cast<ItemsArgs*>(&a)};
+    return int(hipLaunchKernel(reinterpret_cast<const void*>(&kvx_items_kernel), dim3(1),
+                               dim3(kThreads), args, 0, static_cast<hipStream_t>(stream)));
+}
 
 int launch(int mode, int conv, int order, const KArgs& a, void* stream)
 {

@@ -184,44 +184,26 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     p->d = d;
     p->lens.assign(d.seq_lens, d.seq_lens + d.num_requests);
     p->d.seq_lens = p->lens.data();
-    p->hs = heads_per_rank(d.num_kv_heads, d.src_tp);
-    p->hd = heads_per_rank(d.num_kv_heads, d.dst_tp);
-    p->esz_src = dtype_size(d.src_dtype);
-    p->esz_dst = dtype_size(d.dst_dtype);
-    p->conv = pick_conv(d.src_dtype, d.dst_dtype);
-    p->cache_dtype = cache_dtype_of(d);
-    p->esz_cache = dtype_size(p->cache_dtype);
-    p->dequant = p->cache_dtype != d.dst_dtype;
-
-    // parallel-strategy alignment: decode head i -> global head g -> (shard j,
-    // head h within it); runs of decode heads with the same shard and
-    // consecutive h form one head segment
-    const int H = d.num_kv_heads;
-    for (int i = 0; i < p->hd; ++i) {
-        const int g = d.dst_tp <= H ? d.dst_rank * p->hd + i : d.dst_rank / (d.dst_tp / H);
-        const int j = d.src_tp <= H ? g / p->hs : g * (d.src_tp / H);  // first replica
-        const int h = d.src_tp <= H ? g % p->hs : 0;
-        int slot = 0;
-        while (slot < int(p->read_shards.size()) && p->read_shards[slot] != j) ++slot;
-        if (slot == int(p->read_shards.size())) p->read_shards.push_back(j);
-        kvx::Segment* last = p->segs.empty() ? nullptr : &p->segs.back();
-        if (last && last->slot == slot && last->h0 + last->n == h && last->i0 + last->n == i) {
-            ++last->n;
-        } else {
-            if (int(p->segs.size()) == kvx::kMaxReadShards) {
-                delete p;
-                return fail(KVX_EUNSUPPORTED, "decode rank needs more than %d head segments",
-                            kvx::kMaxReadShards);
-            }
-            p->segs.push_back(kvx::Segment{slot, h, i, 1, {0, 0}});
-        }
+    st = kvx::derive_shape(d, p->sh);
+    if (st != KVX_OK) {
+        delete p;
+        return st;
     }
-    for (kvx::Segment& g : p->segs) g.div_n = kvx::make_fastdiv(uint32_t(g.n));
-
-    // lanes per row: the smallest power of two covering the transfer-tensor
-    // row's 16-byte chunks (a dequantising lane writes two cache chunks)
-    p->cpr = d.head_dim * p->esz_dst / 16;
-    while ((1 << p->lg_lpr) < p->cpr) ++p->lg_lpr;
+    const kvx::Shape& sh = p->sh;
+    p->hs = sh.hs;
+    p->hd = sh.hd;
+    p->esz_src = sh.esz_src;
+    p->esz_dst = sh.esz_dst;
+    p->conv = sh.conv;
+    p->cache_dtype = sh.cache_dtype;
+    p->esz_cache = sh.esz_cache;
+    p->dequant = sh.dequant;
+    p->segs.assign(sh.segs, sh.segs + sh.nsegs);
+    p->read_shards.assign(sh.read_shards, sh.read_shards + sh.nread);
+    p->cpr = sh.cpr;
+    p->lg_lpr = sh.lg_lpr;
+    p->parts = sh.parts;
+    p->parts_unpack = sh.parts_unpack;
 
     // requests: source offsets, transfer-tensor segments, work items
     const bool fp8 = is_fp8(d.dst_dtype);  // the transfer tensor carries scales
@@ -259,11 +241,6 @@ kvx_status kvx_plan(const kvx_desc* desc, kvx_plan_t** out)
     p->src_elems = paged ? 2 * int64_t(src_layers_of(d)) * d.src_num_blocks * d.src_block_size *
                                p->hs * d.head_dim
                          : src_off;
-    const int64_t rpp = kvx::kThreads >> p->lg_lpr;  // rows per workgroup pass
-    int max_n = 0;
-    for (const kvx::Segment& g : p->segs) max_n = std::max(max_n, g.n);
-    p->parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
-    p->parts_unpack = int32_t((int64_t(d.block_size) * p->hd + rpp - 1) / rpp);
     if (nitems * L2 * std::max<int64_t>(int64_t(p->parts) * int64_t(p->segs.size()),
                                         p->parts_unpack) > kvx::kMaxUnits) {
         delete p;
@@ -429,6 +406,53 @@ kvx::FastDiv kvx::make_fastdiv(uint32_t d)
     return FastDiv{uint32_t(mul), shift};
 }
 
+kvx_status kvx::derive_shape(const kvx_desc& d, Shape& s)
+{
+    s = Shape();
+    s.hs = heads_per_rank(d.num_kv_heads, d.src_tp);
+    s.hd = heads_per_rank(d.num_kv_heads, d.dst_tp);
+    s.esz_src = dtype_size(d.src_dtype);
+    s.esz_dst = dtype_size(d.dst_dtype);
+    s.conv = pick_conv(d.src_dtype, d.dst_dtype);
+    s.cache_dtype = cache_dtype_of(d);
+    s.esz_cache = dtype_size(s.cache_dtype);
+    s.dequant = s.cache_dtype != d.dst_dtype;
+
+    // parallel-strategy alignment: decode head i -> global head g -> (shard j,
+    // head h within it); runs of decode heads with the same shard and
+    // consecutive h form one head segment
+    const int H = d.num_kv_heads;
+    for (int i = 0; i < s.hd; ++i) {
+        const int g = d.dst_tp <= H ? d.dst_rank * s.hd + i : d.dst_rank / (d.dst_tp / H);
+        const int j = d.src_tp <= H ? g / s.hs : g * (d.src_tp / H);  // first replica
+        const int h = d.src_tp <= H ? g % s.hs : 0;
+        int slot = 0;
+        while (slot < s.nread && s.read_shards[slot] != j) ++slot;
+        Segment* last = s.nsegs ? &s.segs[s.nsegs - 1] : nullptr;
+        if (last && last->slot == slot && last->h0 + last->n == h && last->i0 + last->n == i) {
+            ++last->n;
+            continue;
+        }
+        if (s.nsegs == kMaxReadShards)  // a new shard also starts a new segment: nread <= nsegs
+            return fail(KVX_EUNSUPPORTED, "decode rank needs more than %d head segments",
+                        kMaxReadShards);
+        if (slot == s.nread) s.read_shards[s.nread++] = j;
+        s.segs[s.nsegs++] = Segment{slot, h, i, 1, {0, 0}};
+    }
+    for (int k = 0; k < s.nsegs; ++k) s.segs[k].div_n = make_fastdiv(uint32_t(s.segs[k].n));
+
+    // lanes per row: the smallest power of two covering the transfer-tensor
+    // row's 16-byte chunks (a dequantising lane writes two cache chunks)
+    s.cpr = d.head_dim * s.esz_dst / 16;
+    while ((1 << s.lg_lpr) < s.cpr) ++s.lg_lpr;
+    const int64_t rpp = kThreads >> s.lg_lpr;  // rows per workgroup pass
+    int max_n = 0;
+    for (int k = 0; k < s.nsegs; ++k) max_n = std::max(max_n, s.segs[k].n);
+    s.parts = int32_t((int64_t(d.block_size) * max_n + rpp - 1) / rpp);
+    s.parts_unpack = int32_t((int64_t(d.block_size) * s.hd + rpp - 1) / rpp);
+    return KVX_OK;
+}
+
 namespace {
 
 int conv_for(const kvx_plan_t* p, int mode)
@@ -444,6 +468,51 @@ int conv_for(const kvx_plan_t* p, int mode)
     if (mode == kvx::kRepack && p->dequant)
         return qd_conv(p->d.src_dtype, p->d.dst_dtype, p->cache_dtype);
     return p->conv;
+}
+
+// The kernel arguments every launch mode shares, from the descriptor, its
+// shape and the work-item table; the source (or transfer-tensor) pointers and
+// a paged source's fields are set by the caller.
+void fill_args(const kvx_desc& d, const kvx::Shape& s, int mode, uint32_t num_items,
+               const Item* items, void* dst, float* scales, const int32_t* bt, int32_t bt_stride,
+               int layer_shift, kvx::KArgs& a)
+{
+    a.dst = dst;
+    a.dscale = scales;
+    a.items = items;
+    a.bt = bt;
+    a.num_items = num_items;
+    a.planes = uint32_t(2 * d.num_layers);
+    a.src_plane0 = uint32_t(2 * (d.src_layer_offset + layer_shift));
+    a.dst_plane0 = uint32_t(2 * (d.dst_layer_offset + layer_shift));
+    if (mode == kvx::kUnpack) {  // transfer-tensor rows are already in decode order
+        a.num_segs = 1;
+        a.parts = uint32_t(s.parts_unpack);
+        a.seg[0] = kvx::Segment{0, 0, 0, s.hd, kvx::make_fastdiv(uint32_t(s.hd))};
+    } else {
+        a.num_segs = uint32_t(s.nsegs);
+        a.parts = uint32_t(s.parts);
+        for (int k = 0; k < s.nsegs; ++k) a.seg[k] = s.segs[k];
+    }
+    const int64_t units = int64_t(num_items) * a.planes * a.num_segs * a.parts;
+    a.units = uint32_t(units);
+    a.units_per_xcd = uint32_t((units + kvx::kXcds - 1) / kvx::kXcds);
+    a.div_parts = kvx::make_fastdiv(a.parts);
+    a.div_segs = kvx::make_fastdiv(a.num_segs);
+    a.div_items = kvx::make_fastdiv(a.num_items);
+    a.div_bs = kvx::make_fastdiv(uint32_t(d.block_size));
+    a.num_blocks = d.num_blocks;
+    a.plane_bytes = d.num_blocks * d.block_size * int64_t(s.hd) * d.head_dim * s.esz_cache;
+    a.plane_scales = d.num_blocks * d.block_size * int64_t(s.hd);
+    a.bt_stride = bt_stride;
+    a.block_size = d.block_size;
+    a.hs = s.hs;
+    a.hd = s.hd;
+    a.head_dim = d.head_dim;
+    a.row_wire_bytes = d.head_dim * s.esz_dst;
+    a.row_dst_bytes = mode == kvx::kPack ? a.row_wire_bytes : d.head_dim * s.esz_cache;
+    a.cpr = s.cpr;
+    a.lg_lpr = s.lg_lpr;
 }
 
 // Shared argument checks of the launch calls; fills the kernel arguments.
@@ -500,42 +569,8 @@ kvx_status prepare(const kvx_plan_t* p, int mode, bool paged_call, const void* c
         return fail(KVX_EDEVICE, "current device %d is not the plan's device %d", cur, p->device);
 
     const kvx_desc& d = p->d;
-    a.dst = dst;
-    a.dscale = scales;
-    a.items = p->dev_items;
-    a.bt = bt;
-    a.num_items = uint32_t(p->items.size());
-    a.planes = uint32_t(2 * d.num_layers);
-    a.src_plane0 = uint32_t(2 * (d.src_layer_offset + layer_shift));
-    a.dst_plane0 = uint32_t(2 * (d.dst_layer_offset + layer_shift));
-    if (mode == kvx::kUnpack) {  // transfer-tensor rows are already in decode order
-        a.num_segs = 1;
-        a.parts = uint32_t(p->parts_unpack);
-        a.seg[0] = kvx::Segment{0, 0, 0, p->hd, kvx::make_fastdiv(uint32_t(p->hd))};
-    } else {
-        a.num_segs = uint32_t(p->segs.size());
-        a.parts = uint32_t(p->parts);
-        for (size_t k = 0; k < p->segs.size(); ++k) a.seg[k] = p->segs[k];
-    }
-    const int64_t units = int64_t(p->items.size()) * a.planes * a.num_segs * a.parts;
-    a.units = uint32_t(units);
-    a.units_per_xcd = uint32_t((units + kvx::kXcds - 1) / kvx::kXcds);
-    a.div_parts = kvx::make_fastdiv(a.parts);
-    a.div_segs = kvx::make_fastdiv(a.num_segs);
-    a.div_items = kvx::make_fastdiv(a.num_items);
-    a.div_bs = kvx::make_fastdiv(uint32_t(d.block_size));
-    a.num_blocks = d.num_blocks;
-    a.plane_bytes = d.num_blocks * d.block_size * int64_t(p->hd) * d.head_dim * p->esz_cache;
-    a.plane_scales = d.num_blocks * d.block_size * int64_t(p->hd);
-    a.bt_stride = bt_stride;
-    a.block_size = d.block_size;
-    a.hs = p->hs;
-    a.hd = p->hd;
-    a.head_dim = d.head_dim;
-    a.row_wire_bytes = d.head_dim * p->esz_dst;
-    a.row_dst_bytes = mode == kvx::kPack ? a.row_wire_bytes : d.head_dim * p->esz_cache;
-    a.cpr = p->cpr;
-    a.lg_lpr = p->lg_lpr;
+    fill_args(d, p->sh, mode, uint32_t(p->items.size()), p->dev_items, dst, scales, bt, bt_stride,
+              layer_shift, a);
     if (mode != kvx::kUnpack && paged) {
         a.sbt = sbt;
         a.sbt_stride = sbt_stride;
@@ -624,6 +659,80 @@ kvx_status kvx_repack_paged(const kvx_plan_t* p, const void* const* shards, cons
     kvx_status st = prepare(p, kvx::kRepack, true, shards, sbt, sbt_stride, nullptr, cache, scales,
                             bt, bt_stride, a);
     return st != KVX_OK ? st : run(p, kvx::kRepack, a, stream);
+}
+
+kvx_status kvx_repack_noalloc(const kvx_desc* desc, const void* const* shards, void* cache,
+                              float* scales, const int32_t* bt, int32_t bt_stride, void* stream)
+{
+    if (!desc) return fail(KVX_EINVAL, "NULL desc");
+    kvx_status st = validate(desc);
+    if (st != KVX_OK) return st;
+    const kvx_desc& d = *desc;
+    if (d.src_order == KVX_PAGED)
+        return fail(KVX_EINVAL, "kvx_repack_noalloc reads token- or head-major sources");
+    if (d.num_requests > kvx::kNoAllocRequests)
+        return fail(KVX_EUNSUPPORTED, "kvx_repack_noalloc takes at most %d requests (%d given)",
+                    kvx::kNoAllocRequests, d.num_requests);
+    kvx::Shape s;
+    st = kvx::derive_shape(d, s);
+    if (st != KVX_OK) return st;
+    int64_t items = 0, max_blocks = 0;
+    for (int r = 0; r < d.num_requests; ++r) {
+        const int64_t nb = (int64_t(d.seq_lens[r]) + d.block_size - 1) / d.block_size;
+        items += nb;
+        max_blocks = std::max(max_blocks, nb);
+    }
+    if (items > kvx::kNoAllocItems)
+        return fail(KVX_EUNSUPPORTED,
+                    "kvx_repack_noalloc takes at most %d pages (%lld given): its work-item table "
+                    "is a static array of that many entries", kvx::kNoAllocItems,
+                    (long long)items);
+    if (items == 0) return KVX_OK;  // nothing to read or write: pointers are not used
+    if (items * 2 * d.num_layers * int64_t(s.nsegs) * s.parts > kvx::kMaxUnits)
+        return fail(KVX_EUNSUPPORTED, "more than %lld work units (pages x 2 x layers x parts)",
+                    (long long)kvx::kMaxUnits);
+
+    kvx::KArgs a;
+    std::memset(&a, 0, sizeof a);
+    if (!shards) return fail(KVX_EINVAL, "NULL src_shards array");
+    for (int k = 0; k < s.nread; ++k) {
+        const int j = s.read_shards[k];
+        if (!shards[j]) return fail(KVX_EINVAL, "src_shards[%d] is NULL", j);
+        if (!aligned16(shards[j])) return fail(KVX_EINVAL, "src_shards[%d] is not 16-byte aligned", j);
+        a.src[k] = shards[j];
+    }
+    const bool fp8 = is_fp8(s.cache_dtype);  // the cache holds scales
+    if (!cache) return fail(KVX_EINVAL, "NULL cache");
+    if (!aligned16(cache)) return fail(KVX_EINVAL, "destination not 16-byte aligned");
+    if (fp8 != (scales != nullptr))
+        return fail(KVX_EINVAL, fp8 ? "8-bit cache needs a scales buffer"
+                                    : "scales given for a 16-bit cache");
+    if (scales && !aligned16(scales)) return fail(KVX_EINVAL, "scales not 16-byte aligned");
+    if (!bt) return fail(KVX_EINVAL, "NULL block table");
+    if (bt_stride < max_blocks)
+        return fail(KVX_EINVAL, "bt_stride %d < max_blocks_per_request %lld", bt_stride,
+                    (long long)max_blocks);
+
+    kvx::Item* table = nullptr;
+    int e = kvx::scratch_items(&table);
+    if (e != 0)
+        return fail(KVX_EDEVICE, "static work-item table: %s", hipGetErrorString(hipError_t(e)));
+    kvx::ItemsArgs ia;
+    std::memset(&ia, 0, sizeof ia);
+    for (int r = 0; r < d.num_requests; ++r) ia.lens[r] = d.seq_lens[r];
+    ia.num_requests = d.num_requests;
+    ia.block_size = d.block_size;
+    ia.src_elems_per_token = 2 * int64_t(src_layers_of(d)) * s.hs * d.head_dim;
+    ia.items = table;
+    e = kvx::build_items(ia, stream);
+    if (e != 0)
+        return fail(KVX_EDEVICE, "work-item launch failed: %s", hipGetErrorString(hipError_t(e)));
+    fill_args(d, s, kvx::kRepack, uint32_t(items), table, cache, scales, bt, bt_stride, 0, a);
+    const int conv = s.dequant ? qd_conv(d.src_dtype, d.dst_dtype, s.cache_dtype) : s.conv;
+    e = kvx::launch(kvx::kRepack, conv, d.src_order, a, stream);
+    if (e != 0)
+        return fail(KVX_EDEVICE, "kernel launch failed: %s", hipGetErrorString(hipError_t(e)));
+    return KVX_OK;
 }
 
 }  // extern "C"

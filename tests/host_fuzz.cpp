@@ -3,6 +3,9 @@
 // by tests/test_host_sanitizers.py with g++ (no GPU code: without a device,
 // plans are host-only and the launch calls return KVX_EDEVICE before any
 // kernel, so the kernel entry below is never reached).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <random>
@@ -12,6 +15,9 @@
 
 namespace kvx {
 int launch(int, int, int, const KArgs&, void*) { std::abort(); }  // never reached without a device
+// the allocation-free repack's static table: no device here, as on a CPU machine
+int scratch_items(Item**) { return int(hipErrorNoDevice); }
+int build_items(const ItemsArgs&, void*) { std::abort(); }      // never reached without a table
 }
 
 int main()
@@ -44,6 +50,21 @@ int main()
         d.dst_layer_offset = pick({0, 0, 2});
         d.dst_layers = pick({0, 0, 3, 100});
         d.cache_dtype = pick({0, 0, 1, 2, 3, 4, 6});
+        // the allocation-free repack validates the same descriptor itself;
+        // aligned stand-in pointers are never dereferenced on the host
+        {
+            std::vector<const void*> sh(size_t(std::max(d.src_tp, 1)),
+                                        reinterpret_cast<const void*>(uintptr_t(0x10000)));
+            void* c = reinterpret_cast<void*>(uintptr_t(0x20000));
+            float* sc = (it & 1) ? reinterpret_cast<float*>(uintptr_t(0x30000)) : nullptr;
+            const int32_t* t = reinterpret_cast<const int32_t*>(uintptr_t(0x40000));
+            const kvx_status st = kvx_repack_noalloc(&d, sh.data(), c, sc, t, 1 << 20, nullptr);
+            if (st == KVX_OK) {
+                int64_t tokens = 0;
+                for (int32_t x : lens) tokens += x;
+                if (tokens != 0) std::abort();   // only an empty problem needs no device
+            }
+        }
         kvx_plan_t* p = nullptr;
         if (kvx_plan(&d, &p) != KVX_OK) { ++rejected; continue; }
         ++ok;

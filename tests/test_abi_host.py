@@ -28,11 +28,11 @@ def declared_entry_points():
 
 def test_every_declared_symbol_is_exported():
     names = declared_entry_points()
-    assert len(names) == 21, names
+    assert len(names) == 22, names
     for n in names:
         assert hasattr(K._lib, n), n
     assert sorted(K.EXPORTS) == names
-    assert K.kvx_abi_version() == 8
+    assert K.kvx_abi_version() == 9
 
 
 def desc_for(w, lens, **over):
@@ -353,3 +353,51 @@ def test_binding_checks_tensor_arguments_before_any_launch():
         K.kvx_pack(plan, [None], cpu)
     with pytest.raises(ValueError, match="device tensor"):
         K.kvx_unpack(plan, None, cpu, None, None, 1)
+
+
+def test_noalloc_repack_host_checks():
+    """kvx_repack_noalloc validates its descriptor and arguments before any
+    device work, with the status codes of kvx_plan and kvx_repack; its own
+    limits are 256 requests and 65536 pages (its static work-item table).  An
+    empty problem is a no-op; on a host without a device a valid call ends in
+    KVX_EDEVICE (the static table's address cannot be found)."""
+    w = SMALL["llama3_8b_small"]
+    lens = W.seq_lens(w)
+    lib = K._lib
+    sh = (ctypes.c_void_p * 1)(0x10000)
+    fake = ctypes.c_void_p(0x20000)
+
+    def call(d, shards=sh, cache=fake, scales=None, bt=fake, stride=64):
+        return lib.kvx_repack_noalloc(ctypes.byref(d) if d is not None else None, shards, cache,
+                                      scales, bt, stride, None)
+
+    assert call(None) == K.EINVAL
+    assert call(desc_for(w, lens, head_dim=0)) == K.EINVAL
+    assert call(desc_for(w, lens, src_order=K.PAGED, src_block_size=16, src_num_blocks=64)) == \
+        K.EINVAL
+    assert call(desc_for(w, [1] * 257)) == K.EUNSUPPORTED
+    assert "256 requests" in K.kvx_last_error()
+    # 65537 one-token pages: page size 1, 257 requests would trip the other limit
+    assert call(desc_for(w, [65537], block_size=1, num_blocks=1 << 20)) == K.EUNSUPPORTED
+    assert "65536 pages" in K.kvx_last_error()
+    assert call(desc_for(w, [0, 0]), shards=None, cache=None, bt=None) == K.OK   # nothing to move
+    assert call(desc_for(w, lens), shards=None) == K.EINVAL
+    assert call(desc_for(w, lens), shards=(ctypes.c_void_p * 1)(0)) == K.EINVAL
+    assert call(desc_for(w, lens), shards=(ctypes.c_void_p * 1)(0x10008)) == K.EINVAL
+    assert call(desc_for(w, lens), cache=None) == K.EINVAL
+    assert call(desc_for(w, lens), cache=ctypes.c_void_p(0x20004)) == K.EINVAL
+    assert call(desc_for(w, lens), scales=fake) == K.EINVAL          # 16-bit cache
+    assert call(desc_for(w, lens, dst_dtype=K.E4M3FN)) == K.EINVAL   # 8-bit cache, no scales
+    assert call(desc_for(w, lens), bt=None) == K.EINVAL
+    assert call(desc_for(w, lens), stride=1) == K.EINVAL
+    if os.environ.get("HIP_VISIBLE_DEVICES", None) == "" or not _has_device():
+        assert call(desc_for(w, lens)) == K.EDEVICE
+
+
+def _has_device() -> bool:
+    n = ctypes.c_int(0)
+    try:
+        rt = ctypes.CDLL("libamdhip64.so")
+    except OSError:
+        return False
+    return rt.hipGetDeviceCount(ctypes.byref(n)) == 0 and n.value > 0
