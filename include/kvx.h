@@ -309,21 +309,26 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * memory pool, and the paper's conclusion names by-layer transmission as the
  * next step.  A pipe moves a plan's layers in chunks of chunk_layers layers:
  * each chunk is packed straight into a slot of a pinned host ring (the pack
- * kernel's stores cross the host link; on the caller's stream), copied into
- * a device receive slot (host to device, a DMA copy) and unpacked into the
- * cache (on a stream of the pipe).  With `slots` slots, chunk c + 1 is
- * packed and chunk c - 1 unpacked while chunk c crosses the bus.  The cache
- * and scales written equal kvx_pack followed by kvx_unpack of the whole plan.
+ * kernel's stores cross the host link), copied into a device receive slot
+ * (host to device) and unpacked into the cache, each stage on a stream of the
+ * pipe.  With `slots` slots, chunk c + 1 is packed and chunk c - 1 unpacked
+ * while chunk c crosses the bus.  The cache and scales written equal
+ * kvx_pack followed by kvx_unpack of the whole plan.
  *
  * kvx_pipe_create allocates the pinned host ring (slots x the largest
  * chunk's transfer-tensor bytes, hipHostMalloc with hipHostMallocMapped),
- * device receive slots of the same size, one copy stream, one unpack stream
- * and their events (all default priority), on the plan's device.  The plan must
- * outlive the pipe.  KVX_EINVAL for a NULL plan or out, chunk_layers outside
- * [1, num_layers] or slots < 1; KVX_EDEVICE for a host-only plan;
- * KVX_ENOMEM if an allocation fails.
+ * device receive slots of the same size, three streams and their events, on
+ * the plan's device.  The streams are CU-masked (hipExtStreamCreateWithCUMask,
+ * default priority): the pack's covers half the device's CUs, the copy's and
+ * the unpack's a quarter each, so that no stage waits for CUs another holds;
+ * like streams created without flags, they synchronise with the null stream.
+ * The plan must outlive the pipe.  KVX_EINVAL for a NULL plan or out,
+ * chunk_layers outside [1, num_layers] or slots < 1; KVX_EDEVICE for a
+ * host-only plan or when the streams cannot be created; KVX_ENOMEM if an
+ * allocation fails.
  *
- * kvx_pipe_run enqueues the whole transfer and returns; the caller's stream
+ * kvx_pipe_run enqueues the whole transfer and returns: the pipe's streams
+ * start after the caller's stream's earlier work, and the caller's stream
  * then waits for the last unpack.  Arguments as kvx_repack (kvx_repack_paged
  * for a paged plan, whose source block table is passed; otherwise it must be
  * NULL).  Two runs of one pipe must not overlap (they share the slots);

@@ -1,10 +1,19 @@
 // Layer-streamed transfer through a pinned host ring: the plan's layers move
 // in chunks, each packed straight into a slot of pinned host memory (the pack
-// kernel's stores cross the host link), copied by DMA into a device receive
-// slot and unpacked, with the stages of consecutive chunks overlapped on three
-// streams.  Writing the host slot from the kernel leaves the DMA engines one
-// direction only: two DMA copies in opposite directions overlapped in some
-// processes and ran one after the other in others.
+// kernel's stores cross the host link), copied into a device receive slot and
+// unpacked, with the stages of consecutive chunks overlapped on the pipe's
+// three streams.  Writing the host slot from the kernel leaves the copy
+// engines one direction only: two copies in opposite directions overlapped in
+// some processes and ran one after the other in others.
+//
+// Each stage has a stream with a CU mask of its own: the pack on half the
+// CUs, the host-to-device copy (which HIP runs as a blit kernel) and the
+// unpack on a quarter each.  A pack bound by the host link keeps its
+// workgroups resident for long; with all three stages free to use every CU,
+// the copy of one chunk sometimes waited for CUs behind the next pack, and
+// whether it did depended on how HIP had mapped the streams onto hardware
+// queues (on the streams the process created earlier).  CU-masked streams
+// block with the null stream like streams created without flags.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -25,7 +34,7 @@ struct kvx_pipe_s {
     char* host = nullptr;         // pinned ring, slots x slot_bytes, mapped for the device
     char* host_dev = nullptr;     // the ring's device address (the pack writes through it)
     char* recv = nullptr;         // device, slots x slot_bytes
-    hipStream_t h2d = nullptr, unpack = nullptr;
+    hipStream_t pack = nullptr, h2d = nullptr, unpack = nullptr;
     hipEvent_t start = nullptr;
     std::vector<hipEvent_t> packed, received, unpacked;  // one per slot
 };
@@ -37,13 +46,13 @@ using kvx::fail;
 void release(kvx_pipe_s* q)
 {
     if (!q) return;
-    for (hipStream_t s : {q->h2d, q->unpack})
+    for (hipStream_t s : {q->pack, q->h2d, q->unpack})
         if (s) (void)hipStreamSynchronize(s);
     for (auto* v : {&q->packed, &q->received, &q->unpacked})
         for (hipEvent_t e : *v)
             if (e) (void)hipEventDestroy(e);
     if (q->start) (void)hipEventDestroy(q->start);
-    for (hipStream_t s : {q->h2d, q->unpack})
+    for (hipStream_t s : {q->pack, q->h2d, q->unpack})
         if (s) (void)hipStreamDestroy(s);
     if (q->host) (void)hipHostFree(q->host);
     if (q->recv) (void)hipFree(q->recv);
@@ -65,12 +74,28 @@ kvx_status chunk_plan(const kvx_plan_t* p, int n, kvx_plan_t** out)
 
 bool ok(hipError_t e) { return e == hipSuccess; }
 
+// A stream whose kernels run on the CUs selected by `byte_mask` in every byte
+// position it covers: CU i belongs to the stream when bit (i / 8) % 4 of
+// byte_mask is set, so each of the 8 XCDs contributes CUs to it whether the
+// mask's bits are dealt to the XCDs in runs of 32 or round-robin.
+bool masked_stream(int device, unsigned byte_mask, hipStream_t* out)
+{
+    int cus = 0;
+    if (!ok(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device)) ||
+        cus <= 0)
+        return false;
+    std::vector<uint32_t> mask(size_t((cus + 31) / 32), 0u);
+    for (int i = 0; i < cus; ++i)
+        if ((byte_mask >> ((i / 8) % 4)) & 1u) mask[size_t(i / 32)] |= 1u << (i % 32);
+    return ok(hipExtStreamCreateWithCUMask(out, uint32_t(mask.size()), mask.data()));
+}
+
 // A run that fails part way has chunks enqueued on the pipe's streams: the
 // caller's stream still waits for them, so that buffers it releases after the
 // failure are no longer in use.
 kvx_status stop(kvx_pipe_s* q, hipStream_t s0, kvx_status st)
 {
-    for (hipStream_t s : {q->h2d, q->unpack})
+    for (hipStream_t s : {q->pack, q->h2d, q->unpack})
         if (ok(hipEventRecord(q->start, s))) (void)hipStreamWaitEvent(s0, q->start, 0);
     return st;
 }
@@ -121,8 +146,9 @@ kvx_status kvx_pipe_create(const kvx_plan_t* p, int32_t chunk_layers, int32_t sl
             return fail(KVX_ENOMEM, "pipe buffers (2 x %zu bytes) could not be allocated", ring);
         }
     }
-    bool good = ok(hipStreamCreateWithFlags(&q->h2d, hipStreamNonBlocking)) &&
-                ok(hipStreamCreateWithFlags(&q->unpack, hipStreamNonBlocking)) &&
+    bool good = masked_stream(q->device, 0x3u, &q->pack) &&    // half the CUs
+                masked_stream(q->device, 0x4u, &q->h2d) &&     // a quarter
+                masked_stream(q->device, 0x8u, &q->unpack) &&  // a quarter
                 ok(hipEventCreateWithFlags(&q->start, hipEventDisableTiming));
     for (auto* v : {&q->packed, &q->received, &q->unpacked}) {
         v->assign(size_t(slots), nullptr);
@@ -177,7 +203,7 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
 
     // the pipe's streams start after the caller's earlier work
     if (!ok(hipEventRecord(q->start, s0))) return fail(KVX_EDEVICE, "event record failed");
-    for (hipStream_t s : {q->h2d, q->unpack})
+    for (hipStream_t s : {q->pack, q->h2d, q->unpack})
         if (!ok(hipStreamWaitEvent(s, q->start, 0))) return fail(KVX_EDEVICE, "stream wait failed");
 
     for (int c = 0; c < q->num_chunks; ++c) {
@@ -190,20 +216,20 @@ kvx_status kvx_pipe_run(kvx_pipe_t* q, const void* const* shards, const int32_t*
         char* host_dev = q->host_dev + size_t(s) * q->slot_bytes;
         char* recv = q->recv + size_t(s) * q->slot_bytes;
 
-        // pack into the host slot (caller's stream): the slot's previous
-        // chunk must have been copied to the device
-        if (reuse && !ok(hipStreamWaitEvent(s0, q->received[s], 0)))
+        // pack into the host slot: the slot's previous chunk must have been
+        // copied to the device
+        if (reuse && !ok(hipStreamWaitEvent(q->pack, q->received[s], 0)))
             return stop(q, s0, fail(KVX_EDEVICE, "stream wait failed"));
         kvx_status st = kvx::launch_shifted(cp, kvx::kPack, shift, shards, sbt, sbt_stride,
-                                            nullptr, host_dev, nullptr, nullptr, 0, stream);
+                                            nullptr, host_dev, nullptr, nullptr, 0, q->pack);
         if (st != KVX_OK) return stop(q, s0, st);
-        bool good = ok(hipEventRecord(q->packed[s], s0));
+        bool good = ok(hipEventRecord(q->packed[s], q->pack));
         // host -> device: the receive slot must have been unpacked
         good = good && ok(hipStreamWaitEvent(q->h2d, q->packed[s], 0));
         if (reuse) good = good && ok(hipStreamWaitEvent(q->h2d, q->unpacked[s], 0));
         good = good && ok(hipMemcpyAsync(recv, host, bytes, hipMemcpyHostToDevice, q->h2d)) &&
                ok(hipEventRecord(q->received[s], q->h2d));
-        // unpack (pipe's stream)
+        // unpack
         good = good && ok(hipStreamWaitEvent(q->unpack, q->received[s], 0));
         if (!good)
             return stop(q, s0, fail(KVX_EDEVICE, "copy or event enqueue failed: %s",
