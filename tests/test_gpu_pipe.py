@@ -115,3 +115,38 @@ def test_pipe_run_with_a_missing_shard_fails_then_runs():
     want_c, _ = oracle_pool(w, lens, bt, stride, shards)
     assert np.array_equal(cache.cpu().numpy(), want_c)
     del pipe
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_small", "fp8_small"])
+def test_pipe_on_a_side_stream(name):
+    """A caller stream other than the null stream: the pipe's stages start
+    after that stream's earlier work (the pool filled with sentinels on it just
+    before the run, over junk written before that), and the stream's later
+    work (a copy of the pool) sees the whole result, with no device
+    synchronisation in between."""
+    w = (SMALL | SMALL_DEQUANT)[name]
+    lens, bt, stride, shards = inputs(w)
+    log(f"pipe {name} on a side stream")
+    want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
+    plan = K.kvx_plan(desc_for(w, lens))
+    pipe = K.kvx_pipe_create(plan, 1, 2)
+    dsh = [dev_u16(s) for s in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    check_shapes(w, lens, bt, stride, dsh, w.layers)
+    cache, scales = pool(w, w.layers, fill=0x5A)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    for _ in range(2):
+        with torch.cuda.stream(side):
+            cache.fill_(W.SENTINEL)
+            if scales is not None:
+                scales.view(torch.uint8).fill_(W.SENTINEL)
+            K.kvx_pipe_run(pipe, dsh, None, 0, cache, scales, bt_d, stride, side)
+            got_c = cache.clone()
+            got_s = None if scales is None else scales.clone()
+            cache.fill_(0x5A)  # later work on the stream must not overtake the copies
+        side.synchronize()
+        assert np.array_equal(got_c.cpu().numpy(), want_c)
+        if want_s is not None:
+            assert np.array_equal(got_s.cpu().numpy().view(np.uint32), want_s.view(np.uint32))
+    del pipe
