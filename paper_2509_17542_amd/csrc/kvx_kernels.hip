@@ -711,8 +711,31 @@ __device__ __forceinline__ void convert_part(const KArgs& a)
         if constexpr (kHalves)
             __builtin_nontemporal_store(__builtin_bit_cast(v4u, out2),
                                         reinterpret_cast<v4u*>(drow + (sub + a.cpr) * 16));
-        if constexpr (kScales)
+        if constexpr (kScales && !kFp8)  // the 8-bit unpack: the scale it loaded
             if (sub == 0) __builtin_nontemporal_store(sc, sbase + row);
+    }
+    if constexpr (kFp8) {
+        // The quantising launches' 4-byte row scales go out through LDS: lane
+        // 0 of each row leaves its scale and destination slot there, and after
+        // the barrier the first lanes of wave 0 store them all, so a
+        // workgroup's 32 or so consecutive scales leave as one store
+        // instruction covering whole cache lines instead of four 32-byte
+        // pieces, one per wave.  Ordinary stores here: the L2 merges them into
+        // whole lines.  Measured 2% faster on the fp8 decode cache than
+        // non-temporal per-row stores; the 8-bit unpack, whose scales arrive
+        // by a load rather than from the lanes' own arithmetic, measured 8%
+        // slower this way and keeps the per-row store.
+        __shared__ float lds_scale[kThreads];
+        __shared__ int lds_slot[kThreads];  // the row's index in sbase, -1: not written
+        if (sub == 0) {
+            lds_scale[threadIdx.x >> lg] = sc;
+            lds_slot[threadIdx.x >> lg] = ok ? row : -1;
+        }
+        __syncthreads();
+        if (int(threadIdx.x) < (kThreads >> lg)) {
+            const int slot = lds_slot[threadIdx.x];
+            if (slot >= 0) sbase[slot] = lds_scale[threadIdx.x];
+        }
     }
 }
 
