@@ -77,7 +77,8 @@ bool ok(hipError_t e) { return e == hipSuccess; }
 // A stream whose kernels run on the CUs selected by `byte_mask` in every byte
 // position it covers: CU i belongs to the stream when bit (i / 8) % 4 of
 // byte_mask is set, so each of the 8 XCDs contributes CUs to it whether the
-// mask's bits are dealt to the XCDs in runs of 32 or round-robin.
+// mask's bits are dealt to the XCDs in runs of 32 or round-robin.  A device
+// too small to give the stream any CU this way gives it all of them.
 bool masked_stream(int device, unsigned byte_mask, hipStream_t* out)
 {
     int cus = 0;
@@ -85,8 +86,14 @@ bool masked_stream(int device, unsigned byte_mask, hipStream_t* out)
         cus <= 0)
         return false;
     std::vector<uint32_t> mask(size_t((cus + 31) / 32), 0u);
+    bool any = false;
     for (int i = 0; i < cus; ++i)
-        if ((byte_mask >> ((i / 8) % 4)) & 1u) mask[size_t(i / 32)] |= 1u << (i % 32);
+        if ((byte_mask >> ((i / 8) % 4)) & 1u) {
+            mask[size_t(i / 32)] |= 1u << (i % 32);
+            any = true;
+        }
+    if (!any)
+        for (int i = 0; i < cus; ++i) mask[size_t(i / 32)] |= 1u << (i % 32);
     return ok(hipExtStreamCreateWithCUMask(out, uint32_t(mask.size()), mask.data()));
 }
 
