@@ -60,3 +60,26 @@ def test_bench_prints_one_json_line():
     assert cfg_leg["repack"]["GB/s"] > 0 and cfg_leg["latency_ms_per_request"]["p50"] > 0
     assert out["latency_ms_per_request"]["p50"] > 0
     assert out["pack"]["GB/s"] > 0 and out["unpack"]["GB/s"] > 0
+
+
+def test_settle_counts_launches_until_the_time_has_passed():
+    """The configs leg's warm-up: at least the given launches, then whole
+    groups of them until the wall time has passed (a fake launch of 1 ms)."""
+    import time
+    import types
+    sys.path.insert(0, ROOT)
+    import bench
+    calls = []
+    fake_torch = types.SimpleNamespace(cuda=types.SimpleNamespace(synchronize=lambda: None))
+
+    def launch():
+        calls.append(1)
+        time.sleep(0.001)
+
+    n = bench.settle(launch, fake_torch, 3, 0.0)
+    assert n == 3 and len(calls) == 3
+    calls.clear()
+    n = bench.settle(launch, fake_torch, 3, 20.0)
+    assert n == len(calls) and n % 3 == 0 and 18 <= n <= 60
+    calls.clear()
+    assert bench.settle(launch, fake_torch, 0, 5.0) == len(calls) >= 4
