@@ -38,8 +38,10 @@
 // The path is a gather/scatter stream with no reuse and no contraction: the
 // 16-bit conversions are bound by HBM bandwidth, the 8-bit ones (e4m3fn,
 // e5m2, per-row scales) by the vector ALUs and HBM together.  There is no
-// MFMA and no LDS staging: rows are whole 16-byte vectors on both sides, so a
-// [token][head] <-> [head][token] reorder is a change of row addresses only.
+// MFMA and no LDS staging of rows: rows are whole 16-byte vectors on both
+// sides, so a [token][head] <-> [head][token] reorder is a change of row
+// addresses only.  (The quantising kernels use LDS only to gather their 4-byte
+// row scales into whole-line stores.)
 #include <hip/hip_runtime.h>
 
 #include <mutex>

@@ -500,3 +500,38 @@ def pair_rows(fmt, mags, nan=False, block=512, threads=None):
     with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
         list(ex.map(fill, range(0, mags.size, block)))
     return out
+
+# Every conversion in every source order: each (source type, transfer-tensor
+# type, cache type) the library accepts, from token-major, head-major and
+# paged sources, so that every kernel instantiation runs.  Each case merges
+# two prefill shards (TP2 -> TP1: two head segments), has a ragged last page
+# and an empty request, and varies the row size with the order (head_dim 128
+# token-major, 64 head-major, 256 paged; paged sources use 12-token pages
+# against 16-token decode pages).  8-bit transfers draw per-head scales over
+# four decades; bf16 -> fp16 draws values up to about 2^17, so some overflow.
+_MATRIX_TYPES = [("bf16", ""), ("fp16", ""), ("e4m3fn", ""), ("e5m2", ""),
+                 ("e4m3fn", "bf16"), ("e4m3fn", "fp16"), ("e5m2", "bf16"), ("e5m2", "fp16")]
+
+
+def _matrix():
+    out = {}
+    seed = 600
+    for src in ("bf16", "fp16"):
+        for dst, cache in _MATRIX_TYPES:
+            for order, hdim in (("thd", 128), ("htd", 64), ("paged", 256)):
+                if src == dst and not cache and order != "paged":
+                    continue  # a plain copy: the small and paged cases above cover it
+                seed += 1
+                name = f"mx_{src}_{dst}{'_' + cache if cache else ''}_{order}"
+                w = W.Workload(name, 2, 2, 4, hdim, 2, 1, 0, src, dst, order, 16, 24, 3, 1, 45,
+                               seed=seed, lens_override=(45, 0, 19),
+                               sigma=30000.0 if (src, dst) == ("bf16", "fp16") else 1.0,
+                               head_scale_log10=(-2.0, 2.0) if dst in ("e4m3fn", "e5m2") else None,
+                               src_block_size=12 if order == "paged" else 0,
+                               src_num_blocks=16 if order == "paged" else 0,
+                               cache_dtype=cache)
+                out[name] = w
+    return out
+
+
+MATRIX = _matrix()
