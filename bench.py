@@ -61,7 +61,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b_bf16_bs16")
     ap.add_argument("--configs", default=",".join(CONFIG_WORKLOADS),
                     help="comma-separated workloads measured one after another after the headline "
