@@ -77,6 +77,10 @@ def main():
     ap.add_argument("--stream-chunk", type=int, default=4,
                     help="layers per chunk of the layer-streamed transfer leg (0 = skip it)")
     ap.add_argument("--stream-slots", type=int, default=3)
+    ap.add_argument("--stream-extra-streams", type=int, default=0,
+                    help="HIP streams the process creates (and keeps) before the layer-streamed "
+                         "transfer's pipe: a diagnostic of the pipe's independence from how "
+                         "earlier streams map onto hardware queues")
     ap.add_argument("--calib-gib", type=float, default=2.0,
                     help="bytes read (= bytes written) by the plain copies timed as ceilings "
                          "and as the reference of the rocprofv3 byte counters; 0 = skip")
@@ -189,7 +193,7 @@ def main():
         out["layer_stream"] = stream_leg(K, torch, wb.plans[0], wb.infos[0], wb.dshards[0],
                                          wb.sbt_d, wb.sstride, wb.cache, wb.scales, wb.bt_d,
                                          wb.stride, stream, min(args.stream_chunk, w.layers),
-                                         args.stream_slots, timed)
+                                         args.stream_slots, timed, args.stream_extra_streams)
 
     if not args.no_extras:
         out["pd_planner"] = planner_leg(K, w)
@@ -471,12 +475,22 @@ def planner_leg(K, w):
 
 
 def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream,
-               chunk, slots, timed):
+               chunk, slots, timed, extra_streams=0):
     """The layer-streamed transfer through pinned host memory (kvx_pipe_run),
     against the same bytes moved serially (pack everything, copy it to pinned
     host memory, copy it back, unpack everything) and against plain copies of
     the transfer tensor in each direction.  Rates are transfer-tensor bytes
-    per direction per second: this leg is bound by the host link, not HBM."""
+    per direction per second: this leg is bound by the host link, not HBM.
+    `extra_streams` HIP streams are created before the pipe and destroyed
+    after the leg; each pipe run is also timed on its own (HIP events)."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so") if extra_streams > 0 else None
+    extra = []
+    for _ in range(extra_streams):
+        h = ctypes.c_void_p()
+        if hip.hipStreamCreate(ctypes.byref(h)) != 0:
+            raise RuntimeError("hipStreamCreate failed")
+        extra.append(h)
     pipe = K.kvx_pipe_create(plan, chunk, slots)
     pinfo = K.kvx_pipe_info_get(pipe)
     nbytes = int(pinfo.bus_bytes)
@@ -508,11 +522,23 @@ def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_
         ms, _, _, _ = timed(fn, steps, 1)
         res[name + "_ms"] = round(ms, 3)
         log(f"layer stream leg: {name} {ms:.2f} ms ({nbytes / (ms * 1e-3) / 1e9:.1f} GB/s each way)")
+    each = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        piped()
+        b.record(stream)
+        torch.cuda.synchronize()
+        each.append(round(a.elapsed_time(b), 2))
+    res["pipe_ms_each"] = each
+    res["extra_streams_before_pipe"] = extra_streams
     res["pipe_GB/s_each_way"] = round(nbytes / (res["pipe_ms"] * 1e-3) / 1e9, 2)
     res["serial_over_pipe"] = round(res["serial_ms"] / res["pipe_ms"], 3)
     res["note"] = ("layer chunks packed straight into pinned host memory, copied back to the "
                    "device, unpacked; host-link bound, not an HBM figure")
     del pipe, wire, back, host
+    for h in extra:
+        hip.hipStreamDestroy(h)
     return res
 
 

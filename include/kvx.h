@@ -328,14 +328,19 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * allocation fails.
  *
  * kvx_pipe_run enqueues the whole transfer and returns: the pipe's streams
- * start after the caller's stream's earlier work, and the caller's stream
- * then waits for the last unpack.  Arguments as kvx_repack (kvx_repack_paged
- * for a paged plan, whose source block table is passed; otherwise it must be
- * NULL).  Two runs of one pipe must not overlap (they share the slots);
- * runs of different pipes may.  A bad argument is reported before anything is
- * enqueued; a launch or enqueue failure part way through returns its status
- * with the cache partly written, and the caller's stream still waits for the
- * chunks already enqueued. */
+ * start after the caller's stream's earlier work and after the pipe's
+ * previous run (runs of one pipe share the slots, so the pipe orders them
+ * itself), and the caller's stream's later work waits for the last unpack.
+ * On the legacy null stream (NULL or hipStreamLegacy) the pipe enqueues
+ * nothing on the caller's stream, whose synchronisation with the pipe's
+ * streams gives that order by itself; on any other stream it records an
+ * event before the run and waits for one after it.  Arguments as kvx_repack
+ * (kvx_repack_paged for a paged plan, whose source block table is passed;
+ * otherwise it must be NULL).  One pipe must not be used from two threads at
+ * once; runs of different pipes may overlap.  A bad argument is reported
+ * before anything is enqueued; a launch or enqueue failure part way through
+ * returns its status with the cache partly written, and the caller's stream
+ * and the pipe's next run still wait for the chunks already enqueued. */
 typedef struct kvx_pipe_s kvx_pipe_t; /* opaque, library-owned */
 
 typedef struct {

@@ -117,16 +117,23 @@ def test_pipe_run_with_a_missing_shard_fails_then_runs():
     del pipe
 
 
+def _stream(kind):
+    return torch.cuda.Stream() if kind == "side" else torch.cuda.current_stream()
+
+
+@pytest.mark.parametrize("kind", ["side", "default"])
 @pytest.mark.parametrize("name", ["llama3_8b_small", "fp8_small"])
-def test_pipe_on_a_side_stream(name):
-    """A caller stream other than the null stream: the pipe's stages start
-    after that stream's earlier work (the pool filled with sentinels on it just
-    before the run, over junk written before that), and the stream's later
-    work (a copy of the pool) sees the whole result, with no device
-    synchronisation in between."""
+def test_pipe_orders_with_the_callers_stream(name, kind):
+    """On a created stream (an event each way) and on the default (legacy
+    null) stream (the pipe enqueues nothing there; its streams synchronise
+    with it by themselves): the pipe's stages start after the stream's
+    earlier work (the pool filled with sentinels on it just before the run,
+    over junk written before that), and the stream's later work (a copy of
+    the pool) sees the whole result, with no device synchronisation in
+    between."""
     w = (SMALL | SMALL_DEQUANT)[name]
     lens, bt, stride, shards = inputs(w)
-    log(f"pipe {name} on a side stream")
+    log(f"pipe {name} on the {kind} stream")
     want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
     plan = K.kvx_plan(desc_for(w, lens))
     pipe = K.kvx_pipe_create(plan, 1, 2)
@@ -135,18 +142,45 @@ def test_pipe_on_a_side_stream(name):
     check_shapes(w, lens, bt, stride, dsh, w.layers)
     cache, scales = pool(w, w.layers, fill=0x5A)
     torch.cuda.synchronize()
-    side = torch.cuda.Stream()
+    st = _stream(kind)
     for _ in range(2):
-        with torch.cuda.stream(side):
+        with torch.cuda.stream(st):
             cache.fill_(W.SENTINEL)
             if scales is not None:
                 scales.view(torch.uint8).fill_(W.SENTINEL)
-            K.kvx_pipe_run(pipe, dsh, None, 0, cache, scales, bt_d, stride, side)
+            K.kvx_pipe_run(pipe, dsh, None, 0, cache, scales, bt_d, stride, st)
             got_c = cache.clone()
             got_s = None if scales is None else scales.clone()
             cache.fill_(0x5A)  # later work on the stream must not overtake the copies
-        side.synchronize()
+        st.synchronize()
         assert np.array_equal(got_c.cpu().numpy(), want_c)
         if want_s is not None:
             assert np.array_equal(got_s.cpu().numpy().view(np.uint32), want_s.view(np.uint32))
+    del pipe
+
+
+@pytest.mark.parametrize("kind", ["side", "default"])
+def test_pipe_runs_back_to_back(kind):
+    """Three runs of one pipe enqueued one after another with nothing between
+    them, into three pools: the pipe orders its own runs (they share the
+    slots), so each pool holds the whole result.  Three chunks over two
+    slots, so every run reuses a slot of the one before."""
+    w = SMALL["llama3_70b_small_r1"].replace(layers=3, total_layers=3)
+    lens, bt, stride, shards = inputs(w)
+    log(f"pipe back to back on the {kind} stream")
+    want_c, _ = oracle_pool(w, lens, bt, stride, shards)
+    plan = K.kvx_plan(desc_for(w, lens))
+    pipe = K.kvx_pipe_create(plan, 1, 2)
+    dsh = [dev_u16(s) for s in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    check_shapes(w, lens, bt, stride, dsh, w.layers)
+    pools = [pool(w, w.layers)[0] for _ in range(3)]
+    torch.cuda.synchronize()
+    st = _stream(kind)
+    for c in pools:
+        K.kvx_pipe_run(pipe, dsh, None, 0, c, None, bt_d, stride, st)
+    st.synchronize()
+    torch.cuda.synchronize()
+    for c in pools:
+        assert np.array_equal(c.cpu().numpy(), want_c)
     del pipe
