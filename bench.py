@@ -192,8 +192,8 @@ def main():
     if not args.no_extras and args.stream_chunk > 0 and len(stages) == 1:
         out["layer_stream"] = stream_leg(K, torch, wb.plans[0], wb.infos[0], wb.dshards[0],
                                          wb.sbt_d, wb.sstride, wb.cache, wb.scales, wb.bt_d,
-                                         wb.stride, stream, min(args.stream_chunk, w.layers),
-                                         args.stream_slots, timed, args.stream_extra_streams)
+                                         wb.stride, min(args.stream_chunk, w.layers),
+                                         args.stream_slots, args.stream_extra_streams)
 
     if not args.no_extras:
         out["pd_planner"] = planner_leg(K, w)
@@ -474,15 +474,19 @@ def planner_leg(K, w):
     return res
 
 
-def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream,
-               chunk, slots, timed, extra_streams=0):
+def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_d, stride,
+               chunk, slots, extra_streams=0):
     """The layer-streamed transfer through pinned host memory (kvx_pipe_run),
     against the same bytes moved serially (pack everything, copy it to pinned
     host memory, copy it back, unpack everything) and against plain copies of
     the transfer tensor in each direction.  Rates are transfer-tensor bytes
     per direction per second: this leg is bound by the host link, not HBM.
-    `extra_streams` HIP streams are created before the pipe and destroyed
-    after the leg; each pipe run is also timed on its own (HIP events)."""
+    The leg runs on a stream of its own, as a serving engine's transfers
+    would (the legacy null stream synchronises with the pipe's CU-masked
+    streams: work on it between runs costs the pipe about 2.5% per run, and
+    the host sometimes waits in the enqueue).  `extra_streams` HIP streams
+    are created before the pipe and destroyed after the leg; each pipe run is
+    also timed on its own (HIP events)."""
     import ctypes
     hip = ctypes.CDLL("libamdhip64.so") if extra_streams > 0 else None
     extra = []
@@ -494,6 +498,19 @@ def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_
     pipe = K.kvx_pipe_create(plan, chunk, slots)
     pinfo = K.kvx_pipe_info_get(pipe)
     nbytes = int(pinfo.bus_bytes)
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()   # the leg's own stream
+
+    def timed_here(fn, steps, warmup):
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(steps):
+                fn()
+            torch.cuda.synchronize()
+        return (time.perf_counter() - t) / steps * 1e3
 
     def piped():
         K.kvx_pipe_run(pipe, dshards, sbt_d, sstride, cache, scales, bt_d, stride, stream)
@@ -515,19 +532,21 @@ def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_
         K.kvx_unpack(plan, back, cache, scales, bt_d, stride, stream)
 
     res = {"chunk_layers": chunk, "slots": slots, "chunks": int(pinfo.num_chunks),
-           "bytes_each_way": nbytes, "pinned_host_bytes": int(pinfo.host_bytes)}
+           "bytes_each_way": nbytes, "pinned_host_bytes": int(pinfo.host_bytes),
+           "stream": "created"}
     for name, fn, steps in (("pipe", piped, 5), ("serial", serial, 3),
                             ("d2h_copy", lambda: host.copy_(wire, non_blocking=True), 3),
                             ("h2d_copy", lambda: back.copy_(host, non_blocking=True), 3)):
-        ms, _, _, _ = timed(fn, steps, 1)
+        ms = timed_here(fn, steps, 1)
         res[name + "_ms"] = round(ms, 3)
         log(f"layer stream leg: {name} {ms:.2f} ms ({nbytes / (ms * 1e-3) / 1e9:.1f} GB/s each way)")
     each = []
     for _ in range(5):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        piped()
-        b.record(stream)
+        with torch.cuda.stream(stream):
+            a.record(stream)
+            piped()
+            b.record(stream)
         torch.cuda.synchronize()
         each.append(round(a.elapsed_time(b), 2))
     res["pipe_ms_each"] = each

@@ -334,7 +334,11 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * On the legacy null stream (NULL or hipStreamLegacy) the pipe enqueues
  * nothing on the caller's stream, whose synchronisation with the pipe's
  * streams gives that order by itself; on any other stream it records an
- * event before the run and waits for one after it.  Arguments as kvx_repack
+ * event before the run and waits for one after it.  Work that the caller
+ * puts on the legacy null stream between runs is ordered against the pipe's
+ * streams by the runtime, which costs about 2.5% per run and the first few
+ * times made the host wait 20-30 ms in that enqueue: transfers on a created
+ * stream see neither.  Arguments as kvx_repack
  * (kvx_repack_paged for a paged plan, whose source block table is passed;
  * otherwise it must be NULL).  One pipe must not be used from two threads at
  * once; runs of different pipes may overlap.  A bad argument is reported
