@@ -287,8 +287,9 @@ __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float
             q[e] = quotient_for_code(F::widen(h), s, r);  // the element's sign carried through
         }
         // bytes 2-3 of the first conversion's `old` operand are overwritten by
-        // the second, so any register serves (no zeroing move)
-        const int lo = Q::cvt_pk(q[0], q[1], __float_as_int(q[2]), false);
+        // the second, so any register serves; q[0], dead after this
+        // instruction, lets the result take its register (no copy of `old`)
+        const int lo = Q::cvt_pk(q[0], q[1], __float_as_int(q[0]), false);
         out[d] = uint32_t(Q::cvt_pk(q[2], q[3], lo, true));
     }
 }
