@@ -160,6 +160,7 @@ def main():
         **({"src_pages": {"block_size": w.src_block_size, "pool_blocks": w.src_num_blocks}}
            if paged else {}),
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "hbm_peak_from_device": device_hbm_peak(),
         "repack_kernel_ms": {"mean": round(k_mean, 4), "min": round(k_min, 4),
                              "median": round(k_med, 4)},
     }
@@ -175,7 +176,7 @@ def main():
     headline = {"repack": {"kernel_ms": round(k_mean, 4), "GB/s": round(achieved, 1),
                            "frac": round(achieved / HBM_PEAK_GBS, 4)}}
     if not args.no_extras:
-        for name in ("pack", "unpack"):
+        for name in ("pack", "unpack", "pack_unpack"):
             ms, km, _, _ = timed(getattr(wb, name), max(5, args.steps // 2), 2)
             gbs = wb.bytes(name) / (km * 1e-3) / 1e9
             out[name] = {"ms_per_step": round(ms, 4), "kernel_ms": round(km, 4),
@@ -272,6 +273,8 @@ class Workbench:
         self.fork = torch.cuda.Event()
 
     def bytes(self, op):
+        if op == "pack_unpack":
+            return self.bytes("pack") + self.bytes("unpack")
         return sum(getattr(i, f"read_bytes_{op}") + getattr(i, f"write_bytes_{op}")
                    for i in self.infos)
 
@@ -318,6 +321,11 @@ class Workbench:
         wires = self._wires()
         self._per_stage(lambda k, st: self.K.kvx_unpack(self.plans[k], wires[k], self.cache,
                                                         self.scales, self.bt_d, self.stride, st))
+
+    def pack_unpack(self):
+        """The two-step path: pack into the transfer tensor, then unpack it."""
+        self.pack()
+        self.unpack()
 
     def free_wires(self):
         self.wires = None
@@ -416,15 +424,16 @@ def configs_leg(K, W, torch, stream, timed, names, headline_name, headline, step
             continue
         wb = Workbench(K, W, torch, w, stream)
         entry["tokens"] = int(wb.lens.sum())
-        for op in ("repack", "pack", "unpack"):
+        for op in ("repack", "pack", "unpack", "pack_unpack"):
             n = steps if op == "repack" else max(5, steps // 2)
             nw = settle(getattr(wb, op), torch, warmup, CONFIG_SETTLE_MS)
-            _, km, kmin, _ = timed(getattr(wb, op), n, 0)
+            _, km, kmin, kmed = timed(getattr(wb, op), n, 0)
             nbytes = wb.bytes(op)
             gbs = nbytes / (km * 1e-3) / 1e9
             entry[op] = {"bytes_per_launch": nbytes, "kernel_ms": round(km, 4),
-                         "kernel_ms_min": round(kmin, 4), "GB/s": round(gbs, 1),
-                         "frac": round(gbs / HBM_PEAK_GBS, 4), "warmup_launches": nw}
+                         "kernel_ms_min": round(kmin, 4), "kernel_ms_median": round(kmed, 4),
+                         "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "warmup_launches": nw}
             log(f"config {name}: {op} {km:.3f} ms -> {gbs:.0f} GB/s")
         wb.free_wires()
         entry["latency_ms_per_request"] = wb.latency()
@@ -559,6 +568,22 @@ def stream_leg(K, torch, plan, info, dshards, sbt_d, sstride, cache, scales, bt_
     for h in extra:
         hip.hipStreamDestroy(h)
     return res
+
+
+def device_hbm_peak():
+    """The HBM peak the HIP runtime's device attributes imply: 2 transfers per
+    memory clock x bus width.  Context only; the roofline uses the published
+    8 TB/s."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    bus, clk = ctypes.c_int(0), ctypes.c_int(0)
+    # hipDeviceAttributeMemoryBusWidth (bits) = 59, hipDeviceAttributeMemoryClockRate (kHz) = 60
+    if hip.hipDeviceGetAttribute(ctypes.byref(bus), 59, 0) or \
+            hip.hipDeviceGetAttribute(ctypes.byref(clk), 60, 0):
+        return None
+    return {"bus_width_bits": bus.value, "memory_clock_khz": clk.value,
+            "GB/s": round(2 * clk.value * 1e3 * bus.value / 8 / 1e9, 1),
+            "formula": "2 x memory clock x bus width / 8"}
 
 
 CALIB_TOKENS_PER_GIB = 1 << 18   # 1 layer, 8 heads, dim 128, bf16: 2 x 8 x 256 B per token

@@ -60,6 +60,9 @@ def test_bench_prints_one_json_line():
     assert cfg_leg["repack"]["GB/s"] > 0 and cfg_leg["latency_ms_per_request"]["p50"] > 0
     assert out["latency_ms_per_request"]["p50"] > 0
     assert out["pack"]["GB/s"] > 0 and out["unpack"]["GB/s"] > 0
+    assert out["pack_unpack"]["GB/s"] > 0
+    peak = out["hbm_peak_from_device"]
+    assert peak is None or (peak["bus_width_bits"] > 0 and peak["GB/s"] > 0)
 
 
 def test_settle_counts_launches_until_the_time_has_passed():
