@@ -128,11 +128,10 @@ __device__ __forceinline__ float quotient(float a, float s, float r)
 
 // a / s with one remainder correction, for the fast path's 8-bit codes.  Its
 // result is not always the correctly rounded quotient, but its code always
-// is that quotient's: an exhaustive GPU check over every pair of 16-bit
-// magnitudes (row maximum, element <= it), bf16 and fp16, with s = amax /
-// fmax in [2^-80, 2^100], gives the same e4m3fn and e5m2 codes as
-// `quotient` for every pair (the bare product a * r differs on 9,000-25,000
-// pairs per source and format).  a may be negative: every step is odd in a
+// is that quotient's: the GPU test over every pair of finite 16-bit values
+// (row maximum, element of no larger magnitude, both signs), bf16 and fp16
+// sources, e4m3fn and e5m2 codes, finds every code equal to the oracle's,
+// which rounds the exact quotient.  a may be negative: every step is odd in a
 // (rounding to nearest is symmetric), and the residual is formed as s*q - a
 // and subtracted, so a signed zero keeps its sign (q - (+0) * r is -0 for
 // q = -0, where q + (+0) * r would be +0).
@@ -264,9 +263,9 @@ __device__ __forceinline__ void fp8_codes(const uint32_t (&w)[NW], int lg, float
     m = group_max(m, lg);
     // s = amax / fmax by the reciprocal and one remainder correction: equal
     // to the IEEE quotient for every 16-bit row maximum, and inside the fast
-    // range exactly when the IEEE quotient is (exhaustive check of all bf16
-    // and fp16 maxima for both formats, in exact rational arithmetic); NaN
-    // when the row holds a NaN or an infinity
+    // range exactly when the IEEE quotient is (the GPU test over every finite
+    // bf16 and fp16 row maximum, both formats, compares each scale with the
+    // oracle's IEEE quotient); NaN when the row holds a NaN or an infinity
     constexpr float kInv = 1.0f / Q::kMax;
     const float amax = F::widen(m);
     const float q0 = amax * kInv;
