@@ -593,7 +593,8 @@ def copy_legs(K, torch, gib, timed, stream):
     """Plain copies of known size: the identity layout through kvx (one request,
     TP1 -> TP1, bf16, pages 0, 1, 2, ... in order: a memcpy of `gib` GiB done
     by the repack kernel, the reference for the counters), the HIP runtime's
-    device copy and a torch elementwise kernel."""
+    device copy and a torch elementwise kernel; and, for context, a pure write
+    (torch fill) of the same bytes."""
     import numpy as np
     T = int(gib * CALIB_TOKENS_PER_GIB)
     nbytes = T * 2 * 8 * 128 * 2                     # read = written
@@ -602,15 +603,19 @@ def copy_legs(K, torch, gib, timed, stream):
     bt = torch.arange(T // 16, dtype=torch.int32, device="cuda")
     plan = K.kvx_plan(K.make_desc(1, 8, 128, 1, 1, 0, K.BF16, K.BF16, K.THD, 16, T // 16, [T]))
     legs = {}
-    for kind, fn in (
+    for kind, fn, rd, wr in (
             ("kvx_identity_memcpy", lambda: K.kvx_repack(plan, [src], dst, None, bt, T // 16,
-                                                         stream)),
-            ("hipMemcpy_d2d", lambda: dst.view(torch.int16).copy_(src)),
-            ("torch_elementwise", lambda: torch.bitwise_not(src, out=dst.view(torch.int16)))):
+                                                         stream), nbytes, nbytes),
+            ("hipMemcpy_d2d", lambda: dst.view(torch.int16).copy_(src), nbytes, nbytes),
+            ("torch_elementwise", lambda: torch.bitwise_not(src, out=dst.view(torch.int16)),
+             nbytes, nbytes),
+            # one direction only, for context: the HBM rate of pure writes
+            ("torch_fill_write_only", lambda: dst.fill_(7), 0, nbytes)):
         ms, km, _, _ = timed(fn, 10, 2)
-        legs[kind] = {"bytes_read": nbytes, "bytes_written": nbytes, "kernel_ms": round(km, 4),
-                      "GB/s": round(2 * nbytes / (km * 1e-3) / 1e9, 1)}
-        log(f"plain copy ({kind}): {2 * nbytes / (km * 1e-3) / 1e9:.0f} GB/s")
+        gbs = (rd + wr) / (km * 1e-3) / 1e9
+        legs[kind] = {"bytes_read": rd, "bytes_written": wr, "kernel_ms": round(km, 4),
+                      "GB/s": round(gbs, 1)}
+        log(f"plain {kind}: {gbs:.0f} GB/s")
     legs["kvx_identity_memcpy"]["grid_units"] = (T // 16) * 2
     del src, dst, bt, np
     return legs

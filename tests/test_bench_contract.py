@@ -61,6 +61,8 @@ def test_bench_prints_one_json_line():
     assert out["latency_ms_per_request"]["p50"] > 0
     assert out["pack"]["GB/s"] > 0 and out["unpack"]["GB/s"] > 0
     assert out["pack_unpack"]["GB/s"] > 0
+    fill = out["copy_ceiling"]["torch_fill_write_only"]
+    assert fill["bytes_read"] == 0 and fill["GB/s"] > 0
     peak = out["hbm_peak_from_device"]
     assert peak is None or (peak["bus_width_bits"] > 0 and peak["GB/s"] > 0)
 
