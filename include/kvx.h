@@ -61,6 +61,15 @@
  * stay alive until the stream reaches that point.  A plan is immutable and may
  * be used concurrently on several streams of its device.
  *
+ * Graphs: these calls (and kvx_repack_noalloc) launch kernels and nothing
+ * else: no allocation, copy, memset or synchronisation.  Called on a stream
+ * under HIP graph capture they are recorded, and each replay reads the
+ * sources, block tables and transfer tensor as they are at replay time.  The
+ * recorded kernels hold the plan's device table and the buffer addresses:
+ * the plan and the buffers must outlive the graph.  Make the first
+ * kvx_repack_noalloc call on a device outside capture (it looks the address
+ * of its static table up once per device).
+ *
  * Errors: every call returns a kvx_status; nothing is thrown and nothing
  * aborts.  kvx_last_error() gives a message for the calling thread's last
  * non-OK status.  A plan whose requests hold no tokens has nothing to move:
