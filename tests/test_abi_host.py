@@ -136,6 +136,25 @@ def test_plan_rejects(over, status):
     assert K.kvx_last_error()
 
 
+# The largest launch a plan accepts is 2^24 - 8 work units (units of one
+# (layer, k/v) plane, one page, one head segment and one workgroup pass).  With
+# one 16-byte row per one-token page, each page gives one unit per plane.
+UNIT_LIMIT_PAGES = (1 << 23) - 4
+
+
+def test_plan_work_unit_limit():
+    """Exactly 2^24 - 8 units plan; one page more is refused before anything
+    is allocated on a device."""
+    kw = dict(BASE, num_layers=1, num_kv_heads=1, head_dim=8, dst_tp=1, src_dtype=K.BF16,
+              dst_dtype=K.BF16, block_size=1, num_blocks=UNIT_LIMIT_PAGES + 1)
+    plan = K.kvx_plan(K.make_desc(**dict(kw, seq_lens=[UNIT_LIMIT_PAGES])))
+    assert K.kvx_plan_info_get(plan).num_items == UNIT_LIMIT_PAGES
+    del plan
+    with pytest.raises(K.KvxError) as e:
+        K.kvx_plan(K.make_desc(**dict(kw, seq_lens=[UNIT_LIMIT_PAGES + 1])))
+    assert e.value.status == K.EUNSUPPORTED and "work units" in str(e.value)
+
+
 def test_plan_accepts_empty_batches():
     """No tokens: nothing to move, the launch calls succeed without looking at
     any pointer (and launch nothing, so this is safe on any host)."""

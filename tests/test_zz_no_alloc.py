@@ -16,7 +16,7 @@ import torch
 
 import workload as W
 from cases import FULL, SMALL, SMALL_DEQUANT, inputs
-from gpu_util import DEV, desc_for, dev_u16, log, pool
+from gpu_util import DEV, desc_for, dev_u16, log, oracle_pool, pool
 
 import paper_2509_17542_amd as K
 
@@ -82,6 +82,24 @@ def test_noalloc_full_qwen_then_small():
     lens2, bt2, stride2, shards2 = inputs(small)
     log(f"noalloc then {small.name}: {int(lens2.sum())} tokens")
     _check(small, lens2, bt2, stride2, shards2)
+
+
+def test_noalloc_at_its_table_limit():
+    """256 requests and 65536 pages, the most the static table holds (one-token
+    pages of one 16-byte row), against the plan-based repack and the oracle;
+    then a smaller call."""
+    w = SMALL["llama3_8b_small"].replace(name="noalloc_limit", heads=1, head_dim=8,
+                                         block_size=1, num_blocks=65536, num_requests=256,
+                                         lens_override=(256,) * 256)
+    lens, bt, stride, shards = inputs(w)
+    assert int(lens.sum()) == 65536
+    log(f"noalloc at its limit: {len(lens)} requests, {int(lens.sum())} pages")
+    (rc, _), (gc, _) = _both(w, lens, bt, stride, shards)
+    assert torch.equal(rc, gc), "cache differs from kvx_repack"
+    want, _ = oracle_pool(w, lens, bt, stride, shards)
+    assert np.array_equal(gc.cpu().numpy(), want), "cache differs from the oracle"
+    small = SMALL["llama3_8b_small"]
+    _check(small, *inputs(small))
 
 
 def test_noalloc_rejects_beyond_its_table():
