@@ -2,15 +2,18 @@
 (source buffers holding a prefill stage's layers, caches holding a decode
 stage's layers) against the oracle, byte for byte.
 
-Small cases compose every (source stage, decode stage) pair and compare
-whole decode-stage pools with the oracle's whole-model pool; the full-size
+Small cases compose every (source stage, decode stage) pair, through the
+repack, through pack then unpack, or through the layer-streamed pipe (whose
+chunks shift within the stage's layers), and compare whole decode-stage
+pools with the oracle's whole-model pool; the full-size
 case converts the Llama-3-8B workload from two prefill stages of 16 layers
 into one decode cache and is checked on sampled requests and planes."""
 import numpy as np
 import pytest
 import torch
 
-from cases import FP8_NAMES, FULL, SMALL, SMALL_PAGED, dst_size, oracle_problem, read_shards
+from cases import (FP8_NAMES, FULL, SMALL, SMALL_DEQUANT, SMALL_PAGED, dst_size,
+                   oracle_problem, read_shards)
 from gpu_util import DEV, check_sampled, check_unused_pages, desc_for, dev_u16, log
 
 import oracle as O
@@ -46,10 +49,11 @@ def _stage_desc(w, lens, conv0, nconv, src_stage, dst_stage):
     return d
 
 
-def _run_stage(w, lens, bt_d, stride, dshards, sbt_d, sstride, desc, cache, scales, via_wire):
-    """One stage plan: repack, or pack then unpack.  Host-side shape checks
-    first: the shards hold the source stage's layers, the cache the decode
-    stage's layers."""
+def _run_stage(w, lens, bt_d, stride, dshards, sbt_d, sstride, desc, cache, scales, how):
+    """One stage plan: repack ("repack"), pack then unpack ("wire"), or the
+    layer-streamed pipe in chunks of n layers over 2 slots ("pipeN").
+    Host-side shape checks first: the shards hold the source stage's layers,
+    the cache the decode stage's layers."""
     Hs, D = w.hs, w.head_dim
     if w.src_order == "paged":
         need = desc.src_layers * 2 * w.src_num_blocks * w.src_block_size * Hs * D
@@ -61,7 +65,13 @@ def _run_stage(w, lens, bt_d, stride, dshards, sbt_d, sstride, desc, cache, scal
     assert cache.numel() == rows * D * dst_size(w)
     assert scales is None or scales.numel() == rows
     plan = K.kvx_plan(desc)
-    if via_wire:
+    if how.startswith("pipe"):
+        # chunks of the stage's converted layers (at most all of them); the
+        # last may be shorter
+        pipe = K.kvx_pipe_create(plan, min(int(how[4:]), desc.num_layers), 2)
+        K.kvx_pipe_run(pipe, dshards, sbt_d, sstride, cache, scales, bt_d, stride)
+        K.kvx_pipe_destroy(pipe)  # waits for the pipe's streams
+    elif how == "wire":
         info = K.kvx_plan_info_get(plan)
         wire = torch.empty(max(int(info.wire_bytes), 16), dtype=torch.uint8, device=DEV)
         if sbt_d is not None:
@@ -75,18 +85,27 @@ def _run_stage(w, lens, bt_d, stride, dshards, sbt_d, sstride, desc, cache, scal
         K.kvx_repack(plan, dshards, cache, scales, bt_d, stride)
 
 
-CASES = [("llama3_8b_small", 6, (3, 3), (2, 2, 2), False), ("fp8_small", 5, (1, 4), (2, 3), True),
-         ("llama3_70b_small_r1", 4, (4,), (1, 1, 2), False), ("qwen_htd_small", 5, (2, 1, 2), (5,), True),
-         ("paged16_tp4to2_bs32_small", 4, (2, 2), (3, 1), False),
-         ("paged16_e4m3_bs24", 3, (1, 2), (3,), True)]
+CASES = [("llama3_8b_small", 6, (3, 3), (2, 2, 2), "repack"),
+         ("fp8_small", 5, (1, 4), (2, 3), "wire"),
+         ("llama3_70b_small_r1", 4, (4,), (1, 1, 2), "repack"),
+         ("qwen_htd_small", 5, (2, 1, 2), (5,), "wire"),
+         ("paged16_tp4to2_bs32_small", 4, (2, 2), (3, 1), "repack"),
+         ("paged16_e4m3_bs24", 3, (1, 2), (3,), "wire"),
+         # the layer-streamed pipe over stage plans: chunks shifted within a
+         # stage's layers, chunk sizes that do not divide them
+         ("llama3_8b_small", 6, (3, 3), (2, 4), "pipe1"),
+         ("fp8_small", 5, (1, 4), (2, 3), "pipe2"),
+         ("llama3_70b_small_r1", 7, (4, 3), (7,), "pipe3"),
+         ("paged16_tp4to2_bs32_small", 5, (2, 3), (4, 1), "pipe2"),
+         ("dequant_bf16_e4m3_bf16", 6, (6,), (3, 3), "pipe2")]
 
 
-@pytest.mark.parametrize("name,L,src_sizes,dst_sizes,via_wire", CASES)
-def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
-    w = (SMALL | SMALL_PAGED)[name].replace(layers=L, total_layers=L)
+@pytest.mark.parametrize("name,L,src_sizes,dst_sizes,how", CASES)
+def test_stage_plans_small(name, L, src_sizes, dst_sizes, how):
+    w = (SMALL | SMALL_PAGED | SMALL_DEQUANT)[name].replace(layers=L, total_layers=L)
     lens = W.seq_lens(w)
     bt, stride = W.block_table(w, lens)
-    log(f"stages {name}: prefill {src_sizes} -> decode {dst_sizes}")
+    log(f"stages {name}: prefill {src_sizes} -> decode {dst_sizes}, {how}")
     whole = oracle_problem(O, w, lens, L)
     want_c = np.full(O.cache_bytes(whole), W.SENTINEL, dtype=np.uint8)
     want_s = None
@@ -115,7 +134,7 @@ def test_stage_plans_small(name, L, src_sizes, dst_sizes, via_wire):
             if lo < hi:
                 desc = _stage_desc(w, lens, lo, hi - lo, (s0, sn), (d0, dn))
                 _run_stage(w, lens, bt_d, stride, dsh, sbt_d, sstride, desc, cache, scales,
-                           via_wire)
+                           how)
         torch.cuda.synchronize()
         got_c.append(cache.cpu().numpy())
         if scales is not None:
@@ -139,7 +158,7 @@ def test_full_llama3_8b_two_prefill_stages():
         log(f"full 8B: prefill stage layers {s0}..{s0 + 15}")
         dsh = [dev_u16(s) for s in W.source_shards(w, lens, s0, 16)]
         desc = _stage_desc(w, lens, s0, 16, (s0, 16), (0, 32))
-        _run_stage(w, lens, bt_d, stride, dsh, None, 0, desc, cache, None, False)
+        _run_stage(w, lens, bt_d, stride, dsh, None, 0, desc, cache, None, "repack")
         torch.cuda.synchronize()
         del dsh
     shards = W.source_shards(w, lens, 0, w.layers)
