@@ -6,7 +6,9 @@ smaller problem (fewer requests and tokens), so the second reads a static
 work-item table that still holds the first call's longer contents.  Cases
 cover token- and head-major sources, a TP merge (two head segments), an fp8
 cache with scales, a quantise-dequantise cache, and the Qwen-7B workload at
-full size (32 requests, 486 pages).
+full size (32 requests, 486 pages).  Also: the call at its table's limit, a
+pipeline-stage descriptor, and the random descriptors with token- or
+head-major sources against the oracle.
 """
 from __future__ import annotations
 
@@ -15,7 +17,7 @@ import pytest
 import torch
 
 import workload as W
-from cases import FULL, SMALL, SMALL_DEQUANT, inputs
+from cases import FULL, RANDOM, SMALL, SMALL_DEQUANT, inputs, out_of_pool
 from gpu_util import DEV, desc_for, dev_u16, log, oracle_pool, pool
 
 import paper_2509_17542_amd as K
@@ -100,6 +102,50 @@ def test_noalloc_at_its_table_limit():
     assert np.array_equal(gc.cpu().numpy(), want), "cache differs from the oracle"
     small = SMALL["llama3_8b_small"]
     _check(small, *inputs(small))
+
+
+def test_noalloc_stage_plan():
+    """A pipeline-stage descriptor: the source buffers hold prefill layers
+    1-3, the cache decode layers 2-4 of a 5-layer model, and the two common
+    layers are converted (layer offsets on both sides)."""
+    w = SMALL["llama3_8b_small"].replace(layers=5, total_layers=5)
+    lens = W.seq_lens(w)
+    bt, stride = W.block_table(w, lens)
+    shards = W.source_shards(w, lens, 1, 3)
+    desc = desc_for(w, lens, 2)
+    desc.src_layer_offset, desc.src_layers = 1, 3
+    desc.dst_layer_offset, desc.dst_layers = 0, 3
+    dsh = [dev_u16(x) for x in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    ref_c, _ = pool(w, 3)
+    K.kvx_repack(K.kvx_plan(desc), dsh, ref_c, None, bt_d, stride)
+    got_c, _ = pool(w, 3)
+    log("noalloc stage plan: prefill layers 1-3 -> decode layers 2-4")
+    K.kvx_repack_noalloc(desc, dsh, got_c, None, bt_d, stride)
+    torch.cuda.synchronize()
+    assert torch.equal(ref_c, got_c)
+    assert not torch.equal(got_c, pool(w, 3)[0]), "nothing was written"
+
+
+@pytest.mark.parametrize("name", [n for n, w in RANDOM.items() if w.src_order != "paged"])
+def test_noalloc_random_descriptor(name):
+    """The random descriptors with token- or head-major sources (replicated
+    heads, page sizes that are not powers of two, empty requests, about 10% of
+    the block-table entries outside the pool) against the oracle."""
+    w = RANDOM[name]
+    lens, bt, stride, shards = inputs(w)
+    bt = out_of_pool(bt, w.num_blocks, np.random.default_rng(int(name[4:])))
+    log(f"noalloc {name}: TP {w.src_tp}->{w.dst_tp} {w.src_dtype}->{w.dst_dtype} "
+        f"{w.src_order} bs={w.block_size} lens={list(lens)}")
+    dsh = [dev_u16(x) for x in shards]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    cache, scales = pool(w, w.layers)
+    K.kvx_repack_noalloc(desc_for(w, lens), dsh, cache, scales, bt_d, stride)
+    torch.cuda.synchronize()
+    want_c, want_s = oracle_pool(w, lens, bt, stride, shards)
+    assert np.array_equal(cache.cpu().numpy(), want_c)
+    if want_s is not None:
+        assert np.array_equal(scales.view(torch.uint8).cpu().numpy(), want_s.view(np.uint8))
 
 
 def test_noalloc_rejects_beyond_its_table():
