@@ -49,8 +49,11 @@
  * pages not in a block-table row, transfer-tensor padding) are never written.
  * A page id outside its pool names no page: a decode page id outside
  * [0, num_blocks) writes nothing, and a row whose source page id lies outside
- * [0, src_num_blocks) is written neither to the cache nor to the transfer
- * tensor (nor its scale).
+ * [0, src_num_blocks) is written neither to the cache (repack) nor to the
+ * transfer tensor or its scale (pack).  kvx_unpack cannot see source page
+ * ids: it copies whatever the transfer tensor holds at such a row, so after
+ * a pack, an unpack (and the layer-streamed pipe) writes those rows with the
+ * transfer tensor's earlier contents.
  *
  * Ownership: every buffer is caller-owned device memory; the library never
  * allocates or frees it.  A plan is library-owned: kvx_plan copies seq_lens
@@ -322,7 +325,8 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * (host to device) and unpacked into the cache, each stage on a stream of the
  * pipe.  With `slots` slots, chunk c + 1 is packed and chunk c - 1 unpacked
  * while chunk c crosses the bus.  The cache and scales written equal
- * kvx_pack followed by kvx_unpack of the whole plan.
+ * kvx_pack followed by kvx_unpack of the whole plan (rows whose source page
+ * id is outside the source pool take whatever their ring slot held).
  *
  * kvx_pipe_create allocates the pinned host ring (slots x the largest
  * chunk's transfer-tensor bytes, hipHostMalloc with hipHostMallocMapped),
