@@ -335,7 +335,9 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * default priority): the pack's covers half the device's CUs, the copy's and
  * the unpack's a quarter each, so that no stage waits for CUs another holds;
  * like streams created without flags, they synchronise with the null stream.
- * The plan must outlive the pipe.  KVX_EINVAL for a NULL plan or out,
+ * The plan must outlive the pipe.  A plan with no tokens gets a pipe that
+ * allocates nothing and whose runs return KVX_OK at once (on any host).
+ * KVX_EINVAL for a NULL plan or out,
  * chunk_layers outside [1, num_layers] or slots < 1; KVX_EDEVICE for a
  * host-only plan or when the streams cannot be created; KVX_ENOMEM if an
  * allocation fails.

@@ -142,6 +142,19 @@ kvx_status kvx_pipe_create(const kvx_plan_t* p, int32_t chunk_layers, int32_t sl
     if (chunk_layers < 1 || chunk_layers > L)
         return fail(KVX_EINVAL, "chunk_layers %d outside [1, %d]", chunk_layers, L);
     if (slots < 1) return fail(KVX_EINVAL, "slots must be >= 1");
+    if (p->items.empty()) {
+        // no tokens: nothing to move, as for the plan's own launches; the pipe
+        // holds no buffers, streams or events, and its runs return at once
+        kvx_pipe_s* q = new (std::nothrow) kvx_pipe_s();
+        if (!q) return fail(KVX_ENOMEM, "host allocation failed");
+        q->plan = p;
+        q->chunk_layers = chunk_layers;
+        q->num_chunks = (L + chunk_layers - 1) / chunk_layers;
+        q->slots = slots;
+        q->device = p->device;
+        *out = q;
+        return KVX_OK;
+    }
     if (p->device < 0) return fail(KVX_EDEVICE, "plan has no device tables (no HIP device)");
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != p->device)

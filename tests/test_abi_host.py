@@ -335,6 +335,18 @@ def test_pipe_create_errors_on_the_host():
         assert e.value.status == K.EDEVICE
 
 
+def test_pipe_of_a_plan_without_tokens():
+    """No tokens: the pipe allocates nothing and its run returns at once, on
+    any host (a device is not needed), like the plan's own launches."""
+    for lens in ([], [0, 0]):
+        plan = K.kvx_plan(K.make_desc(**dict(BASE, seq_lens=lens)))
+        pipe = K.kvx_pipe_create(plan, 1, 3)
+        info = K.kvx_pipe_info_get(pipe)
+        assert (info.num_chunks, info.slots, info.host_bytes, info.bus_bytes) == (2, 3, 0, 0)
+        assert K._lib.kvx_pipe_run(pipe, None, None, 0, None, None, None, 0, None) == K.OK
+        K.kvx_pipe_destroy(pipe)
+
+
 def test_buffer_size_queries_reject_bad_arguments():
     plan = K.kvx_plan(desc_for(SMALL["tiny"], W.seq_lens(SMALL["tiny"])))
     for j in (-1, SMALL["tiny"].src_tp):
