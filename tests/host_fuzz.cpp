@@ -86,7 +86,16 @@ int main()
         if (d.src_order == KVX_PAGED)
             kvx_check_src_block_table(p, bt.data(), info.max_src_blocks_per_request);
         kvx_pipe_t* q = nullptr;
-        kvx_pipe_create(p, 1, 2, &q);   // host-only plan: EDEVICE
+        // host-only plan: EDEVICE, unless it has no tokens (a pipe that moves
+        // nothing, whose run returns at once)
+        if (kvx_pipe_create(p, 1, 2, &q) == KVX_OK) {
+            if (kvx_pipe_run(q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr) !=
+                KVX_OK) {
+                std::printf("pipe of a plan without tokens failed to run\n");
+                return 1;
+            }
+            kvx_pipe_destroy(q);
+        }
         kvx_plan_destroy(p);
     }
     // mostly valid problems: every head map, order, dtype and layer range
