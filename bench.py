@@ -7,9 +7,11 @@ Llama-3-8B-shaped KV of 16 requests, 32 layers x 8 KV heads x 128 dims, bf16,
 into 16-token pages of a 65536-page pool), with the inputs already resident in
 HBM.  Prints one JSON line on stdout: throughput in GB/s of algorithmic bytes
 (read + written), the HBM roofline of the kernel (HIP-event kernel time on
-the launch stream), pack and unpack alone, per-request latency, and the CPU
-oracle timed on a bounded sample of the same workload.  Progress goes to
-stderr.
+the launch stream), pack, unpack and pack-then-unpack, per-request latency,
+plain copies of known size beside it, the layer-streamed transfer through
+pinned host memory, the P:D planner, every named workload in turn
+(`configs`), and the CPU oracle timed on a bounded sample of the headline
+workload.  Progress goes to stderr.
 """
 from __future__ import annotations
 
