@@ -184,3 +184,32 @@ def test_pipe_runs_back_to_back(kind):
     for c in pools:
         assert np.array_equal(c.cpu().numpy(), want_c)
     del pipe
+
+
+def test_two_pipes_run_at_once():
+    """Two pipes of one plan, each with its own ring, run on two created
+    streams at the same time (runs of different pipes may overlap), with
+    their own sources and pools; each pool holds its own whole result.  Three
+    chunks over two slots in each pipe."""
+    w = SMALL["fp8_small"].replace(layers=3, total_layers=3)
+    lens, bt, stride, shards = inputs(w)
+    variants = [shards, [None if s is None else np.roll(s, 37) for s in shards]]
+    plan = K.kvx_plan(desc_for(w, lens))
+    pipes = [K.kvx_pipe_create(plan, 1, 2) for _ in variants]
+    dsh = [[dev_u16(s) for s in v] for v in variants]
+    bt_d = torch.from_numpy(np.ascontiguousarray(bt, dtype=np.int32)).to(DEV)
+    for d in dsh:
+        check_shapes(w, lens, bt, stride, d, w.layers)
+    pools = [pool(w, w.layers) for _ in variants]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in variants]
+    log("two pipes at once on two streams")
+    for _ in range(2):
+        for p, d, (c, s), st in zip(pipes, dsh, pools, streams):
+            K.kvx_pipe_run(p, d, None, 0, c, s, bt_d, stride, st)
+    torch.cuda.synchronize()
+    for v, (c, s) in zip(variants, pools):
+        want_c, want_s = oracle_pool(w, lens, bt, stride, v)
+        assert np.array_equal(c.cpu().numpy(), want_c)
+        assert np.array_equal(s.view(torch.uint8).cpu().numpy(), want_s.view(np.uint8))
+    del pipes
