@@ -173,6 +173,21 @@ def test_plan_accepts_empty_batches():
         K.kvx_unpack(paged, None, None, None, None, 0)
 
 
+def test_plan_copies_seq_lens():
+    """The plan keeps its own copy of the lengths: overwriting the caller's
+    array afterwards changes neither its sizes nor its transfer-tensor
+    segments."""
+    d = K.make_desc(**BASE)
+    plan = K.kvx_plan(d)
+    before = K.kvx_plan_info_get(plan)
+    segs = [K.kvx_plan_segment(plan, r) for r in range(2)]
+    d._lens[0], d._lens[1] = 4000, 1
+    after = K.kvx_plan_info_get(plan)
+    assert (after.total_tokens, after.wire_bytes, after.num_items) == \
+        (before.total_tokens, before.wire_bytes, before.num_items) == (47, before.wire_bytes, 4)
+    assert [K.kvx_plan_segment(plan, r) for r in range(2)] == segs
+
+
 def test_segment_out_of_range():
     plan = K.kvx_plan(K.make_desc(**BASE))
     with pytest.raises(K.KvxError) as e:
