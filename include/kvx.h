@@ -60,9 +60,10 @@
  * and allocates a small device table on the device current at that time.
  *
  * Streams: kvx_pack / kvx_unpack / kvx_repack (and the _paged forms) only
- * enqueue work on the given hipStream_t (passed as void*, NULL = default stream) and return; buffers must
- * stay alive until the stream reaches that point.  A plan is immutable and may
- * be used concurrently on several streams of its device.
+ * enqueue work on the given hipStream_t (passed as void*, NULL = default
+ * stream) and return; buffers must stay alive until the stream reaches that
+ * point.  A plan is immutable and may be used concurrently on several streams
+ * of its device, from several host threads.
  *
  * Graphs: these calls (and kvx_repack_noalloc) launch kernels and nothing
  * else: no allocation, copy, memset or synchronisation.  Called on a stream
@@ -94,7 +95,7 @@ typedef enum {
     KVX_OK = 0,
     KVX_EINVAL = -1,       /* invalid argument, shape or pointer */
     KVX_EUNSUPPORTED = -2, /* valid request this library does not implement */
-    KVX_ENOMEM = -3,       /* host or device allocation failed (kvx_plan only) */
+    KVX_ENOMEM = -3,       /* host or device allocation failed (kvx_plan, kvx_pipe_create) */
     KVX_EDEVICE = -4       /* no usable device for the plan, or a HIP error */
 } kvx_status;
 
@@ -170,8 +171,8 @@ typedef struct {
  * the current HIP device when one is usable; otherwise the plan is host-only
  * and the launch calls return KVX_EDEVICE).
  * Returns KVX_EINVAL for: NULL desc/out; a dimension <= 0; a TP degree that
- * neither divides H nor is a multiple of it; dst_rank outside [0, dst_tp); block_size <= 0;
- * num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
+ * neither divides H nor is a multiple of it; dst_rank outside [0, dst_tp);
+ * block_size <= 0; num_blocks <= 0; num_requests < 0; NULL seq_lens with requests; T_r < 0;
  * an unknown order; for KVX_PAGED, src_block_size <= 0 or src_num_blocks <= 0;
  * a negative layer offset or count, or converted layers outside either side's
  * src_layers / dst_layers;
@@ -180,12 +181,15 @@ typedef struct {
  * KVX_EUNSUPPORTED for: a dtype pair outside {fp16->fp16, bf16->bf16,
  * fp16->bf16, bf16->fp16, fp16/bf16->e4m3fn, fp16/bf16->e5m2}; a cache_dtype
  * other than dst_dtype unless dst_dtype is 8-bit and cache_dtype 16-bit; a
- * transfer-tensor row (head_dim
- * * dst element size) above 1024 bytes; more than 1024 heads per decode rank; more than
- * 65535 source heads per shard; 2*L > 65535; more than 2^24-1 logical pages
- * (sum over requests of ceil(T_r / block_size)); a decode cache, source
- * shard or transfer tensor of 2^62 bytes or more.  KVX_ENOMEM / KVX_EDEVICE if
- * the table cannot be allocated. */
+ * transfer-tensor row (head_dim * dst element size) above 1024 bytes; more
+ * than 1024 heads per decode rank; more than 65535 source heads per shard; a
+ * decode rank whose heads form more than 64 head segments (runs of heads
+ * from one source shard); 2*L > 65535; more than 2^24 - 8 work units in one
+ * launch (logical pages, the sum over requests of ceil(T_r / block_size),
+ * x 2L planes x head segments x workgroup passes per page; so at most
+ * 2^23 - 4 pages); a decode cache, source shard or transfer tensor of 2^62
+ * bytes or more.  KVX_ENOMEM / KVX_EDEVICE if the table cannot be
+ * allocated. */
 kvx_status kvx_plan(const kvx_desc *desc, kvx_plan_t **out);
 
 kvx_status kvx_plan_info_get(const kvx_plan_t *plan, kvx_plan_info *info);
