@@ -126,6 +126,9 @@ BASE = dict(num_layers=2, num_kv_heads=8, head_dim=64, src_tp=1, dst_tp=2, dst_r
     (dict(dst_dtype=3, cache_dtype=4), K.EUNSUPPORTED),
     (dict(src_dtype=4, dst_dtype=4), K.EUNSUPPORTED),    # an 8-bit source
     (dict(dst_dtype=5), K.EINVAL),
+    # 128 one-head prefill shards merged into one decode rank: 128 head
+    # segments, above the 64 a launch carries (64 are accepted)
+    (dict(num_kv_heads=128, head_dim=16, src_tp=128, dst_tp=1), K.EUNSUPPORTED),
 ])
 def test_plan_rejects(over, status):
     kw = dict(BASE)
@@ -153,6 +156,12 @@ def test_plan_work_unit_limit():
     with pytest.raises(K.KvxError) as e:
         K.kvx_plan(K.make_desc(**dict(kw, seq_lens=[UNIT_LIMIT_PAGES + 1])))
     assert e.value.status == K.EUNSUPPORTED and "work units" in str(e.value)
+
+
+def test_plan_accepts_64_head_segments():
+    plan = K.kvx_plan(K.make_desc(**dict(BASE, num_kv_heads=64, head_dim=16, src_tp=64,
+                                         dst_tp=1)))
+    assert K.kvx_plan_segment(plan, 0)[0] == 0
 
 
 def test_plan_accepts_empty_batches():
