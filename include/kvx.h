@@ -341,10 +341,9 @@ kvx_status kvx_check_src_block_table(const kvx_plan_t *plan, const int32_t *host
  * like streams created without flags, they synchronise with the null stream.
  * The plan must outlive the pipe.  A plan with no tokens gets a pipe that
  * allocates nothing and whose runs return KVX_OK at once (on any host).
- * KVX_EINVAL for a NULL plan or out,
- * chunk_layers outside [1, num_layers] or slots < 1; KVX_EDEVICE for a
- * host-only plan or when the streams cannot be created; KVX_ENOMEM if an
- * allocation fails.
+ * KVX_EINVAL for a NULL plan or out, chunk_layers outside [1, num_layers] or
+ * slots < 1; KVX_EDEVICE for a host-only plan with tokens or when the
+ * streams cannot be created; KVX_ENOMEM if an allocation fails.
  *
  * kvx_pipe_run enqueues the whole transfer and returns: the pipe's streams
  * start after the caller's stream's earlier work and after the pipe's
