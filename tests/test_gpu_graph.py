@@ -139,6 +139,8 @@ PACK_UNPACK = {
     "llama3_70b_small_r1": SMALL["llama3_70b_small_r1"],
     "fp8_small": SMALL["fp8_small"],
     "paged16_bs64_small": SMALL_PAGED["paged16_bs64_small"],
+    "dequant_fp16_e4m3_fp16_htd": SMALL_DEQUANT["dequant_fp16_e4m3_fp16_htd"],
+    "e5m2_fp16_htd_tp2to4": SMALL_E5M2["e5m2_fp16_htd_tp2to4"],
 }
 
 
