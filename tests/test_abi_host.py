@@ -197,6 +197,35 @@ def test_plan_copies_seq_lens():
     assert [K.kvx_plan_segment(plan, r) for r in range(2)] == segs
 
 
+def test_plans_and_errors_from_several_threads():
+    """Plans built and refused from 8 host threads at once: each thread gets
+    its own plan sizes and its own last-error message (kept per thread)."""
+    import threading
+    results, errors = {}, []
+    start = threading.Barrier(8)
+
+    def work(k):
+        try:
+            start.wait()
+            for _ in range(50):
+                plan = K.kvx_plan(K.make_desc(**dict(BASE, seq_lens=[40 + k, 7])))
+                assert K.kvx_plan_info_get(plan).total_tokens == 47 + k
+                st = K._lib.kvx_plan(ctypes.byref(K.make_desc(**dict(BASE, dst_rank=2 + k))),
+                                     ctypes.byref(K._vp()))
+                assert st == K.EINVAL and f"dst_rank {2 + k} outside" in K.kvx_last_error()
+            results[k] = True
+        except Exception as e:  # reported by the main thread
+            errors.append((k, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(8)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    assert len(results) == 8
+
+
 def test_segment_out_of_range():
     plan = K.kvx_plan(K.make_desc(**BASE))
     with pytest.raises(K.KvxError) as e:
